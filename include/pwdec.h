@@ -1,0 +1,153 @@
+/*
+ * pwdec.h - C ABI of the MI355X parallel-window neural decoder.
+ *
+ * The library decodes many independent decoding windows of a distance-d rotated surface
+ * code in parallel. Each window takes the syndromes of its rounds and outputs one logit
+ * and one correction bit for its core region (Sec. 3.1; Algorithm 1, inference branch,
+ * with the input of shape batch x rounds x stabilizers). The per-window bits of a memory
+ * experiment combine by XOR into the global logical correction (eq. global_xor).
+ *
+ * Conventions shared by every entry point:
+ *  - Every function returns PWD_OK (0) on success or a negative pwd_status. No C++
+ *    exception crosses the ABI. On failure decoder_last_error() describes the cause.
+ *  - Pointers named d_* are device pointers (HIP global memory of the decoder's device);
+ *    the caller owns and allocates them. Host pointers are read during the call only.
+ *  - hip_stream is a hipStream_t (NULL = the default stream). Device work is enqueued on
+ *    it and the call returns without synchronising; results are valid once the stream
+ *    has been synchronised. A handle holds scratch memory sized for max_windows, so one
+ *    handle must not run on two streams at once.
+ *  - Stabilizer bits are packed LSB-first into uint32 words: the bit of stabilizer s is
+ *    bit (s % 32) of word (s / 32); words = ceil((d*d-1)/32). Input bits at positions
+ *    >= d*d-1 are ignored; output bits there are written as 0.
+ *  - Stabilizer (token) order: the d*d-1 stabilizers of the rotated surface code in
+ *    row-major order of their cell (r, c) on the (d+1)x(d+1) lattice (App. A.1.2). A
+ *    stabilizer at (r, c) acts on data qubits (r-1..r, c-1..c) inside the d x d patch;
+ *    interior cells 1 <= r, c <= d-1 are weight 4, top/bottom edge cells are kept when
+ *    r+c is even, left/right edge cells when r+c is odd.
+ */
+#ifndef PWDEC_H
+#define PWDEC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct pwd_decoder pwd_decoder; /* opaque handle */
+
+/* Window geometry (Sec. 3.1, App. A.1.1). A window has window_rounds rounds: a left
+ * buffer of floor((window_rounds - distance) / 2) rounds, a core of `distance` rounds and
+ * a right buffer of the rest. distance: odd, 3..25. window_rounds: distance..3*distance.
+ * max_windows: the largest batch decode_windows will be given (scratch is sized for it). */
+typedef struct {
+    int32_t distance;
+    int32_t window_rounds;
+    int32_t max_windows;
+} pwd_geometry;
+
+/* Network dimensions (App. A model table): d_model, layers, heads, MLP expansion and the
+ * arithmetic type. PWD_DTYPE_BF16: bf16 weights and matrix operands, fp32 accumulation,
+ * softmax, LayerNorm, residual stream and recurrent state. PWD_DTYPE_F32: fp32 throughout. */
+typedef struct {
+    int32_t d_model;
+    int32_t n_layers;
+    int32_t n_heads;
+    int32_t mlp_ratio;
+    int32_t dtype;
+} pwd_model_dims;
+
+enum { PWD_DTYPE_F32 = 0, PWD_DTYPE_BF16 = 1 };
+
+/* Window types (App. A.1.1): the initial window has zero padding in place of its left
+ * buffer, the final window in place of its right buffer. */
+enum { PWD_WIN_INITIAL = 0, PWD_WIN_BULK = 1, PWD_WIN_FINAL = 2 };
+
+typedef enum {
+    PWD_OK = 0,
+    PWD_EINVAL = -1,       /* null pointer, negative size or malformed argument */
+    PWD_EUNSUPPORTED = -2, /* geometry or dimensions outside the supported range */
+    PWD_EBLOB = -3,        /* weight blob: bad magic, version, size or header mismatch */
+    PWD_ENOMEM = -4,       /* device or host allocation failed */
+    PWD_EHIP = -5,         /* a HIP runtime call failed (message in decoder_last_error) */
+    PWD_EBATCH = -6,       /* n_windows > max_windows */
+    PWD_EDEVICE = -7       /* a device-side check fired (an invalid window type) */
+} pwd_status;
+
+/* Weight blob, version 1. All fields little-endian.
+ *   header: 16 x 32-bit words
+ *     [0] magic 0x31445750 ("PWD1")  [1] version = 1
+ *     [2] distance  [3] window_rounds  [4] d_model  [5] n_layers  [6] n_heads
+ *     [7] mlp hidden size F = mlp_ratio * d_model  [8] dtype
+ *     [9] fold constant kappa (float32 bits; App. A.2 uses 0.707)
+ *     [10] LayerNorm epsilon (float32 bits)  [11..15] zero
+ *   then float32 tensors, row-major, matrices stored [in][out] (y = x W + b):
+ *     w_e[D], b_e[D]                                    StabilizerEmbedder Linear(1 -> D)
+ *     per layer: Wq[D][D] bq[D] Wk[D][D] bk[D] Wv[D][D] bv[D] Wo[D][D] bo[D]
+ *                g1[D] be1[D] W1[D][F] b1[F] W2[F][D] b2[D] g2[D] be2[D]
+ *     Wc[2][2][D][D] bc[D]                              readout 2x2 convolution
+ *     w_o[d][D] b_o[1]                                  readout Linear(d*D -> 1)
+ *     beta[3]                                           logit bias per window type
+ * For PWD_DTYPE_BF16 the values are used rounded to bf16 (they should already be
+ * bf16-representable). The positional encoding is not stored: the library computes it. */
+#define PWD_BLOB_MAGIC 0x31445750u
+#define PWD_BLOB_VERSION 1
+#define PWD_BLOB_HEADER_WORDS 16
+
+/* Number of float32 values that follow the blob header for these dimensions. */
+size_t decoder_blob_floats(const pwd_geometry* geom, const pwd_model_dims* dims);
+
+/* Checks geometry and dimensions on the host only; touches no device.
+ * Supported: distance odd in 3..25; distance <= window_rounds <= 3*distance;
+ * 1 <= max_windows <= 2^24; mlp_ratio = 4; n_layers 1..8;
+ * PWD_DTYPE_BF16: d_model in {128, 256}, head size d_model/n_heads in {16, 32};
+ * PWD_DTYPE_F32: d_model in {16, 32, 64}, head size in {4, 8, 16, 32} and
+ * (d*d-1) * (3*d_model + 4*d_model) * 4 bytes within the on-chip budget (about d <= 5 at
+ * d_model 64). Returns PWD_OK, PWD_EINVAL (null) or PWD_EUNSUPPORTED. */
+int decoder_validate_config(const pwd_geometry* geom, const pwd_model_dims* dims);
+
+/* Creates a decoder on the current HIP device: validates, parses the blob (blob_bytes
+ * must equal 64 + 4 * decoder_blob_floats), rearranges the weights into the kernels'
+ * layouts, uploads them and allocates scratch for max_windows windows. The caller may
+ * free weight_blob on return. *out is set only on success. */
+int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims,
+                   const void* weight_blob, size_t blob_bytes, pwd_decoder** out);
+
+/* Decodes n_windows windows (Algorithm 1, inference branch, then the readout of App. A.3).
+ *   d_meas:   uint32 [n_windows][window_rounds + 1][words] stabilizer measurements; row 0
+ *             is the round just before the window's first round. Detection events are
+ *             E[t] = M[t+1] xor M[t]; an initial window zeroes E[t] for t < left buffer
+ *             and compares its first core round with the all-zero state; a final window
+ *             zeroes E[t] from the end of its core on.
+ *   d_types:  uint8 [n_windows], each PWD_WIN_INITIAL / BULK / FINAL.
+ *   d_logits: float [n_windows] out; d_bits: uint8 [n_windows] out, 1 iff logit > 0.
+ * n_windows = 0 is a no-op. A window with type > 2 gets logit NaN, bit 0, and makes the
+ * next decoder_sync_status return PWD_EDEVICE. Results do not depend on the batch size
+ * or on a window's position in the batch. */
+int decode_windows(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_types,
+                   int64_t n_windows, float* d_logits, uint8_t* d_bits, void* hip_stream);
+
+/* Writes the detection events the decoder feeds to its network:
+ * d_events uint32 [n_windows][window_rounds][words], packed as the input. Same masks and
+ * type check as decode_windows (an invalid type yields all-zero events). */
+int decoder_detection_events(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_types,
+                             int64_t n_windows, uint32_t* d_events, void* hip_stream);
+
+/* Synchronises hip_stream, then reports PWD_EDEVICE if a device-side check fired since
+ * the previous call (and clears it), PWD_EHIP on a stream error, else PWD_OK. */
+int decoder_sync_status(pwd_decoder* dec, void* hip_stream);
+
+/* Message of the last failure on the calling thread ("" if none). Valid until the next
+ * call on this thread. */
+const char* decoder_last_error(void);
+
+/* Frees the device memory of the handle. NULL is accepted. The caller must make sure no
+ * work of this handle is still running. */
+int decoder_destroy(pwd_decoder* dec);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PWDEC_H */

@@ -1,0 +1,195 @@
+// fp32 decoder for small windows: one workgroup runs one window through every round,
+// layer and the readout with its whole state in LDS (Algorithm 1, inference branch;
+// App. A model). Used for the fp32 configurations (d_model <= 64, about d <= 5), where a
+// window is a few kilobytes and the batch is small, so one launch per decode is the point.
+//
+// All matrix products are plain fp32 FMA loops; every output element is produced by one
+// thread in a fixed order, so results do not depend on the batch.
+#include "common.h"
+#include "kernels.h"
+
+namespace {
+
+struct LayerPtrs {
+    const float *Wq, *bq, *Wk, *bk, *Wv, *bv, *Wo, *bo, *g1, *be1, *W1, *b1, *W2, *b2, *g2, *be2;
+};
+
+__device__ const float* layer_ptrs(const float* w, int D, int F, int l, LayerPtrs& L) {
+    const size_t per = (size_t)4 * D * D + 4 * D + 2 * D + (size_t)D * F + F + (size_t)F * D + 3 * D;
+    const float* q = w + 2 * D + per * l;
+    L.Wq = q; q += D * D; L.bq = q; q += D;
+    L.Wk = q; q += D * D; L.bk = q; q += D;
+    L.Wv = q; q += D * D; L.bv = q; q += D;
+    L.Wo = q; q += D * D; L.bo = q; q += D;
+    L.g1 = q; q += D; L.be1 = q; q += D;
+    L.W1 = q; q += (size_t)D * F; L.b1 = q; q += F;
+    L.W2 = q; q += (size_t)F * D; L.b2 = q; q += D;
+    L.g2 = q; q += D; L.be2 = q; q += D;
+    return q;
+}
+
+// out[n][o] = bias[o] + sum_k in[n][k] W[k][o]  (+ res[n][o] when res != nullptr)
+__device__ void linear(const float* in, int N, int K, const float* W, const float* bias, int O,
+                       float* out, const float* res, bool relu) {
+    for (int idx = threadIdx.x; idx < N * O; idx += blockDim.x) {
+        const int n = idx / O, o = idx % O;
+        float acc = bias[o];
+        for (int k = 0; k < K; ++k) acc = fmaf(in[n * K + k], W[(size_t)k * O + o], acc);
+        if (relu) acc = fmaxf(acc, 0.f);
+        if (res) acc += res[idx];
+        out[idx] = acc;
+    }
+}
+
+// x[n][:] = LayerNorm(x[n][:]) for each token (one thread per token, two passes)
+__device__ void layer_norm_rows(float* x, int N, int D, const float* g, const float* b, float eps) {
+    for (int n = threadIdx.x; n < N; n += blockDim.x) {
+        float* r = x + n * D;
+        float s = 0.f;
+        for (int k = 0; k < D; ++k) s += r[k];
+        const float mean = s / D;
+        float v = 0.f;
+        for (int k = 0; k < D; ++k) v += (r[k] - mean) * (r[k] - mean);
+        const float rstd = rsqrtf(v / D + eps);
+        for (int k = 0; k < D; ++k) r[k] = (r[k] - mean) * rstd * g[k] + b[k];
+    }
+}
+
+__global__ __launch_bounds__(256) void f32_window_kernel(F32Params p) {
+    const int win = blockIdx.x;
+    const int N = p.in.N, D = p.D, F = p.F, H = p.H, dh = D / H, d = p.in.d;
+    extern __shared__ __align__(16) float sm[];
+    float* X = sm;                 // [N][D] state / residual stream
+    float* Z = X + N * D;          // [N][D] scratch
+    float* Q = Z + N * D;          // [N][D]
+    float* K = Q + N * D;          // [N][D]
+    float* V = K + N * D;          // [N][D]
+    float* A = V + N * D;          // [N][D] attention output (heads concatenated)
+    float* Hd = A + N * D;         // [N][F] feed-forward hidden
+    float* S = Hd + N * F;         // [H][N][N] scores / probabilities
+    __shared__ uint32_t ev[32];    // event words of one round (N <= 1024)
+    __shared__ float red[256];
+
+    const int type = p.in.types[win];
+    const uint32_t* meas = p.in.meas + (int64_t)win * (p.in.W + 1) * p.in.words;
+    const float* we = p.w;
+    const float scale = rsqrtf((float)dh);
+
+    for (int t = 0; t < p.in.W; ++t) {
+        for (int wd = threadIdx.x; wd < p.in.words; wd += blockDim.x)
+            ev[wd] = type > WIN_FINAL ? 0u : event_word(meas, p.in.words, t, wd, type, p.in.b_left, d);
+        __syncthreads();
+        // embedding + fold: X = kappa (E w_e + b_e + PE + X), X = 0 before round 0
+        for (int idx = threadIdx.x; idx < N * D; idx += blockDim.x) {
+            const int n = idx / D, k = idx % D;
+            const float e = (float)((ev[n >> 5] >> (n & 31)) & 1u);
+            const float s = fmaf(e, we[k], p.S0[idx]);
+            X[idx] = p.kappa * (s + (t > 0 ? X[idx] : 0.f));
+        }
+        __syncthreads();
+        for (int l = 0; l < p.L; ++l) {
+            LayerPtrs L;
+            layer_ptrs(p.w, D, F, l, L);
+            linear(X, N, D, L.Wq, L.bq, D, Q, nullptr, false);
+            linear(X, N, D, L.Wk, L.bk, D, K, nullptr, false);
+            linear(X, N, D, L.Wv, L.bv, D, V, nullptr, false);
+            __syncthreads();
+            for (int idx = threadIdx.x; idx < H * N * N; idx += blockDim.x) {
+                const int h = idx / (N * N), q = (idx / N) % N, k = idx % N;
+                float acc = 0.f;
+                for (int e = 0; e < dh; ++e) acc = fmaf(Q[q * D + h * dh + e], K[k * D + h * dh + e], acc);
+                S[idx] = acc * scale;
+            }
+            __syncthreads();
+            for (int row = threadIdx.x; row < H * N; row += blockDim.x) {
+                float* r = S + row * N;
+                float mx = r[0];
+                for (int k = 1; k < N; ++k) mx = fmaxf(mx, r[k]);
+                float sum = 0.f;
+                for (int k = 0; k < N; ++k) {
+                    r[k] = expf(r[k] - mx);
+                    sum += r[k];
+                }
+                const float inv = 1.f / sum;
+                for (int k = 0; k < N; ++k) r[k] *= inv;
+            }
+            __syncthreads();
+            for (int idx = threadIdx.x; idx < N * D; idx += blockDim.x) {
+                const int q = idx / D, c = idx % D, h = c / dh;
+                float acc = 0.f;
+                for (int k = 0; k < N; ++k) acc = fmaf(S[(h * N + q) * N + k], V[k * D + c], acc);
+                A[idx] = acc;
+            }
+            __syncthreads();
+            linear(A, N, D, L.Wo, L.bo, D, Z, X, false);      // Z = X + A Wo + bo
+            __syncthreads();
+            layer_norm_rows(Z, N, D, L.g1, L.be1, p.eps);
+            __syncthreads();
+            linear(Z, N, D, L.W1, L.b1, F, Hd, nullptr, true);
+            __syncthreads();
+            linear(Hd, N, F, L.W2, L.b2, D, X, Z, false);     // X = Z + FF(Z)
+            __syncthreads();
+            layer_norm_rows(X, N, D, L.g2, L.be2, p.eps);
+            __syncthreads();
+        }
+    }
+
+    // readout (App. A.3): 2x2 valid convolution + ReLU, mean over columns, linear
+    LayerPtrs L;
+    const float* Wc = layer_ptrs(p.w, D, F, p.L - 1, L);
+    const float* bc = Wc + 4 * (size_t)D * D;
+    const float* wo = bc + D;
+    const float bo = wo[(size_t)d * D];
+    const float* beta = wo + (size_t)d * D + 1;
+    const int gw = d + 1;
+    float part = 0.f;
+    for (int idx = threadIdx.x; idx < d * D; idx += blockDim.x) {
+        const int i = idx / D, o = idx % D;
+        float pool = 0.f;
+        for (int j = 0; j < d; ++j) {
+            float acc = bc[o];
+            for (int a = 0; a < 2; ++a)
+                for (int b = 0; b < 2; ++b) {
+                    const int tok = p.cell_token[(i + a) * gw + (j + b)];
+                    if (tok < 0) continue;
+                    const float* wab = Wc + (size_t)(a * 2 + b) * D * D;
+                    for (int k = 0; k < D; ++k) acc = fmaf(X[tok * D + k], wab[(size_t)k * D + o], acc);
+                }
+            pool += fmaxf(acc, 0.f);
+        }
+        part = fmaf(wo[idx], pool / (float)d, part);
+    }
+    red[threadIdx.x] = part;
+    __syncthreads();
+    for (int n = blockDim.x / 2; n > 0; n >>= 1) {
+        if ((int)threadIdx.x < n) red[threadIdx.x] += red[threadIdx.x + n];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        if (type > WIN_FINAL) {
+            p.logits[win] = __builtin_nanf("");
+            p.bits[win] = 0;
+            atomicOr(p.err, 1);
+        } else {
+            const float logit = red[0] + bo + beta[type];
+            p.logits[win] = logit;
+            p.bits[win] = logit > 0.f ? 1 : 0;
+        }
+    }
+}
+
+}  // namespace
+
+size_t f32_window_smem_bytes(int N, int D, int H, int F) {
+    return ((size_t)6 * N * D + (size_t)N * F + (size_t)H * N * N) * sizeof(float);
+}
+
+hipError_t launch_f32_window(const F32Params& p, hipStream_t s) {
+    if (p.in.nwin <= 0) return hipSuccess;
+    const size_t smem = f32_window_smem_bytes(p.in.N, p.D, p.H, p.F);
+    hipError_t e = hipFuncSetAttribute((const void*)f32_window_kernel,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+    if (e != hipSuccess) return e;
+    f32_window_kernel<<<dim3((unsigned)p.in.nwin), dim3(256), smem, s>>>(p);
+    return hipGetLastError();
+}

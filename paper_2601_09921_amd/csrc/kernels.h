@@ -1,0 +1,81 @@
+// Kernel parameter blocks and launchers of the decoder (host <-> device interface inside
+// the library; nothing here is part of the public C ABI).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+// Window geometry and input pointers common to the stages that read syndromes.
+struct SyndromeIn {
+    const uint32_t* meas;   // [nwin][W+1][words]
+    const uint8_t* types;   // [nwin]
+    int nwin, W, words, d, N, b_left;
+};
+
+// Stage flags of the token-local kernel.
+enum { TOK_POST = 1, TOK_EMBED = 2, TOK_QKV = 4 };
+
+struct TokParams {
+    SyndromeIn in;
+    int Npad, nbw;          // padded tokens and 16-token blocks per window
+    int t;                  // round whose embedding TOK_EMBED adds
+    float kappa, eps;
+    float* X;               // fp32 residual / state, C fragments
+    uint16_t* QKV;          // bf16 B fragments [tb][3][D/32][64][8]
+    const uint16_t* Y;      // bf16 attention output [tb][D/32][64][8]
+    const float* S0;        // b_e + PE, fp32 C fragments [nbw][D/16][64][4] (0 on padding)
+    const float* we;        // [D]
+    // layer weights of the POST stage (A fragments bf16, vectors fp32)
+    const uint16_t *Wo, *W1, *W2;
+    const float *bo, *g1, *be1, *b1, *b2, *g2, *be2;
+    // QKV projection of the layer that follows (A fragments of [3D out][D in]), bias [3D]
+    const uint16_t* Wqkv;
+    const float* bqkv;
+};
+
+struct AttnParams {
+    const uint16_t* QKV;
+    uint16_t* Y;
+    int N, Npad, nbw, H;
+    float scale_log2;       // log2(e) / sqrt(dh)
+};
+
+struct ReadoutParams {
+    const float* X;         // final state, C fragments
+    const uint8_t* types;
+    float* logits;
+    uint8_t* bits;
+    int* err;               // device error word
+    const float* Wc;        // [2][2][D][D] fp32 ([a][b][in][out])
+    const float* bc;        // [D]
+    const float* wo;        // [d][D]
+    float bo;
+    float beta[3];
+    const int* cell_token;  // [(d+1)*(d+1)] token index or -1
+    int nwin, d, D, nbw;
+};
+
+struct EventsParams {
+    SyndromeIn in;
+    uint32_t* events;       // [nwin][W][words]
+    int* err;
+};
+
+struct F32Params {
+    SyndromeIn in;
+    const float* w;         // blob tensors in blob order (fp32)
+    const float* S0;        // b_e + PE per token [N][D]
+    const int* cell_token;  // [(d+1)*(d+1)]
+    float* logits;
+    uint8_t* bits;
+    int* err;
+    int D, L, H, F;
+    float kappa, eps;
+};
+
+hipError_t launch_events(const EventsParams& p, hipStream_t s);
+hipError_t launch_tok(int D, int flags, const TokParams& p, int64_t n_tb, hipStream_t s);
+hipError_t launch_attn(int dh, const AttnParams& p, int nwin, hipStream_t s);
+hipError_t launch_readout(const ReadoutParams& p, hipStream_t s);
+hipError_t launch_f32_window(const F32Params& p, hipStream_t s);
+size_t f32_window_smem_bytes(int N, int D, int H, int F);
+size_t attn_smem_bytes(int dh, int Npad, int nbw);

@@ -1,0 +1,504 @@
+// Host side of the C ABI in include/pwdec.h: validation, weight-blob parsing, the rotated
+// surface-code geometry, the positional-encoding table, weight relayout into MFMA
+// fragments, device allocation and the per-round launch sequence (Algorithm 1).
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/pwdec.h"
+#include "kernels.h"
+
+int64_t tok_block_granule();
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return code;
+}
+
+#define HIP_OK(call)                                                                     \
+    do {                                                                                 \
+        hipError_t e_ = (call);                                                          \
+        if (e_ != hipSuccess)                                                            \
+            return fail(PWD_EHIP, "%s failed: %s", #call, hipGetErrorString(e_));        \
+    } while (0)
+
+// Restores the caller's current device on scope exit.
+struct DeviceGuard {
+    int prev = -1;
+    hipError_t err = hipSuccess;
+    explicit DeviceGuard(int dev) {
+        err = hipGetDevice(&prev);
+        if (err == hipSuccess && prev != dev) err = hipSetDevice(dev);
+    }
+    ~DeviceGuard() {
+        if (prev >= 0) (void)hipSetDevice(prev);
+    }
+};
+
+uint16_t to_bf16(float f) {
+    uint32_t u;
+    std::memcpy(&u, &f, 4);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40);   // quiet NaN
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+int kslot(int g, int i) { return i < 4 ? 4 * g + i : 16 + 4 * g + (i - 4); }
+
+// W is [K][O] row-major (y = x W). Output: A fragments of W^T, [O/16][K/32][64][8] bf16.
+void append_frags(std::vector<uint16_t>& out, const float* W, int K, int O) {
+    for (int ro = 0; ro < O / 16; ++ro)
+        for (int ks = 0; ks < K / 32; ++ks)
+            for (int lane = 0; lane < 64; ++lane)
+                for (int i = 0; i < 8; ++i) {
+                    const int row = ro * 16 + (lane & 15);
+                    const int k = ks * 32 + kslot(lane >> 4, i);
+                    out.push_back(to_bf16(W[(size_t)k * O + row]));
+                }
+}
+
+// Stabilizer cells of the rotated surface code, row-major over the (d+1)x(d+1) lattice.
+std::vector<std::pair<int, int>> stabilizer_cells(int d) {
+    std::vector<std::pair<int, int>> cells;
+    for (int r = 0; r <= d; ++r)
+        for (int c = 0; c <= d; ++c) {
+            const bool inner = r >= 1 && r <= d - 1 && c >= 1 && c <= d - 1;
+            const bool tb = (r == 0 || r == d) && c >= 1 && c <= d - 1 && (r + c) % 2 == 0;
+            const bool lr = (c == 0 || c == d) && r >= 1 && r <= d - 1 && (r + c) % 2 == 1;
+            if (inner || tb || lr) cells.emplace_back(r, c);
+        }
+    return cells;
+}
+
+size_t layer_floats(int D, int F) { return (size_t)4 * D * D + 2 * (size_t)D * F + F + 9 * (size_t)D; }
+
+}  // namespace
+
+struct pwd_decoder {
+    int device = 0;
+    int d = 0, W = 0, max_windows = 0, N = 0, Npad = 0, nbw = 0, words = 0, b_left = 0;
+    int D = 0, L = 0, H = 0, F = 0, dh = 0, dtype = 0;
+    float kappa = 0.f, eps = 0.f;
+    int64_t n_tb_alloc = 0;
+    // device memory
+    void* weights = nullptr;       // one allocation for every parameter table
+    float* X = nullptr;
+    uint16_t* QKV = nullptr;
+    uint16_t* Y = nullptr;
+    int* err = nullptr;
+    // views into `weights`
+    struct Layer {
+        const uint16_t *Wo, *W1, *W2, *Wqkv;
+        const float *bo, *g1, *be1, *b1, *b2, *g2, *be2, *bqkv;
+    };
+    std::vector<Layer> layers;
+    const float* S0 = nullptr;
+    const float* we = nullptr;
+    const float* Wc = nullptr;
+    const float* bc = nullptr;
+    const float* wo = nullptr;
+    const int* cell_token = nullptr;
+    const float* f32w = nullptr;   // fp32 path: the blob tensors as given
+    float bo_out = 0.f, beta[3] = {0.f, 0.f, 0.f};
+};
+
+extern "C" {
+
+const char* decoder_last_error(void) { return g_last_error.c_str(); }
+
+size_t decoder_blob_floats(const pwd_geometry* geom, const pwd_model_dims* dims) {
+    if (!geom || !dims) return 0;
+    const int D = dims->d_model, F = dims->mlp_ratio * dims->d_model, d = geom->distance;
+    return 2 * (size_t)D + (size_t)dims->n_layers * layer_floats(D, F) + 4 * (size_t)D * D + D +
+           (size_t)d * D + 1 + 3;
+}
+
+int decoder_validate_config(const pwd_geometry* g, const pwd_model_dims* m) {
+    if (!g || !m) return fail(PWD_EINVAL, "null geometry or dimensions");
+    const int d = g->distance;
+    if (d < 3 || d > 25 || d % 2 == 0) return fail(PWD_EUNSUPPORTED, "distance %d: need odd 3..25", d);
+    if (g->window_rounds < d || g->window_rounds > 3 * d)
+        return fail(PWD_EUNSUPPORTED, "window_rounds %d: need %d..%d", g->window_rounds, d, 3 * d);
+    if (g->max_windows < 1 || g->max_windows > (1 << 24))
+        return fail(PWD_EUNSUPPORTED, "max_windows %d: need 1..2^24", g->max_windows);
+    if (m->mlp_ratio != 4) return fail(PWD_EUNSUPPORTED, "mlp_ratio %d: need 4", m->mlp_ratio);
+    if (m->n_layers < 1 || m->n_layers > 8) return fail(PWD_EUNSUPPORTED, "n_layers %d: need 1..8", m->n_layers);
+    if (m->n_heads < 1 || m->d_model % m->n_heads != 0)
+        return fail(PWD_EUNSUPPORTED, "d_model %d not divisible by n_heads %d", m->d_model, m->n_heads);
+    const int dh = m->d_model / m->n_heads;
+    const int N = d * d - 1;
+    if (m->dtype == PWD_DTYPE_BF16) {
+        if (m->d_model != 128 && m->d_model != 256)
+            return fail(PWD_EUNSUPPORTED, "bf16 d_model %d: need 128 or 256", m->d_model);
+        if (dh != 16 && dh != 32) return fail(PWD_EUNSUPPORTED, "bf16 head size %d: need 16 or 32", dh);
+        const size_t smem = attn_smem_bytes(dh, (N + 15) / 16 * 16, (N + 15) / 16);
+        if (smem > 160 * 1024) return fail(PWD_EUNSUPPORTED, "attention tile needs %zu bytes of LDS", smem);
+    } else if (m->dtype == PWD_DTYPE_F32) {
+        if (m->d_model != 16 && m->d_model != 32 && m->d_model != 64)
+            return fail(PWD_EUNSUPPORTED, "fp32 d_model %d: need 16, 32 or 64", m->d_model);
+        if (dh != 4 && dh != 8 && dh != 16 && dh != 32)
+            return fail(PWD_EUNSUPPORTED, "fp32 head size %d: need 4, 8, 16 or 32", dh);
+        const size_t smem = f32_window_smem_bytes(N, m->d_model, m->n_heads, 4 * m->d_model);
+        if (smem > 64 * 1024)
+            return fail(PWD_EUNSUPPORTED, "fp32 window of %d tokens needs %zu bytes of LDS (max 65536)", N, smem);
+    } else {
+        return fail(PWD_EUNSUPPORTED, "dtype %d: need 0 (fp32) or 1 (bf16)", m->dtype);
+    }
+    return PWD_OK;
+}
+
+int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const void* blob,
+                   size_t blob_bytes, pwd_decoder** out) {
+    if (!out || !blob) return fail(PWD_EINVAL, "null blob or output handle");
+    int rc = decoder_validate_config(geom, dims);
+    if (rc != PWD_OK) return rc;
+    const size_t nf = decoder_blob_floats(geom, dims);
+    if (blob_bytes != PWD_BLOB_HEADER_WORDS * 4 + nf * 4)
+        return fail(PWD_EBLOB, "blob has %zu bytes, expected %zu", blob_bytes, PWD_BLOB_HEADER_WORDS * 4 + nf * 4);
+    uint32_t hdr[PWD_BLOB_HEADER_WORDS];
+    std::memcpy(hdr, blob, sizeof hdr);
+    const int d = geom->distance, D = dims->d_model, L = dims->n_layers, H = dims->n_heads;
+    const int F = dims->mlp_ratio * D;
+    if (hdr[0] != PWD_BLOB_MAGIC) return fail(PWD_EBLOB, "bad blob magic 0x%08x", hdr[0]);
+    if (hdr[1] != PWD_BLOB_VERSION) return fail(PWD_EBLOB, "blob version %u, expected %d", hdr[1], PWD_BLOB_VERSION);
+    const int expect[7] = {d, geom->window_rounds, D, L, H, F, dims->dtype};
+    for (int i = 0; i < 7; ++i)
+        if ((int)hdr[2 + i] != expect[i])
+            return fail(PWD_EBLOB, "blob header word %d is %d, expected %d", 2 + i, (int)hdr[2 + i], expect[i]);
+    float kappa, eps;
+    std::memcpy(&kappa, &hdr[9], 4);
+    std::memcpy(&eps, &hdr[10], 4);
+    if (!(eps > 0.f) || !std::isfinite(kappa)) return fail(PWD_EBLOB, "blob kappa/eps invalid");
+    const float* wf = reinterpret_cast<const float*>(static_cast<const char*>(blob) + PWD_BLOB_HEADER_WORDS * 4);
+    std::vector<float> w(wf, wf + nf);   // aligned copy
+
+    int device = 0;
+    HIP_OK(hipGetDevice(&device));
+    pwd_decoder* dec = new (std::nothrow) pwd_decoder();
+    if (!dec) return fail(PWD_ENOMEM, "host allocation failed");
+    dec->device = device;
+    dec->d = d;
+    dec->W = geom->window_rounds;
+    dec->max_windows = geom->max_windows;
+    dec->N = d * d - 1;
+    dec->Npad = (dec->N + 15) / 16 * 16;
+    dec->nbw = dec->Npad / 16;
+    dec->words = (dec->N + 31) / 32;
+    dec->b_left = (dec->W - d) / 2;
+    dec->D = D; dec->L = L; dec->H = H; dec->F = F; dec->dh = D / H; dec->dtype = dims->dtype;
+    dec->kappa = kappa; dec->eps = eps;
+
+    // geometry tables
+    const auto cells = stabilizer_cells(d);
+    std::vector<int> cell_token((size_t)(d + 1) * (d + 1), -1);
+    for (size_t s = 0; s < cells.size(); ++s) cell_token[cells[s].first * (d + 1) + cells[s].second] = (int)s;
+
+    // the parameter tables, laid out in one host image, then one upload
+    std::vector<unsigned char> img;
+    auto align = [&]() { img.resize((img.size() + 255) & ~(size_t)255); };
+    auto put = [&](const void* src, size_t bytes) {
+        align();
+        const size_t off = img.size();
+        img.resize(off + bytes);
+        std::memcpy(img.data() + off, src, bytes);
+        return off;
+    };
+
+    // S0 = b_e + PE[pos(s)] (App. A.1.4 sinusoids over the flattened lattice index), double
+    // precision on the host, rounded to fp32.
+    const float* b_e = w.data() + D;
+    std::vector<double> pe_row(D);
+    auto pe_of = [&](int pos) {
+        for (int i = 0; i < D / 2; ++i) {
+            const double ang = pos / std::pow(10000.0, 2.0 * i / D);
+            pe_row[2 * i] = std::sin(ang);
+            pe_row[2 * i + 1] = std::cos(ang);
+        }
+    };
+    const size_t off_cell = put(cell_token.data(), cell_token.size() * sizeof(int));
+
+    struct LayerOff { size_t Wo, W1, W2, Wqkv, bo, g1, be1, b1, b2, g2, be2, bqkv; };
+    std::vector<LayerOff> loff(L);
+    size_t off_S0 = 0, off_we = 0, off_Wc = 0, off_bc = 0, off_wo = 0, off_f32 = 0;
+    const size_t lf = layer_floats(D, F);
+    const float* tail = w.data() + 2 * D + (size_t)L * lf;   // Wc, bc, w_o, b_o, beta
+    if (dims->dtype == PWD_DTYPE_BF16) {
+        const int RT = D / 16;
+        std::vector<float> s0((size_t)dec->nbw * RT * 64 * 4, 0.f);
+        for (int s = 0; s < dec->N; ++s) {
+            pe_of(cells[s].first * (d + 1) + cells[s].second);
+            const int blk = s / 16, cl = s % 16;
+            for (int f = 0; f < D; ++f) {
+                const int rt = f / 16, g = (f % 16) / 4, i = f % 4;
+                s0[(((size_t)blk * RT + rt) * 64 + g * 16 + cl) * 4 + i] = (float)((double)b_e[f] + pe_row[f]);
+            }
+        }
+        off_S0 = put(s0.data(), s0.size() * 4);
+        off_we = put(w.data(), (size_t)D * 4);
+        for (int l = 0; l < L; ++l) {
+            const float* p = w.data() + 2 * D + (size_t)l * lf;
+            const float *Wq = p, *bq = Wq + D * D, *Wk = bq + D, *bk = Wk + D * D, *Wv = bk + D, *bv = Wv + D * D;
+            const float *Wo = bv + D, *bo = Wo + D * D, *g1 = bo + D, *be1 = g1 + D, *W1 = be1 + D;
+            const float *b1 = W1 + (size_t)D * F, *W2 = b1 + F, *b2 = W2 + (size_t)F * D, *g2 = b2 + D, *be2 = g2 + D;
+            std::vector<float> wqkv((size_t)D * 3 * D), bqkv(3 * D);
+            for (int k = 0; k < D; ++k)
+                for (int o = 0; o < D; ++o) {
+                    wqkv[(size_t)k * 3 * D + o] = Wq[k * D + o];
+                    wqkv[(size_t)k * 3 * D + D + o] = Wk[k * D + o];
+                    wqkv[(size_t)k * 3 * D + 2 * D + o] = Wv[k * D + o];
+                }
+            for (int o = 0; o < D; ++o) {
+                bqkv[o] = bq[o];
+                bqkv[D + o] = bk[o];
+                bqkv[2 * D + o] = bv[o];
+            }
+            std::vector<uint16_t> fr;
+            fr.clear(); append_frags(fr, Wo, D, D); loff[l].Wo = put(fr.data(), fr.size() * 2);
+            fr.clear(); append_frags(fr, W1, D, F); loff[l].W1 = put(fr.data(), fr.size() * 2);
+            fr.clear(); append_frags(fr, W2, F, D); loff[l].W2 = put(fr.data(), fr.size() * 2);
+            fr.clear(); append_frags(fr, wqkv.data(), D, 3 * D); loff[l].Wqkv = put(fr.data(), fr.size() * 2);
+            loff[l].bo = put(bo, D * 4);
+            loff[l].g1 = put(g1, D * 4);
+            loff[l].be1 = put(be1, D * 4);
+            loff[l].b1 = put(b1, F * 4);
+            loff[l].b2 = put(b2, D * 4);
+            loff[l].g2 = put(g2, D * 4);
+            loff[l].be2 = put(be2, D * 4);
+            loff[l].bqkv = put(bqkv.data(), 3 * D * 4);
+        }
+        off_Wc = put(tail, (size_t)4 * D * D * 4);
+        off_bc = put(tail + 4 * (size_t)D * D, D * 4);
+        off_wo = put(tail + 4 * (size_t)D * D + D, (size_t)d * D * 4);
+    } else {
+        std::vector<float> s0((size_t)dec->N * D);
+        for (int s = 0; s < dec->N; ++s) {
+            pe_of(cells[s].first * (d + 1) + cells[s].second);
+            for (int f = 0; f < D; ++f) s0[(size_t)s * D + f] = (float)((double)b_e[f] + pe_row[f]);
+        }
+        off_S0 = put(s0.data(), s0.size() * 4);
+        off_f32 = put(w.data(), nf * 4);
+    }
+    const float* bo_beta = tail + 4 * (size_t)D * D + D + (size_t)d * D;
+    dec->bo_out = bo_beta[0];
+    for (int i = 0; i < 3; ++i) dec->beta[i] = bo_beta[1 + i];
+
+    auto cleanup_fail = [&](int code) {
+        decoder_destroy(dec);
+        return code;
+    };
+    hipError_t e = hipMalloc(&dec->weights, img.size());
+    if (e != hipSuccess) return cleanup_fail(fail(PWD_ENOMEM, "hipMalloc(weights, %zu): %s", img.size(), hipGetErrorString(e)));
+    e = hipMemcpy(dec->weights, img.data(), img.size(), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return cleanup_fail(fail(PWD_EHIP, "hipMemcpy(weights): %s", hipGetErrorString(e)));
+    e = hipMalloc(&dec->err, sizeof(int));
+    if (e == hipSuccess) e = hipMemset(dec->err, 0, sizeof(int));
+    if (e != hipSuccess) return cleanup_fail(fail(PWD_ENOMEM, "error word: %s", hipGetErrorString(e)));
+
+    const unsigned char* base = static_cast<const unsigned char*>(dec->weights);
+    auto fptr = [&](size_t off) { return reinterpret_cast<const float*>(base + off); };
+    auto hptr = [&](size_t off) { return reinterpret_cast<const uint16_t*>(base + off); };
+    dec->cell_token = reinterpret_cast<const int*>(base + off_cell);
+    dec->S0 = fptr(off_S0);
+    if (dims->dtype == PWD_DTYPE_BF16) {
+        dec->we = fptr(off_we);
+        dec->Wc = fptr(off_Wc);
+        dec->bc = fptr(off_bc);
+        dec->wo = fptr(off_wo);
+        for (int l = 0; l < L; ++l) {
+            pwd_decoder::Layer ly;
+            ly.Wo = hptr(loff[l].Wo); ly.W1 = hptr(loff[l].W1); ly.W2 = hptr(loff[l].W2); ly.Wqkv = hptr(loff[l].Wqkv);
+            ly.bo = fptr(loff[l].bo); ly.g1 = fptr(loff[l].g1); ly.be1 = fptr(loff[l].be1); ly.b1 = fptr(loff[l].b1);
+            ly.b2 = fptr(loff[l].b2); ly.g2 = fptr(loff[l].g2); ly.be2 = fptr(loff[l].be2); ly.bqkv = fptr(loff[l].bqkv);
+            dec->layers.push_back(ly);
+        }
+        const int64_t gran = tok_block_granule();
+        dec->n_tb_alloc = ((int64_t)dec->max_windows * dec->nbw + gran - 1) / gran * gran;
+        const size_t xb = (size_t)dec->n_tb_alloc * 16 * D * sizeof(float);
+        const size_t qb = (size_t)dec->n_tb_alloc * 48 * D * sizeof(uint16_t);
+        const size_t yb = (size_t)dec->n_tb_alloc * 16 * D * sizeof(uint16_t);
+        if ((e = hipMalloc(&dec->X, xb)) != hipSuccess || (e = hipMalloc(&dec->QKV, qb)) != hipSuccess ||
+            (e = hipMalloc(&dec->Y, yb)) != hipSuccess)
+            return cleanup_fail(fail(PWD_ENOMEM, "scratch for %d windows (%zu bytes): %s", dec->max_windows,
+                                     xb + qb + yb, hipGetErrorString(e)));
+        // padding blocks are computed too; start them from finite values
+        if ((e = hipMemset(dec->X, 0, xb)) != hipSuccess || (e = hipMemset(dec->QKV, 0, qb)) != hipSuccess ||
+            (e = hipMemset(dec->Y, 0, yb)) != hipSuccess)
+            return cleanup_fail(fail(PWD_EHIP, "scratch clear: %s", hipGetErrorString(e)));
+    } else {
+        dec->f32w = fptr(off_f32);
+    }
+    *out = dec;
+    return PWD_OK;
+}
+
+int decoder_destroy(pwd_decoder* dec) {
+    if (!dec) return PWD_OK;
+    DeviceGuard dg(dec->device);
+    (void)hipFree(dec->weights);
+    (void)hipFree(dec->X);
+    (void)hipFree(dec->QKV);
+    (void)hipFree(dec->Y);
+    (void)hipFree(dec->err);
+    delete dec;
+    return PWD_OK;
+}
+
+static SyndromeIn syndrome_in(const pwd_decoder* dec, const uint32_t* meas, const uint8_t* types, int64_t n) {
+    SyndromeIn in;
+    in.meas = meas;
+    in.types = types;
+    in.nwin = (int)n;
+    in.W = dec->W;
+    in.words = dec->words;
+    in.d = dec->d;
+    in.N = dec->N;
+    in.b_left = dec->b_left;
+    return in;
+}
+
+int decode_windows(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_types, int64_t n,
+                   float* d_logits, uint8_t* d_bits, void* hip_stream) {
+    if (!dec) return fail(PWD_EINVAL, "null decoder");
+    if (n < 0) return fail(PWD_EINVAL, "negative n_windows");
+    if (n > dec->max_windows) return fail(PWD_EBATCH, "n_windows %lld > max_windows %d", (long long)n, dec->max_windows);
+    if (n == 0) return PWD_OK;
+    if (!d_meas || !d_types || !d_logits || !d_bits) return fail(PWD_EINVAL, "null buffer");
+    DeviceGuard dg(dec->device);
+    HIP_OK(dg.err);
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+    const SyndromeIn in = syndrome_in(dec, d_meas, d_types, n);
+
+    if (dec->dtype == PWD_DTYPE_F32) {
+        F32Params p;
+        p.in = in;
+        p.w = dec->f32w;
+        p.S0 = dec->S0;
+        p.cell_token = dec->cell_token;
+        p.logits = d_logits;
+        p.bits = d_bits;
+        p.err = dec->err;
+        p.D = dec->D; p.L = dec->L; p.H = dec->H; p.F = dec->F;
+        p.kappa = dec->kappa; p.eps = dec->eps;
+        HIP_OK(launch_f32_window(p, s));
+        return PWD_OK;
+    }
+
+    const int64_t n_tb = n * dec->nbw;
+    TokParams tp;
+    std::memset(&tp, 0, sizeof tp);
+    tp.in = in;
+    tp.Npad = dec->Npad;
+    tp.nbw = dec->nbw;
+    tp.kappa = dec->kappa;
+    tp.eps = dec->eps;
+    tp.X = dec->X;
+    tp.QKV = dec->QKV;
+    tp.Y = dec->Y;
+    tp.S0 = dec->S0;
+    tp.we = dec->we;
+    auto set_post = [&](int l) {
+        const auto& ly = dec->layers[l];
+        tp.Wo = ly.Wo; tp.W1 = ly.W1; tp.W2 = ly.W2;
+        tp.bo = ly.bo; tp.g1 = ly.g1; tp.be1 = ly.be1; tp.b1 = ly.b1; tp.b2 = ly.b2; tp.g2 = ly.g2; tp.be2 = ly.be2;
+    };
+    auto set_qkv = [&](int l) {
+        tp.Wqkv = dec->layers[l].Wqkv;
+        tp.bqkv = dec->layers[l].bqkv;
+    };
+    AttnParams ap;
+    ap.QKV = dec->QKV;
+    ap.Y = dec->Y;
+    ap.N = dec->N;
+    ap.Npad = dec->Npad;
+    ap.nbw = dec->nbw;
+    ap.H = dec->H;
+    ap.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)dec->dh));
+
+    // round 0: embed (state D_0 = 0) and project layer 0
+    tp.t = 0;
+    set_qkv(0);
+    HIP_OK(launch_tok(dec->D, TOK_EMBED | TOK_QKV, tp, n_tb, s));
+    for (int t = 0; t < dec->W; ++t) {
+        for (int l = 0; l < dec->L; ++l) {
+            HIP_OK(launch_attn(dec->dh, ap, (int)n, s));
+            set_post(l);
+            if (l + 1 < dec->L) {
+                set_qkv(l + 1);
+                HIP_OK(launch_tok(dec->D, TOK_POST | TOK_QKV, tp, n_tb, s));
+            } else if (t + 1 < dec->W) {
+                tp.t = t + 1;          // fold the next round's embedding into D_t
+                set_qkv(0);
+                HIP_OK(launch_tok(dec->D, TOK_POST | TOK_EMBED | TOK_QKV, tp, n_tb, s));
+            } else {
+                HIP_OK(launch_tok(dec->D, TOK_POST, tp, n_tb, s));
+            }
+        }
+    }
+    ReadoutParams rp;
+    rp.X = dec->X;
+    rp.types = d_types;
+    rp.logits = d_logits;
+    rp.bits = d_bits;
+    rp.err = dec->err;
+    rp.Wc = dec->Wc;
+    rp.bc = dec->bc;
+    rp.wo = dec->wo;
+    rp.bo = dec->bo_out;
+    for (int i = 0; i < 3; ++i) rp.beta[i] = dec->beta[i];
+    rp.cell_token = dec->cell_token;
+    rp.nwin = (int)n;
+    rp.d = dec->d;
+    rp.D = dec->D;
+    rp.nbw = dec->nbw;
+    HIP_OK(launch_readout(rp, s));
+    return PWD_OK;
+}
+
+int decoder_detection_events(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_types,
+                             int64_t n, uint32_t* d_events, void* hip_stream) {
+    if (!dec) return fail(PWD_EINVAL, "null decoder");
+    if (n < 0) return fail(PWD_EINVAL, "negative n_windows");
+    if (n > dec->max_windows) return fail(PWD_EBATCH, "n_windows %lld > max_windows %d", (long long)n, dec->max_windows);
+    if (n == 0) return PWD_OK;
+    if (!d_meas || !d_types || !d_events) return fail(PWD_EINVAL, "null buffer");
+    DeviceGuard dg(dec->device);
+    HIP_OK(dg.err);
+    EventsParams p;
+    p.in = syndrome_in(dec, d_meas, d_types, n);
+    p.events = d_events;
+    p.err = dec->err;
+    HIP_OK(launch_events(p, static_cast<hipStream_t>(hip_stream)));
+    return PWD_OK;
+}
+
+int decoder_sync_status(pwd_decoder* dec, void* hip_stream) {
+    if (!dec) return fail(PWD_EINVAL, "null decoder");
+    DeviceGuard dg(dec->device);
+    HIP_OK(dg.err);
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+    HIP_OK(hipStreamSynchronize(s));
+    int flag = 0;
+    HIP_OK(hipMemcpy(&flag, dec->err, sizeof(int), hipMemcpyDeviceToHost));
+    if (flag) {
+        HIP_OK(hipMemset(dec->err, 0, sizeof(int)));
+        return fail(PWD_EDEVICE, "a window had an invalid type (> 2)");
+    }
+    return PWD_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,161 @@
+"""Thin ctypes binding of libpwdec.so (include/pwdec.h).
+
+Argument marshalling only: every step of the decoder runs in the library's HIP kernels.
+Device buffers are torch tensors on the decoder's GPU; torch supplies memory and streams.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+import struct
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libpwdec.so")
+HEADER = os.path.join(os.path.dirname(HERE), "include", "pwdec.h")
+
+PWD_OK, PWD_EINVAL, PWD_EUNSUPPORTED, PWD_EBLOB, PWD_ENOMEM, PWD_EHIP, PWD_EBATCH, PWD_EDEVICE = (
+    0, -1, -2, -3, -4, -5, -6, -7)
+DTYPE_F32, DTYPE_BF16 = 0, 1
+BLOB_MAGIC = 0x31445750
+BLOB_VERSION = 1
+
+
+class PwdError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"pwdec error {code}: {msg}")
+        self.code = code
+
+
+class Geometry(ctypes.Structure):
+    _fields_ = [("distance", ctypes.c_int32), ("window_rounds", ctypes.c_int32),
+                ("max_windows", ctypes.c_int32)]
+
+
+class ModelDims(ctypes.Structure):
+    _fields_ = [("d_model", ctypes.c_int32), ("n_layers", ctypes.c_int32), ("n_heads", ctypes.c_int32),
+                ("mlp_ratio", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def load_library() -> ctypes.CDLL:
+    """Loads the in-tree libpwdec.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_2601_09921_amd.build.build()")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I64, VP = ctypes.POINTER, ctypes.c_int64, ctypes.c_void_p
+    sig = {
+        "decoder_blob_floats": (ctypes.c_size_t, [P(Geometry), P(ModelDims)]),
+        "decoder_validate_config": (ctypes.c_int, [P(Geometry), P(ModelDims)]),
+        "decoder_create": (ctypes.c_int, [P(Geometry), P(ModelDims), ctypes.c_void_p, ctypes.c_size_t, P(VP)]),
+        "decode_windows": (ctypes.c_int, [VP, VP, VP, I64, VP, VP, VP]),
+        "decoder_detection_events": (ctypes.c_int, [VP, VP, VP, I64, VP, VP]),
+        "decoder_sync_status": (ctypes.c_int, [VP, VP]),
+        "decoder_last_error": (ctypes.c_char_p, []),
+        "decoder_destroy": (ctypes.c_int, [VP]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype, fn.argtypes = res, args
+    _lib = lib
+    return lib
+
+
+def header_functions() -> list[str]:
+    """Names of the functions declared in include/pwdec.h."""
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", text, flags=re.M)
+
+
+def _check(rc: int):
+    if rc != PWD_OK:
+        raise PwdError(rc, load_library().decoder_last_error().decode())
+
+
+def geometry(d: int, W: int, max_windows: int) -> Geometry:
+    return Geometry(d, W, max_windows)
+
+
+def dims(D: int, L: int, H: int, mlp_ratio: int, dtype: int) -> ModelDims:
+    return ModelDims(D, L, H, mlp_ratio, dtype)
+
+
+def make_blob(d: int, W: int, D: int, L: int, H: int, F: int, dtype: int, weights: dict) -> bytes:
+    """Serializes a weight dict into the library's blob format (header + fp32 tensors)."""
+    kappa = np.float32(weights["kappa"])
+    eps = np.float32(weights["eps"])
+    hdr = [BLOB_MAGIC, BLOB_VERSION, d, W, D, L, H, F, dtype,
+           struct.unpack("<I", struct.pack("<f", kappa))[0],
+           struct.unpack("<I", struct.pack("<f", eps))[0], 0, 0, 0, 0, 0]
+    parts = [weights["w_e"], weights["b_e"]]
+    for lw in weights["layers"]:
+        parts += [lw[k] for k in ("Wq", "bq", "Wk", "bk", "Wv", "bv", "Wo", "bo", "g1", "be1",
+                                  "W1", "b1", "W2", "b2", "g2", "be2")]
+    parts += [weights["Wc"], weights["bc"], weights["w_o"], weights["b_o"], weights["beta"]]
+    body = np.concatenate([np.asarray(p, dtype=np.float64).ravel() for p in parts]).astype("<f4")
+    return struct.pack("<16I", *hdr) + body.tobytes()
+
+
+def _stream_ptr(stream) -> ctypes.c_void_p:
+    if stream is None:
+        import torch
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+class Decoder:
+    """Owns one pwd_decoder handle."""
+
+    def __init__(self, d: int, W: int, max_windows: int, D: int, L: int, H: int, mlp_ratio: int,
+                 dtype: int, blob: bytes):
+        lib = load_library()
+        self._lib = lib
+        self.d, self.W, self.max_windows = d, W, max_windows
+        self.N = d * d - 1
+        self.words = (self.N + 31) // 32
+        g, m = geometry(d, W, max_windows), dims(D, L, H, mlp_ratio, dtype)
+        h = ctypes.c_void_p()
+        buf = ctypes.create_string_buffer(blob, len(blob))
+        _check(lib.decoder_create(ctypes.byref(g), ctypes.byref(m), buf, len(blob), ctypes.byref(h)))
+        self._h = h
+
+    @classmethod
+    def from_workload(cls, wl, weights: dict, max_windows: int | None = None) -> "Decoder":
+        blob = make_blob(wl.d, wl.W, wl.D, wl.L, wl.H, wl.F, wl.dtype, weights)
+        return cls(wl.d, wl.W, max_windows or wl.B, wl.D, wl.L, wl.H, wl.mlp_ratio, wl.dtype, blob)
+
+    def decode(self, meas, types, logits, bits, stream=None):
+        """meas: int32/uint32 [n][W+1][words] cuda tensor; types: uint8 [n]; outputs float32/uint8 [n]."""
+        n = types.shape[0]
+        _check(self._lib.decode_windows(self._h, ctypes.c_void_p(meas.data_ptr()),
+                                        ctypes.c_void_p(types.data_ptr()), n,
+                                        ctypes.c_void_p(logits.data_ptr()), ctypes.c_void_p(bits.data_ptr()),
+                                        _stream_ptr(stream)))
+
+    def detection_events(self, meas, types, events, stream=None):
+        n = types.shape[0]
+        _check(self._lib.decoder_detection_events(self._h, ctypes.c_void_p(meas.data_ptr()),
+                                                  ctypes.c_void_p(types.data_ptr()), n,
+                                                  ctypes.c_void_p(events.data_ptr()), _stream_ptr(stream)))
+
+    def sync_status(self, stream=None) -> int:
+        return self._lib.decoder_sync_status(self._h, _stream_ptr(stream))
+
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            self._lib.decoder_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

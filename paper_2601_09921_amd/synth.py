@@ -212,6 +212,9 @@ def make_windows(wl: Workload, seed: int | None = None, B: int | None = None,
     for pair_p > 0 one diagonal pair flipped per round with probability pair_p; the
     measurements are M[0] ~ Bernoulli(0.5) and M[t+1] = M[t] xor flips[t].
 
+    Window w draws from its own generator, seeded with (seed, w), so the first k windows
+    of a large batch equal a batch of k windows.
+
     realistic_boundaries: initial windows get all-zero rows 0..b_left (no rounds exist
     before the experiment starts) and final windows hold the last core round's values for
     the rows after the core (no rounds exist after the experiment ends). With False every
@@ -222,30 +225,29 @@ def make_windows(wl: Workload, seed: int | None = None, B: int | None = None,
     seed = input_seed(wl.d) if seed is None else seed
     N, W = wl.N, wl.W
     types = window_types(B)
+    meas = np.zeros((B, W + 1, N), np.uint8)
     if zero:
-        return np.zeros((B, W + 1, N), np.uint8), types
-    rng = np.random.default_rng(seed)
-    m0 = (rng.random((B, 1, N)) < 0.5).astype(np.uint8)
-    flips = (rng.random((B, W, N)) < wl.p).astype(np.uint8)
-    if wl.pair_p > 0:
-        pairs = diagonal_pairs(wl.d)
-        hit = rng.random((B, W)) < wl.pair_p
-        choice = rng.integers(0, len(pairs), size=(B, W))
-        bw, tw = np.nonzero(hit)
-        for b, t in zip(bw, tw):
-            i, j = pairs[choice[b, t]]
-            flips[b, t, i] ^= 1
-            flips[b, t, j] ^= 1
-    if realistic_boundaries:
-        bl = wl.b_left
-        first = types == WIN_INITIAL
-        m0[first] = 0
-        flips[first, :bl, :] = 0          # rows 0..b_left stay zero
-        last = types == WIN_FINAL
-        flips[last, bl + wl.d:, :] = 0    # rows after the core hold their value
-    meas = np.concatenate([m0, flips], axis=1)
-    meas = np.bitwise_xor.accumulate(meas, axis=1)
-    return meas.astype(np.uint8), types
+        return meas, types
+    pairs = diagonal_pairs(wl.d) if wl.pair_p > 0 else None
+    bl = wl.b_left
+    rows = np.empty((W + 1, N), np.uint8)
+    for w in range(B):
+        rng = np.random.default_rng([seed, w])
+        rows[0] = rng.random(N) < 0.5
+        rows[1:] = rng.random((W, N)) < wl.p
+        if pairs is not None:
+            hit = np.nonzero(rng.random(W) < wl.pair_p)[0]
+            choice = rng.integers(0, len(pairs), size=W)
+            for t in hit:
+                i, j = pairs[choice[t]]
+                rows[1 + t, i] ^= 1
+                rows[1 + t, j] ^= 1
+        if realistic_boundaries and types[w] == WIN_INITIAL:
+            rows[:bl + 1] = 0                 # rows 0..b_left stay zero
+        if realistic_boundaries and types[w] == WIN_FINAL:
+            rows[bl + 1 + wl.d:] = 0          # rows after the core hold their value
+        np.bitwise_xor.accumulate(rows, axis=0, out=meas[w])
+    return meas, types
 
 
 def make_stream(N: int, T: int, p: float, seed: int) -> np.ndarray:

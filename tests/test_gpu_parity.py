@@ -1,0 +1,145 @@
+"""GPU parity of the HIP decoder against the fp64 oracle, through the C ABI.
+
+Small batches (several token tiles and a ragged tail) compare every window; at the full
+batch sizes of each workload, windows the oracle can afford are compared one by one and
+the rest are checked through batch invariance and output consistency."""
+import numpy as np
+import pytest
+
+from gpu_helpers import (check_bits, check_logits, decoder, gpu_decode, gpu_events, inputs,
+                         oracle, say, weights)
+from oracle import decoder as O
+from paper_2601_09921_amd import pwdec, synth
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+SMALL = {"d3": 64, "d7": 97, "d11": 13, "d17": 4, "d25": 3}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    pwdec.load_library()
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+@pytest.mark.parametrize("realistic", [True, False])
+def test_detection_events_bit_exact(name, realistic):
+    wl = synth.WORKLOADS[name]
+    B = max(SMALL[name], 6)
+    meas, types = inputs(name, B, realistic)
+    say(f"events {name} B={B} realistic={realistic}")
+    dec = decoder(name, max(B, SMALL[name]))
+    ev, rc = gpu_events(dec, meas, types, wl.W, wl.words)
+    assert rc == pwdec.PWD_OK
+    expect = O.pack_bits(O.detection_events(meas, types, wl.d))
+    assert np.array_equal(ev, expect)
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_logits_match_oracle(name):
+    B = SMALL[name]
+    meas, types = inputs(name, B)
+    say(f"decode {name} B={B}")
+    logits, bits, rc = gpu_decode(decoder(name, B), meas, types)
+    assert rc == pwdec.PWD_OK
+    o_logits, o_bits, _ = oracle(name, B)
+    check_logits(name, logits, o_logits)
+    check_bits(bits, o_logits)
+    assert np.array_equal(bits, (logits > 0).astype(np.uint8))
+
+
+@pytest.mark.parametrize("name", ["d3", "d7", "d11"])
+def test_masks_reach_the_network(name):
+    """Windows whose padded rows hold random measurements decode like the oracle, which
+    zeroes those events (App. A.1.1 boundary padding)."""
+    B = min(SMALL[name], 12)
+    meas, types = inputs(name, B, realistic=False)
+    say(f"decode {name} B={B} random padding rows")
+    logits, bits, rc = gpu_decode(decoder(name, SMALL[name]), meas, types)
+    assert rc == pwdec.PWD_OK
+    o_logits, _, _ = oracle(name, B, realistic=False)
+    check_logits(name, logits, o_logits)
+
+
+@pytest.mark.parametrize("name", ["d3", "d7", "d11", "d25"])
+def test_batch_invariance_and_repeatability(name):
+    B = SMALL[name]
+    meas, types = inputs(name, B)
+    dec = decoder(name, B)
+    say(f"batch invariance {name} B={B}")
+    full, fbits, _ = gpu_decode(dec, meas, types)
+    again, _, _ = gpu_decode(dec, meas, types)
+    assert np.array_equal(full.view(np.uint32), again.view(np.uint32))
+    for w in sorted({0, B // 2, B - 1}):
+        one, obits, _ = gpu_decode(dec, meas[w:w + 1], types[w:w + 1])
+        assert one.view(np.uint32)[0] == full.view(np.uint32)[w], f"window {w}"
+        assert obits[0] == fbits[w]
+    perm = np.random.default_rng(0).permutation(B)
+    pl, _, _ = gpu_decode(dec, meas[perm], types[perm])
+    assert np.array_equal(pl.view(np.uint32), full[perm].view(np.uint32))
+
+
+@pytest.mark.parametrize("name", ["d3", "d7", "d11"])
+def test_zero_syndromes(name):
+    B = 9
+    meas, types = inputs(name, B, zero=True)
+    say(f"zero syndromes {name}")
+    logits, _, rc = gpu_decode(decoder(name, max(B, SMALL[name])), meas, types)
+    assert rc == pwdec.PWD_OK
+    for t in range(3):
+        sel = logits[types == t]
+        assert (sel.view(np.uint32) == sel.view(np.uint32)[0]).all()
+    o_logits, _, _ = oracle(name, B, zero=True)
+    check_logits(name, logits, o_logits)
+
+
+@pytest.mark.parametrize("name", ["d3", "d7"])
+def test_invalid_type_and_batch_limits(name):
+    B = 6
+    meas, types = inputs(name, B)
+    dec = decoder(name, SMALL[name])
+    bad = types.copy()
+    bad[4] = 3
+    say(f"invalid type {name}")
+    logits, bits, rc = gpu_decode(dec, meas, bad)
+    assert rc == pwdec.PWD_EDEVICE
+    assert np.isnan(logits[4]) and bits[4] == 0
+    good, _, _ = gpu_decode(dec, meas, types)
+    ok = np.arange(B) != 4
+    assert np.array_equal(logits[ok].view(np.uint32), good[ok].view(np.uint32))
+    assert dec.sync_status() == pwdec.PWD_OK
+    # n = 0 is a no-op; n > max_windows is refused before any launch
+    z = torch.zeros(1, dtype=torch.float32, device="cuda")
+    zb = torch.zeros(1, dtype=torch.uint8, device="cuda")
+    mt = torch.zeros((1, 1), dtype=torch.int32, device="cuda")
+    dec.decode(mt, torch.zeros(0, dtype=torch.uint8, device="cuda"), z, zb)
+    big = SMALL[name] + 1
+    with pytest.raises(pwdec.PwdError) as ei:
+        dec.decode(torch.zeros((big, 1), dtype=torch.int32, device="cuda"),
+                   torch.zeros(big, dtype=torch.uint8, device="cuda"), z, zb)
+    assert ei.value.code == pwdec.PWD_EBATCH
+
+
+@pytest.mark.parametrize("name", ["d7", "d11", "d17", "d25"])
+def test_full_batch_sampled(name):
+    """The full batch of the workload, in the launch configuration the benchmark times:
+    the leading windows against the oracle, sampled windows against a batch of one."""
+    wl = synth.WORKLOADS[name]
+    B = wl.B
+    meas, types = inputs(name, B)
+    dec = decoder(name, B)
+    say(f"full batch {name} B={B}")
+    logits, bits, rc = gpu_decode(dec, meas, types)
+    assert rc == pwdec.PWD_OK
+    assert np.isfinite(logits).all()
+    assert np.array_equal(bits, (logits > 0).astype(np.uint8))
+    k = SMALL[name]
+    o_logits, _, _ = oracle(name, k)
+    check_logits(name, logits[:k], o_logits)
+    check_bits(bits[:k], o_logits)
+    for w in (B // 3 + 1, B - 1):
+        one, _, _ = gpu_decode(dec, meas[w:w + 1], types[w:w + 1])
+        assert one.view(np.uint32)[0] == logits.view(np.uint32)[w], f"window {w}"
