@@ -1,0 +1,219 @@
+"""Throughput benchmark of the parallel-window decoder on one MI355X.
+
+One step = one decode_windows call over the whole batch of the d=25 workload (8192
+windows of 50 rounds, 624 stabilizer tokens, D=256, 4 layers, 8 heads, MLP 4x, bf16),
+inputs already resident in HBM. The throughput accounting follows the paper's
+(Sec. 4.2): decoding time per round = time / (windows * d).
+
+Prints one JSON line with the metric, the per-stage kernel times (HIP events on the
+decode stream), the roofline of the dominant kernel, and the fp64 oracle timed on a
+bounded sample of the same workload on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+MFMA_BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+FP32_PEAK_TFLOPS = 157.3            # MI355X fp32 vector
+HBM_PEAK_GBS = 8000.0
+PAPER_US_PER_ROUND = {3: 0.781, 7: 0.789, 11: 0.812, 17: 0.841, 25: 0.979}   # one TPU v6e
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+STAGE_KERNELS = {
+    "embed_qkv": "tok_kernel<256, EMBED|QKV>",
+    "attention": "attn_kernel<32>",
+    "post_qkv": "tok_kernel<256, POST|QKV>",
+    "post_embed_qkv": "tok_kernel<256, POST|EMBED|QKV>",
+    "post": "tok_kernel<256, POST>",
+    "readout": "readout_kernel",
+    "fp32_window": "f32_window_kernel",
+}
+
+
+def stage_flops(wl, B):
+    """Algorithmic FLOPs of one launch of each stage (real tokens only)."""
+    N, D, F, d = wl.N, wl.D, wl.F, wl.d
+    qkv = 6 * N * D * D
+    post = 2 * N * D * D + 4 * N * D * F
+    attn = 4 * N * N * D
+    readout = 8 * d * d * D * D + 2 * d * D
+    per_window_all = wl.W * wl.L * (qkv + attn + post) + readout
+    return {
+        "embed_qkv": B * qkv,
+        "attention": B * attn,
+        "post_qkv": B * (post + qkv),
+        "post_embed_qkv": B * (post + qkv),
+        "post": B * post,
+        "readout": B * readout,
+        "fp32_window": B * per_window_all,
+    }, B * per_window_all
+
+
+def source_hash():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2601_09921_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        h.update(open(os.path.join(csrc, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(stage):
+    """HBM bytes per launch of `stage` from committed rocprofv3 counter runs, or None when
+    they were taken on other kernel sources."""
+    try:
+        t = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    if t.get("source_hash") != source_hash():
+        return None
+    return t.get("bytes_per_launch", {}).get(stage)
+
+
+def cpu_baseline(wl, weights, sample):
+    """The fp64 oracle on `sample` windows (one per window type) on the host cores."""
+    from oracle import decoder as O
+    from paper_2601_09921_amd import synth
+    try:
+        import threadpoolctl
+        info = threadpoolctl.threadpool_info()
+        cores = max([i.get("num_threads", 1) for i in info if i.get("user_api") == "blas"] or [1])
+    except Exception:
+        cores = 1
+    meas, types = synth.make_windows(wl, B=sample)
+    t0 = time.perf_counter()
+    O.forward_windows(meas, types, weights, wl.d, wl.H)
+    dt = time.perf_counter() - t0
+    return {
+        "value": sample * wl.d / dt,
+        "unit": "rounds/s",
+        "cores": int(cores),
+        "kind": "oracle",
+        "sample": f"{sample} windows (types {sorted(set(types.tolist()))}) of the {wl.name} workload, "
+                  f"fp64 numpy, {dt:.1f} s; windows are independent, so the rate holds for the full batch",
+        "seconds": dt,
+        "us_per_round": dt / (sample * wl.d) * 1e6,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="d25")
+    ap.add_argument("--cpu-sample", type=int, default=3, help="oracle windows for the CPU baseline (0: skip)")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: windows are independent, so more GPUs only split the "
+              "batch (see the sharding note in the design); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2601_09921_amd import pwdec, synth
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    pwdec.load_library()
+    wl = synth.WORKLOADS[args.workload]
+    B = wl.B
+    weights = synth.make_weights(wl)
+    meas, types = synth.make_windows(wl)
+    dev_meas = torch.from_numpy(synth.pack_bits(meas).view(np.int32)).cuda()
+    dev_types = torch.from_numpy(types).cuda()
+    logits = torch.empty(B, dtype=torch.float32, device="cuda")
+    bits = torch.empty(B, dtype=torch.uint8, device="cuda")
+    dec = pwdec.Decoder.from_workload(wl, weights)
+    stream = torch.cuda.current_stream()
+
+    for _ in range(args.warmup):
+        dec.decode(dev_meas, dev_types, logits, bits, stream)
+    torch.cuda.synchronize()
+    if dec.sync_status() != pwdec.PWD_OK:
+        raise RuntimeError("decoder reported a device error")
+
+    dec.profile(True)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        dec.decode(dev_meas, dev_types, logits, bits, stream)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    stages = dec.profile_read()
+    dec.profile(False)
+    ev_ms = ev0.elapsed_time(ev1)
+    step_s = wall / args.steps
+    assert np.isfinite(logits.cpu().numpy()).all()
+
+    flops, step_flops = stage_flops(wl, B)
+    stage_stats = {}
+    for name, (ms, n) in stages.items():
+        avg = ms / n
+        stage_stats[name] = {
+            "kernel": STAGE_KERNELS[name], "launches_per_step": n // args.steps,
+            "avg_ms": round(avg, 4), "share": round(ms / (ev_ms or 1), 4),
+            "tflops": round(flops[name] / (avg * 1e-3) / 1e12, 1),
+        }
+    dom = max(stages, key=lambda k: stages[k][0])
+    dom_avg_s = stages[dom][0] / stages[dom][1] * 1e-3
+    bf16 = wl.dtype == synth.DTYPE_BF16
+    peak = MFMA_BF16_PEAK_TFLOPS if bf16 else FP32_PEAK_TFLOPS
+    achieved = flops[dom] / dom_avg_s / 1e12
+    rounds = B * wl.d
+    out = {
+        "metric": "decoding rounds/s (one MI355X), us per round = time/(windows*d)",
+        "value": rounds / step_s,
+        "unit": "rounds/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": step_s * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if bf16 else "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{wl.name}: rotated surface code d={wl.d}, {wl.N} stabilizer tokens, "
+                        f"{wl.W}-round windows ({wl.d}-round core), {B} windows (initial/bulk/final mix), "
+                        f"Bernoulli({wl.p}) detection events; decoder D={wl.D}, {wl.L} layers, "
+                        f"{wl.H} heads, MLP {wl.mlp_ratio}x, random-init weights",
+            "distance": wl.d, "windows": B, "window_rounds": wl.W, "tokens": wl.N,
+        },
+        "us_per_round": step_s / rounds * 1e6,
+        "rnn_steps_per_s": B * wl.W / step_s,
+        "event_ms_per_step": ev_ms / args.steps,
+        "flop_per_step": step_flops,
+        "mfma_frac_call": step_flops / step_s / 1e12 / peak,
+        "floor_us_per_round_at_peak": step_flops / (peak * 1e12) / rounds * 1e6,
+        "paper_us_per_round_tpu_v6e": PAPER_US_PER_ROUND.get(wl.d),
+        "stages": stage_stats,
+        "roofline": {
+            "bound": "mfma" if bf16 else "alu",
+            "kernel": STAGE_KERNELS[dom],
+            "achieved": round(achieved, 1),
+            "peak": peak,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / peak, 4),
+            "traffic": load_traffic(dom),
+        },
+    }
+    dec.close()
+    if args.cpu_sample > 0:
+        out["cpu_baseline"] = cpu_baseline(wl, weights, args.cpu_sample)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -142,6 +142,33 @@ int decoder_sync_status(pwd_decoder* dec, void* hip_stream);
  * call on this thread. */
 const char* decoder_last_error(void);
 
+/* Kernel stages of decode_windows, for per-stage timing. */
+enum {
+    PWD_STAGE_EMBED_QKV = 0,      /* round-0 embedding + layer-0 Q/K/V projection */
+    PWD_STAGE_ATTENTION = 1,      /* multi-head self-attention, one launch per layer and round */
+    PWD_STAGE_POST_QKV = 2,       /* out-projection, LayerNorms, feed-forward + next layer's Q/K/V */
+    PWD_STAGE_POST_EMBED_QKV = 3, /* last layer of a round + next round's embedding and Q/K/V */
+    PWD_STAGE_POST = 4,           /* last layer of the last round */
+    PWD_STAGE_READOUT = 5,        /* readout */
+    PWD_STAGE_FP32_WINDOW = 6,    /* the whole fp32 decoder (fp32 configurations) */
+    PWD_NUM_STAGES = 7
+};
+
+typedef struct {
+    double ms[PWD_NUM_STAGES];       /* summed kernel time per stage, milliseconds */
+    int64_t launches[PWD_NUM_STAGES];
+} pwd_stage_times;
+
+/* Turns per-stage kernel timing on (enable != 0) or off. While on, decode_windows records a
+ * pair of HIP events around each kernel launch on its stream (no synchronisation inside the
+ * call); the times accumulate until decoder_profile_read. Turning it on clears what was
+ * accumulated. Costs one event record per launch. */
+int decoder_profile(pwd_decoder* dec, int enable);
+
+/* Synchronises the events recorded since the last read, adds their elapsed times to *out
+ * (which the caller zeroes first) and releases them. PWD_EINVAL if out is NULL. */
+int decoder_profile_read(pwd_decoder* dec, pwd_stage_times* out);
+
 /* Frees the device memory of the handle. NULL is accepted. The caller must make sure no
  * work of this handle is still running. */
 int decoder_destroy(pwd_decoder* dec);

@@ -115,7 +115,41 @@ struct pwd_decoder {
     const int* cell_token = nullptr;
     const float* f32w = nullptr;   // fp32 path: the blob tensors as given
     float bo_out = 0.f, beta[3] = {0.f, 0.f, 0.f};
+    // per-stage timing (decoder_profile)
+    bool profiling = false;
+    struct Mark { hipEvent_t begin, end; int stage; };
+    std::vector<Mark> marks;       // recorded, not yet read
+    std::vector<hipEvent_t> spare; // released events for reuse
 };
+
+namespace {
+
+hipEvent_t take_event(pwd_decoder* dec) {
+    if (!dec->spare.empty()) {
+        hipEvent_t e = dec->spare.back();
+        dec->spare.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+// Launches `launch` on stream s; with profiling on, brackets it with an event pair.
+template <class Fn>
+hipError_t timed(pwd_decoder* dec, int stage, hipStream_t s, Fn launch) {
+    if (!dec->profiling) return launch();
+    hipEvent_t b = take_event(dec), e = take_event(dec);
+    if (!b || !e) return hipErrorOutOfMemory;
+    hipError_t err = hipEventRecord(b, s);
+    if (err == hipSuccess) err = launch();
+    if (err == hipSuccess) err = hipEventRecord(e, s);
+    if (err != hipSuccess) return err;
+    dec->marks.push_back({b, e, stage});
+    return hipSuccess;
+}
+
+}  // namespace
 
 extern "C" {
 
@@ -354,6 +388,11 @@ int decoder_destroy(pwd_decoder* dec) {
     (void)hipFree(dec->QKV);
     (void)hipFree(dec->Y);
     (void)hipFree(dec->err);
+    for (auto& m : dec->marks) {
+        (void)hipEventDestroy(m.begin);
+        (void)hipEventDestroy(m.end);
+    }
+    for (auto e : dec->spare) (void)hipEventDestroy(e);
     delete dec;
     return PWD_OK;
 }
@@ -394,7 +433,7 @@ int decode_windows(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_ty
         p.err = dec->err;
         p.D = dec->D; p.L = dec->L; p.H = dec->H; p.F = dec->F;
         p.kappa = dec->kappa; p.eps = dec->eps;
-        HIP_OK(launch_f32_window(p, s));
+        HIP_OK(timed(dec, PWD_STAGE_FP32_WINDOW, s, [&] { return launch_f32_window(p, s); }));
         return PWD_OK;
     }
 
@@ -432,20 +471,20 @@ int decode_windows(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_ty
     // round 0: embed (state D_0 = 0) and project layer 0
     tp.t = 0;
     set_qkv(0);
-    HIP_OK(launch_tok(dec->D, TOK_EMBED | TOK_QKV, tp, n_tb, s));
+    HIP_OK(timed(dec, PWD_STAGE_EMBED_QKV, s, [&] { return launch_tok(dec->D, TOK_EMBED | TOK_QKV, tp, n_tb, s); }));
     for (int t = 0; t < dec->W; ++t) {
         for (int l = 0; l < dec->L; ++l) {
-            HIP_OK(launch_attn(dec->dh, ap, (int)n, s));
+            HIP_OK(timed(dec, PWD_STAGE_ATTENTION, s, [&] { return launch_attn(dec->dh, ap, (int)n, s); }));
             set_post(l);
             if (l + 1 < dec->L) {
                 set_qkv(l + 1);
-                HIP_OK(launch_tok(dec->D, TOK_POST | TOK_QKV, tp, n_tb, s));
+                HIP_OK(timed(dec, PWD_STAGE_POST_QKV, s, [&] { return launch_tok(dec->D, TOK_POST | TOK_QKV, tp, n_tb, s); }));
             } else if (t + 1 < dec->W) {
                 tp.t = t + 1;          // fold the next round's embedding into D_t
                 set_qkv(0);
-                HIP_OK(launch_tok(dec->D, TOK_POST | TOK_EMBED | TOK_QKV, tp, n_tb, s));
+                HIP_OK(timed(dec, PWD_STAGE_POST_EMBED_QKV, s, [&] { return launch_tok(dec->D, TOK_POST | TOK_EMBED | TOK_QKV, tp, n_tb, s); }));
             } else {
-                HIP_OK(launch_tok(dec->D, TOK_POST, tp, n_tb, s));
+                HIP_OK(timed(dec, PWD_STAGE_POST, s, [&] { return launch_tok(dec->D, TOK_POST, tp, n_tb, s); }));
             }
         }
     }
@@ -465,7 +504,7 @@ int decode_windows(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_ty
     rp.d = dec->d;
     rp.D = dec->D;
     rp.nbw = dec->nbw;
-    HIP_OK(launch_readout(rp, s));
+    HIP_OK(timed(dec, PWD_STAGE_READOUT, s, [&] { return launch_readout(rp, s); }));
     return PWD_OK;
 }
 
@@ -498,6 +537,37 @@ int decoder_sync_status(pwd_decoder* dec, void* hip_stream) {
         HIP_OK(hipMemset(dec->err, 0, sizeof(int)));
         return fail(PWD_EDEVICE, "a window had an invalid type (> 2)");
     }
+    return PWD_OK;
+}
+
+int decoder_profile(pwd_decoder* dec, int enable) {
+    if (!dec) return fail(PWD_EINVAL, "null decoder");
+    DeviceGuard dg(dec->device);
+    HIP_OK(dg.err);
+    for (auto& m : dec->marks) {
+        HIP_OK(hipEventSynchronize(m.end));
+        dec->spare.push_back(m.begin);
+        dec->spare.push_back(m.end);
+    }
+    dec->marks.clear();
+    dec->profiling = enable != 0;
+    return PWD_OK;
+}
+
+int decoder_profile_read(pwd_decoder* dec, pwd_stage_times* out) {
+    if (!dec || !out) return fail(PWD_EINVAL, "null decoder or output");
+    DeviceGuard dg(dec->device);
+    HIP_OK(dg.err);
+    for (auto& m : dec->marks) {
+        HIP_OK(hipEventSynchronize(m.end));
+        float ms = 0.f;
+        HIP_OK(hipEventElapsedTime(&ms, m.begin, m.end));
+        out->ms[m.stage] += ms;
+        out->launches[m.stage] += 1;
+        dec->spare.push_back(m.begin);
+        dec->spare.push_back(m.end);
+    }
+    dec->marks.clear();
     return PWD_OK;
 }
 

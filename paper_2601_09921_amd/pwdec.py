@@ -39,6 +39,14 @@ class ModelDims(ctypes.Structure):
                 ("mlp_ratio", ctypes.c_int32), ("dtype", ctypes.c_int32)]
 
 
+NUM_STAGES = 7
+STAGE_NAMES = ["embed_qkv", "attention", "post_qkv", "post_embed_qkv", "post", "readout", "fp32_window"]
+
+
+class StageTimes(ctypes.Structure):
+    _fields_ = [("ms", ctypes.c_double * NUM_STAGES), ("launches", ctypes.c_int64 * NUM_STAGES)]
+
+
 _lib = None
 
 
@@ -60,6 +68,8 @@ def load_library() -> ctypes.CDLL:
         "decoder_sync_status": (ctypes.c_int, [VP, VP]),
         "decoder_last_error": (ctypes.c_char_p, []),
         "decoder_destroy": (ctypes.c_int, [VP]),
+        "decoder_profile": (ctypes.c_int, [VP, ctypes.c_int]),
+        "decoder_profile_read": (ctypes.c_int, [VP, P(StageTimes)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -148,6 +158,16 @@ class Decoder:
 
     def sync_status(self, stream=None) -> int:
         return self._lib.decoder_sync_status(self._h, _stream_ptr(stream))
+
+    def profile(self, enable: bool):
+        """Per-stage kernel timing with HIP events on the decode stream (on/off)."""
+        _check(self._lib.decoder_profile(self._h, 1 if enable else 0))
+
+    def profile_read(self) -> dict:
+        """{stage: (total ms, launches)} of the launches recorded since the last read."""
+        st = StageTimes()
+        _check(self._lib.decoder_profile_read(self._h, ctypes.byref(st)))
+        return {STAGE_NAMES[i]: (st.ms[i], st.launches[i]) for i in range(NUM_STAGES) if st.launches[i]}
 
     def close(self):
         if getattr(self, "_h", None) is not None and self._h.value:
