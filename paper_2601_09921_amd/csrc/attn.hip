@@ -2,60 +2,125 @@
 // model table's Multi-Head Attention), bf16 MFMA with fp32 softmax statistics.
 //
 // One workgroup per (window, head). K_h (as MFMA A fragments) and V_h^T are staged in LDS
-// once; each wavefront then takes 16-query blocks and streams the keys in steps of 32:
-//   S^T = K Q^T             (16 keys x 16 queries per MFMA, lanes hold queries)
-//   online softmax           (running max and sum per query, exp2 with log2(e)/sqrt(dh))
-//   O^T += V^T P^T           (P^T is the S^T accumulator rounded to bf16, no shuffle)
-// Padding keys (index >= N) get probability 0. The output is written as the B fragments
-// the out-projection consumes.
+// once; each wavefront then takes pairs of 16-query blocks and streams the keys in steps of
+// 32:
+//   S^T = K Q'^T - m      (16 keys x 16 queries per MFMA, lanes hold queries)
+//   P^T = exp2(S^T)       (P^T is the S^T accumulator rounded to bf16, no shuffle)
+//   O^T += V^T P^T,  l += sum P
+// Q' = Q log2(e)/sqrt(dh) comes pre-scaled from the Q/K/V projection, so S is in log2 units.
+// The shift m of a query is the Cauchy-Schwarz bound |q'| max_k |k| >= every score of the
+// row; softmax is shift-invariant, so this is the exact softmax without a running maximum
+// or rescaling, and m enters as the initial value of the MFMA accumulator. Should a row's
+// sum underflow (a bound far above the true maximum), that query block is recomputed with
+// the running-maximum form. Padding keys (index >= N) get probability 0. The output is
+// written as the B fragments the out-projection consumes.
 #include "common.h"
 #include "kernels.h"
 
 namespace {
 
 constexpr int WAVES = 4;
+constexpr int QB = 2;                 // query blocks per wavefront pass
 
 __host__ __device__ inline int vt_stride(int Npad) { return ((Npad + 31) & ~31) + 8; }   // + 8: spread banks
 
+PWD_DEV float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+
+template <int DH>
+struct Frag;
+template <>
+struct Frag<32> {
+    using T = bf16x8;
+    static __device__ __forceinline__ f32x4 mma(T a, T b, f32x4 c) { return mfma16x16x32(a, b, c); }
+};
+template <>
+struct Frag<16> {
+    using T = bf16x4;
+    static __device__ __forceinline__ f32x4 mma(T a, T b, f32x4 c) { return mfma16x16x16(a, b, c); }
+};
+
+template <int DH>
+PWD_DEV typename Frag<DH>::T ld_kfrag(const uint16_t* ks, int kb, int lane) {
+    if constexpr (DH == 32)
+        return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(ks + (kb * 64 + lane) * 8));
+    else
+        return __builtin_bit_cast(bf16x4, *reinterpret_cast<const u16x4*>(ks + (kb * 64 + lane) * 4));
+}
+
+// V^T A fragment of row tile rt for the 32 keys of superblock sb (k slots kslot(g, i)).
+PWD_DEV bf16x8 ld_vfrag(const uint16_t* vt, int vts, int rt, int sb, int col, int g) {
+    const uint16_t* row = vt + (rt * 16 + col) * vts + 32 * sb + 4 * g;
+    const u16x4 lo = *reinterpret_cast<const u16x4*>(row);
+    const u16x4 hi = *reinterpret_cast<const u16x4*>(row + 16);
+    u16x8 v;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        v[i] = lo[i];
+        v[4 + i] = hi[i];
+    }
+    return __builtin_bit_cast(bf16x8, v);
+}
+
+PWD_DEV float sum4(float v) {
+    v += __shfl_xor(v, 16);
+    return v + __shfl_xor(v, 32);
+}
+
 template <int DH>
 __global__ __launch_bounds__(WAVES * 64) void attn_kernel(AttnParams p) {
+    using FT = typename Frag<DH>::T;
     constexpr int RT = DH / 16;                 // 16-row tiles of O^T
+    constexpr int NV = DH == 32 ? 8 : 4;        // Q/K values per lane
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int g = lane >> 4, col = lane & 15;
     const int win = blockIdx.x / p.H, h = blockIdx.x % p.H;
-    const int nbw = p.nbw;
-    const int KSD = p.H * DH / 32;              // k-steps of D (fragments per Q/K/V)
+    const int nbw = p.nbw, N = p.N;
+    const int KSD = p.H * DH / 32;              // fragments per Q/K/V of a token block
     const int64_t tb_base = (int64_t)win * nbw;
     const int vts = vt_stride(p.Npad);
 
     extern __shared__ __align__(16) unsigned char smem[];
-    // K fragments: DH 32 -> 8 bf16 per lane, DH 16 -> 4 bf16 per lane
     uint16_t* ks = reinterpret_cast<uint16_t*>(smem);
-    uint16_t* vt = ks + (size_t)nbw * 64 * (DH == 32 ? 8 : 4);
+    uint16_t* vt = ks + (size_t)nbw * 64 * NV;
+    __shared__ float kmax_w[WAVES];
 
     // fragment and slot range of head h inside a Q/K/V fragment
     const int frag = DH == 32 ? h : h / 2;
     const int slot0 = DH == 32 ? 0 : (h % 2) * 4;
 
+    // ---- stage K (A fragments) and V^T; track max |k| over the real keys
+    float kmax2 = 0.f;
     for (int kb = wave; kb < nbw; kb += WAVES) {
-        const uint16_t* src = p.QKV + (((tb_base + kb) * 3 + 1) * KSD + frag) * 512 + lane * 8;
-        const u16x8 kv = *reinterpret_cast<const u16x8*>(src);
-        if (DH == 32) {
-            *reinterpret_cast<u16x8*>(ks + (kb * 64 + lane) * 8) = kv;
-        } else {
-            u16x4 k4;
-            for (int i = 0; i < 4; ++i) k4[i] = kv[slot0 + i];
-            *reinterpret_cast<u16x4*>(ks + (kb * 64 + lane) * 4) = k4;
+        const u16x8 kv = *reinterpret_cast<const u16x8*>(
+            p.QKV + (((tb_base + kb) * 3 + 1) * KSD + frag) * 512 + lane * 8);
+        float n2 = 0.f;
+        u16x4 k4;
+#pragma unroll
+        for (int i = 0; i < NV; ++i) {
+            const uint16_t u = kv[slot0 + i];
+            const float f = (float)__builtin_bit_cast(__bf16, u);
+            n2 = fmaf(f, f, n2);
+            if (DH == 16) k4[i] = u;
         }
-        const uint16_t* vsrc = p.QKV + (((tb_base + kb) * 3 + 2) * KSD + frag) * 512 + lane * 8;
-        const u16x8 vv = *reinterpret_cast<const u16x8*>(vsrc);
+        if (DH == 32) *reinterpret_cast<u16x8*>(ks + (kb * 64 + lane) * 8) = kv;
+        else *reinterpret_cast<u16x4*>(ks + (kb * 64 + lane) * 4) = k4;
+        n2 = sum4(n2);
+        if (kb * 16 + col < N) kmax2 = fmaxf(kmax2, n2);
+
+        const u16x8 vv = *reinterpret_cast<const u16x8*>(
+            p.QKV + (((tb_base + kb) * 3 + 2) * KSD + frag) * 512 + lane * 8);
         const int key = kb * 16 + col;
         if (DH == 32) {
+#pragma unroll
             for (int i = 0; i < 8; ++i) vt[kslot(g, i) * vts + key] = vv[i];
         } else {
+#pragma unroll
             for (int i = 0; i < 4; ++i) vt[(4 * g + i) * vts + key] = vv[slot0 + i];
         }
     }
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) kmax2 = fmaxf(kmax2, __shfl_xor(kmax2, off));
+    if (lane == 0) kmax_w[wave] = kmax2;
     // zero the key tail [Npad, 32*ceil(Npad/32)) so P = 0 never meets garbage
     const int kpad = (p.Npad + 31) & ~31;
     for (int idx = threadIdx.x; idx < DH * (kpad - p.Npad); idx += blockDim.x) {
@@ -63,80 +128,136 @@ __global__ __launch_bounds__(WAVES * 64) void attn_kernel(AttnParams p) {
         vt[r * vts + k] = 0;
     }
     __syncthreads();
+    float kmax = 0.f;
+#pragma unroll
+    for (int w = 0; w < WAVES; ++w) kmax = fmaxf(kmax, kmax_w[w]);
+    kmax = sqrtf(kmax);
 
-    const float c = p.scale_log2;
     const int nsb = (nbw + 1) / 2;
-    for (int qb = wave; qb < nbw; qb += WAVES) {
-        const uint16_t* qsrc = p.QKV + (((tb_base + qb) * 3 + 0) * KSD + frag) * 512 + lane * 8;
-        const u16x8 qv = *reinterpret_cast<const u16x8*>(qsrc);
-        bf16x8 q8 = __builtin_bit_cast(bf16x8, qv);
-        bf16x4 q4;
-        for (int i = 0; i < 4; ++i) q4[i] = q8[slot0 + i];
+    const bool tail_mask = nsb * 32 > N;        // the last superblock holds padding keys
+    for (int qb0 = wave * QB; qb0 < nbw; qb0 += WAVES * QB) {
+        FT q[QB];
+        f32x4 shift[QB];
+        float m[QB];
+#pragma unroll
+        for (int j = 0; j < QB; ++j) {
+            const int qb = min(qb0 + j, nbw - 1);    // a lone last block computes a duplicate
+            const u16x8 qv = *reinterpret_cast<const u16x8*>(
+                p.QKV + (((tb_base + qb) * 3 + 0) * KSD + frag) * 512 + lane * 8);
+            float n2 = 0.f;
+#pragma unroll
+            for (int i = 0; i < NV; ++i) {
+                const float f = (float)__builtin_bit_cast(__bf16, (uint16_t)qv[slot0 + i]);
+                n2 = fmaf(f, f, n2);
+                q[j][i] = __builtin_bit_cast(__bf16, (uint16_t)qv[slot0 + i]);
+            }
+            m[j] = sqrtf(sum4(n2)) * kmax;
+            shift[j] = f32x4{-m[j], -m[j], -m[j], -m[j]};
+        }
 
-        f32x4 o[RT];
-        for (int rt = 0; rt < RT; ++rt) o[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-        float m = -INFINITY, l = 0.f;
+        f32x4 o[QB][RT];
+        float l[QB];
+#pragma unroll
+        for (int j = 0; j < QB; ++j) {
+            l[j] = 0.f;
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) o[j][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
 
         for (int sb = 0; sb < nsb; ++sb) {
-            f32x4 s[2];
-            for (int j = 0; j < 2; ++j) {
-                const int kb = 2 * sb + j;
+            f32x4 s[QB][2];
+#pragma unroll
+            for (int kk = 0; kk < 2; ++kk) {
+                const int kb = 2 * sb + kk;
                 if (kb < nbw) {
-                    const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
-                    if (DH == 32) {
-                        const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(ks + (kb * 64 + lane) * 8));
-                        s[j] = mfma16x16x32(a, q8, zero);
-                    } else {
-                        const bf16x4 a = __builtin_bit_cast(bf16x4, *reinterpret_cast<const u16x4*>(ks + (kb * 64 + lane) * 4));
-                        s[j] = mfma16x16x16(a, q4, zero);
-                    }
-                    for (int i = 0; i < 4; ++i)
-                        if (kb * 16 + 4 * g + i >= p.N) s[j][i] = -INFINITY;
+                    const FT a = ld_kfrag<DH>(ks, kb, lane);
+#pragma unroll
+                    for (int j = 0; j < QB; ++j) s[j][kk] = Frag<DH>::mma(a, q[j], shift[j]);
                 } else {
-                    s[j] = f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+#pragma unroll
+                    for (int j = 0; j < QB; ++j) s[j][kk] = f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
                 }
             }
-            float mx = fmaxf(fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3])),
-                             fmaxf(fmaxf(s[1][0], s[1][1]), fmaxf(s[1][2], s[1][3])));
-            mx = fmaxf(mx, __shfl_xor(mx, 16));
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
-            const float mnew = fmaxf(m, mx);
-            const float alpha = exp2f((m - mnew) * c);
-            const float mc = mnew * c;
-            f32x4 pr[2];
-            float ls = 0.f;
-            for (int j = 0; j < 2; ++j)
-                for (int i = 0; i < 4; ++i) {
-                    pr[j][i] = exp2f(s[j][i] * c - mc);
-                    ls += pr[j][i];
-                }
-            l = l * alpha + ls;
-            m = mnew;
-            const bf16x8 pb = pack_b(pr[0], pr[1]);
+            if (tail_mask && sb == nsb - 1) {
+#pragma unroll
+                for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        if ((2 * sb + kk) * 16 + 4 * g + i >= N)
+#pragma unroll
+                            for (int j = 0; j < QB; ++j) s[j][kk][i] = -INFINITY;
+            }
+            bf16x8 pb[QB];
+#pragma unroll
+            for (int j = 0; j < QB; ++j) {
+                f32x4 pr[2];
+#pragma unroll
+                for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) pr[kk][i] = exp2_fast(s[j][kk][i]);
+                l[j] += ((pr[0][0] + pr[0][1]) + (pr[0][2] + pr[0][3])) + ((pr[1][0] + pr[1][1]) + (pr[1][2] + pr[1][3]));
+                pb[j] = pack_b(pr[0], pr[1]);
+            }
+#pragma unroll
             for (int rt = 0; rt < RT; ++rt) {
-                const uint16_t* row = vt + (rt * 16 + col) * vts + 32 * sb + 4 * g;
-                u16x8 v;
-                const u16x4 lo = *reinterpret_cast<const u16x4*>(row);
-                const u16x4 hi = *reinterpret_cast<const u16x4*>(row + 16);
-                for (int i = 0; i < 4; ++i) {
-                    v[i] = lo[i];
-                    v[4 + i] = hi[i];
-                }
-                o[rt] = o[rt] * alpha;
-                o[rt] = mfma16x16x32(__builtin_bit_cast(bf16x8, v), pb, o[rt]);
+                const bf16x8 v = ld_vfrag(vt, vts, rt, sb, col, g);
+#pragma unroll
+                for (int j = 0; j < QB; ++j) o[j][rt] = mfma16x16x32(v, pb[j], o[j][rt]);
             }
         }
-        l += __shfl_xor(l, 16);
-        l += __shfl_xor(l, 32);
-        const float inv = 1.0f / l;
-        uint16_t* dst = p.Y + ((tb_base + qb) * KSD + frag) * 512 + lane * 8;
-        if constexpr (DH == 32) {
-            const bf16x8 out = pack_b(o[0] * inv, o[RT - 1] * inv);
-            *reinterpret_cast<u16x8*>(dst) = __builtin_bit_cast(u16x8, out);
-        } else {
-            u16x4 out;
-            for (int i = 0; i < 4; ++i) out[i] = __builtin_bit_cast(uint16_t, (__bf16)(o[0][i] * inv));
-            *reinterpret_cast<u16x4*>(dst + slot0) = out;
+
+#pragma unroll
+        for (int j = 0; j < QB; ++j) {
+            const int qb = qb0 + j;
+            float lt = sum4(l[j]);
+            // underflowed row sums: redo this block with a running maximum (wave-uniform)
+            if (__builtin_amdgcn_ballot_w64(lt < 1e-30f) != 0) {
+                float mm = -INFINITY, ll = 0.f;
+#pragma unroll
+                for (int rt = 0; rt < RT; ++rt) o[j][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+                const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+                for (int sb = 0; sb < nsb; ++sb) {
+                    f32x4 s2[2];
+                    for (int kk = 0; kk < 2; ++kk) {
+                        const int kb = 2 * sb + kk;
+                        if (kb < nbw) s2[kk] = Frag<DH>::mma(ld_kfrag<DH>(ks, kb, lane), q[j], zero);
+                        else s2[kk] = f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+                        for (int i = 0; i < 4; ++i)
+                            if (kb * 16 + 4 * g + i >= N) s2[kk][i] = -INFINITY;
+                    }
+                    float mx = fmaxf(fmaxf(fmaxf(s2[0][0], s2[0][1]), fmaxf(s2[0][2], s2[0][3])),
+                                     fmaxf(fmaxf(s2[1][0], s2[1][1]), fmaxf(s2[1][2], s2[1][3])));
+                    mx = fmaxf(mx, __shfl_xor(mx, 16));
+                    mx = fmaxf(mx, __shfl_xor(mx, 32));
+                    const float mnew = fmaxf(mm, mx);
+                    const float alpha = exp2_fast(mm - mnew);
+                    f32x4 pr[2];
+                    float ls = 0.f;
+                    for (int kk = 0; kk < 2; ++kk)
+                        for (int i = 0; i < 4; ++i) {
+                            pr[kk][i] = exp2_fast(s2[kk][i] - mnew);
+                            ls += pr[kk][i];
+                        }
+                    ll = ll * alpha + ls;
+                    mm = mnew;
+                    const bf16x8 pb2 = pack_b(pr[0], pr[1]);
+                    for (int rt = 0; rt < RT; ++rt)
+                        o[j][rt] = mfma16x16x32(ld_vfrag(vt, vts, rt, sb, col, g), pb2, o[j][rt] * alpha);
+                }
+                lt = sum4(ll);
+            }
+            if (qb >= nbw) continue;
+            const float inv = 1.0f / lt;
+            uint16_t* dst = p.Y + ((tb_base + qb) * KSD + frag) * 512 + lane * 8;
+            if constexpr (DH == 32) {
+                const bf16x8 out = pack_b(o[j][0] * inv, o[j][RT - 1] * inv);
+                *reinterpret_cast<u16x8*>(dst) = __builtin_bit_cast(u16x8, out);
+            } else {
+                u16x4 out;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) out[i] = __builtin_bit_cast(uint16_t, (__bf16)(o[j][0][i] * inv));
+                *reinterpret_cast<u16x4*>(dst + slot0) = out;
+            }
         }
     }
 }

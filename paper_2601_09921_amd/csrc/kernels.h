@@ -19,24 +19,23 @@ struct TokParams {
     int Npad, nbw;          // padded tokens and 16-token blocks per window
     int t;                  // round whose embedding TOK_EMBED adds
     float kappa, eps;
+    float qscale;           // log2(e)/sqrt(dh): Q is stored pre-scaled for exp2-based softmax
     float* X;               // fp32 residual / state, C fragments
     uint16_t* QKV;          // bf16 B fragments [tb][3][D/32][64][8]
     const uint16_t* Y;      // bf16 attention output [tb][D/32][64][8]
     const float* S0;        // b_e + PE, fp32 C fragments [nbw][D/16][64][4] (0 on padding)
     const float* we;        // [D]
-    // layer weights of the POST stage (A fragments bf16, vectors fp32)
-    const uint16_t *Wo, *W1, *W2;
-    const float *bo, *g1, *be1, *b1, *b2, *g2, *be2;
-    // QKV projection of the layer that follows (A fragments of [3D out][D in]), bias [3D]
-    const uint16_t* Wqkv;
-    const float* bqkv;
+    // weight streams: bf16 A fragments in consumption order (see tok.hip)
+    const uint16_t* post_stream;   // out-projection + feed-forward of the POST layer
+    const uint16_t* qkv_stream;    // Q/K/V projection of the layer that follows
+    const float *bo, *g1, *be1, *b1, *b2, *g2, *be2;   // POST layer vectors
+    const float* bqkv;                                  // [3D] bias of the Q/K/V projection
 };
 
 struct AttnParams {
     const uint16_t* QKV;
     uint16_t* Y;
-    int N, Npad, nbw, H;
-    float scale_log2;       // log2(e) / sqrt(dh)
+    int N, Npad, nbw, H;    // Q arrives pre-scaled by log2(e)/sqrt(dh)
 };
 
 struct ReadoutParams {
@@ -45,7 +44,7 @@ struct ReadoutParams {
     float* logits;
     uint8_t* bits;
     int* err;               // device error word
-    const float* Wc;        // [2][2][D][D] fp32 ([a][b][in][out])
+    const uint16_t* Wc;     // bf16 A fragments of Wc^T: [D/16][4D/32][64][8], k = tap*D + in
     const float* bc;        // [D]
     const float* wo;        // [d][D]
     float bo;
@@ -73,6 +72,8 @@ struct F32Params {
 };
 
 hipError_t launch_events(const EventsParams& p, hipStream_t s);
+int64_t tok_block_granule();
+int tok_mlp_chunk(int D);
 hipError_t launch_tok(int D, int flags, const TokParams& p, int64_t n_tb, hipStream_t s);
 hipError_t launch_attn(int dh, const AttnParams& p, int nwin, hipStream_t s);
 hipError_t launch_readout(const ReadoutParams& p, hipStream_t s);

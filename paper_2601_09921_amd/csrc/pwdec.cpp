@@ -14,8 +14,6 @@
 #include "../../include/pwdec.h"
 #include "kernels.h"
 
-int64_t tok_block_granule();
-
 namespace {
 
 thread_local std::string g_last_error;
@@ -85,6 +83,42 @@ std::vector<std::pair<int, int>> stabilizer_cells(int d) {
     return cells;
 }
 
+// Weight streams of the token kernel: the A fragments of each GEMM in the order the kernel
+// consumes them. post: Wo (row tile, k-step), then per feed-forward chunk c the W1
+// fragments of its CH hidden units (row tile, k-step) followed by the W2 fragments of its
+// k-steps (row tile, k-step). qkv: per 32-feature output group og, per k-step, the two
+// row tiles 2og and 2og+1.
+void append_post_stream(std::vector<uint16_t>& out, const float* Wo, const float* W1, const float* W2, int D, int CH) {
+    const int F = 4 * D, RT = D / 16, KS = D / 32, FKS = F / 32;
+    std::vector<uint16_t> fo, f1, f2;
+    append_frags(fo, Wo, D, D);
+    append_frags(f1, W1, D, F);
+    append_frags(f2, W2, F, D);
+    auto frag = [&](const std::vector<uint16_t>& v, int ro, int ks, int nks) {
+        out.insert(out.end(), v.begin() + ((size_t)ro * nks + ks) * 512, v.begin() + ((size_t)ro * nks + ks + 1) * 512);
+    };
+    for (int rt = 0; rt < RT; ++rt)
+        for (int ks = 0; ks < KS; ++ks) frag(fo, rt, ks, KS);
+    for (int c = 0; c < F / CH; ++c) {
+        for (int rh = 0; rh < CH / 16; ++rh)
+            for (int ks = 0; ks < KS; ++ks) frag(f1, c * (CH / 16) + rh, ks, KS);
+        for (int rt = 0; rt < RT; ++rt)
+            for (int kh = 0; kh < CH / 32; ++kh) frag(f2, rt, c * (CH / 32) + kh, FKS);
+    }
+}
+
+void append_qkv_stream(std::vector<uint16_t>& out, const float* Wqkv, int D) {
+    const int KS = D / 32;
+    std::vector<uint16_t> f;
+    append_frags(f, Wqkv, D, 3 * D);
+    for (int og = 0; og < 3 * KS; ++og)
+        for (int ks = 0; ks < KS; ++ks)
+            for (int half = 0; half < 2; ++half) {
+                const size_t fr = (size_t)(2 * og + half) * KS + ks;
+                out.insert(out.end(), f.begin() + fr * 512, f.begin() + (fr + 1) * 512);
+            }
+}
+
 size_t layer_floats(int D, int F) { return (size_t)4 * D * D + 2 * (size_t)D * F + F + 9 * (size_t)D; }
 
 }  // namespace
@@ -103,13 +137,13 @@ struct pwd_decoder {
     int* err = nullptr;
     // views into `weights`
     struct Layer {
-        const uint16_t *Wo, *W1, *W2, *Wqkv;
+        const uint16_t *post, *qkv;
         const float *bo, *g1, *be1, *b1, *b2, *g2, *be2, *bqkv;
     };
     std::vector<Layer> layers;
     const float* S0 = nullptr;
     const float* we = nullptr;
-    const float* Wc = nullptr;
+    const uint16_t* Wc = nullptr;
     const float* bc = nullptr;
     const float* wo = nullptr;
     const int* cell_token = nullptr;
@@ -266,7 +300,7 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
     };
     const size_t off_cell = put(cell_token.data(), cell_token.size() * sizeof(int));
 
-    struct LayerOff { size_t Wo, W1, W2, Wqkv, bo, g1, be1, b1, b2, g2, be2, bqkv; };
+    struct LayerOff { size_t post, qkv, bo, g1, be1, b1, b2, g2, be2, bqkv; };
     std::vector<LayerOff> loff(L);
     size_t off_S0 = 0, off_we = 0, off_Wc = 0, off_bc = 0, off_wo = 0, off_f32 = 0;
     const size_t lf = layer_floats(D, F);
@@ -302,10 +336,11 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
                 bqkv[2 * D + o] = bv[o];
             }
             std::vector<uint16_t> fr;
-            fr.clear(); append_frags(fr, Wo, D, D); loff[l].Wo = put(fr.data(), fr.size() * 2);
-            fr.clear(); append_frags(fr, W1, D, F); loff[l].W1 = put(fr.data(), fr.size() * 2);
-            fr.clear(); append_frags(fr, W2, F, D); loff[l].W2 = put(fr.data(), fr.size() * 2);
-            fr.clear(); append_frags(fr, wqkv.data(), D, 3 * D); loff[l].Wqkv = put(fr.data(), fr.size() * 2);
+            append_post_stream(fr, Wo, W1, W2, D, tok_mlp_chunk(D));
+            loff[l].post = put(fr.data(), fr.size() * 2);
+            fr.clear();
+            append_qkv_stream(fr, wqkv.data(), D);
+            loff[l].qkv = put(fr.data(), fr.size() * 2);
             loff[l].bo = put(bo, D * 4);
             loff[l].g1 = put(g1, D * 4);
             loff[l].be1 = put(be1, D * 4);
@@ -315,7 +350,11 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
             loff[l].be2 = put(be2, D * 4);
             loff[l].bqkv = put(bqkv.data(), 3 * D * 4);
         }
-        off_Wc = put(tail, (size_t)4 * D * D * 4);
+        {
+            std::vector<uint16_t> fr;
+            append_frags(fr, tail, 4 * D, D);   // Wc[2][2][D][D] read as [4D][D]
+            off_Wc = put(fr.data(), fr.size() * 2);
+        }
         off_bc = put(tail + 4 * (size_t)D * D, D * 4);
         off_wo = put(tail + 4 * (size_t)D * D + D, (size_t)d * D * 4);
     } else {
@@ -350,12 +389,12 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
     dec->S0 = fptr(off_S0);
     if (dims->dtype == PWD_DTYPE_BF16) {
         dec->we = fptr(off_we);
-        dec->Wc = fptr(off_Wc);
+        dec->Wc = hptr(off_Wc);
         dec->bc = fptr(off_bc);
         dec->wo = fptr(off_wo);
         for (int l = 0; l < L; ++l) {
             pwd_decoder::Layer ly;
-            ly.Wo = hptr(loff[l].Wo); ly.W1 = hptr(loff[l].W1); ly.W2 = hptr(loff[l].W2); ly.Wqkv = hptr(loff[l].Wqkv);
+            ly.post = hptr(loff[l].post); ly.qkv = hptr(loff[l].qkv);
             ly.bo = fptr(loff[l].bo); ly.g1 = fptr(loff[l].g1); ly.be1 = fptr(loff[l].be1); ly.b1 = fptr(loff[l].b1);
             ly.b2 = fptr(loff[l].b2); ly.g2 = fptr(loff[l].g2); ly.be2 = fptr(loff[l].be2); ly.bqkv = fptr(loff[l].bqkv);
             dec->layers.push_back(ly);
@@ -445,6 +484,7 @@ int decode_windows(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_ty
     tp.nbw = dec->nbw;
     tp.kappa = dec->kappa;
     tp.eps = dec->eps;
+    tp.qscale = (float)(1.4426950408889634 / std::sqrt((double)dec->dh));
     tp.X = dec->X;
     tp.QKV = dec->QKV;
     tp.Y = dec->Y;
@@ -452,11 +492,11 @@ int decode_windows(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_ty
     tp.we = dec->we;
     auto set_post = [&](int l) {
         const auto& ly = dec->layers[l];
-        tp.Wo = ly.Wo; tp.W1 = ly.W1; tp.W2 = ly.W2;
+        tp.post_stream = ly.post;
         tp.bo = ly.bo; tp.g1 = ly.g1; tp.be1 = ly.be1; tp.b1 = ly.b1; tp.b2 = ly.b2; tp.g2 = ly.g2; tp.be2 = ly.be2;
     };
     auto set_qkv = [&](int l) {
-        tp.Wqkv = dec->layers[l].Wqkv;
+        tp.qkv_stream = dec->layers[l].qkv;
         tp.bqkv = dec->layers[l].bqkv;
     };
     AttnParams ap;
@@ -466,7 +506,6 @@ int decode_windows(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_ty
     ap.Npad = dec->Npad;
     ap.nbw = dec->nbw;
     ap.H = dec->H;
-    ap.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)dec->dh));
 
     // round 0: embed (state D_0 = 0) and project layer 0
     tp.t = 0;

@@ -1,90 +1,109 @@
 // Readout of the final decoder state (App. A.3) and the detection-event export.
 //
-// Readout, one workgroup per window, one thread per output feature o:
+// Readout:
 //   the tokens go back onto the (d+1)x(d+1) stabilizer grid (zeros at empty cells);
 //   Y[i][j] = ReLU(b_c + sum_{a,b in {0,1}} G[i+a][j+b] Wc[a][b])  (2x2 valid convolution)
 //   P[i] = mean_j Y[i][j]                                           (logical pooling)
 //   logit = sum_i <w_o[i], P[i]> + b_o + beta[type],  bit = logit > 0
-// in fp32, two data-qubit rows at a time with three grid rows staged in LDS. The final sum
-// over features is a fixed-order tree, so a window's logit does not depend on the batch.
+// The convolution is an implicit GEMM on bf16 MFMA (state rounded to bf16, fp32
+// accumulation); pooling and the projection fold into one fixed-order sum, so a window's
+// logit does not depend on the batch.
 #include "common.h"
 #include "kernels.h"
 
 namespace {
 
-constexpr int MAXD = 25;
-constexpr int ROWS = 2;      // data-qubit rows per pass
+constexpr int RB = 2;          // 16-position blocks per wavefront pass
+constexpr int RWAVES = 4;
 
-__global__ __launch_bounds__(256) void readout_kernel(ReadoutParams p) {
+PWD_DEV f32x4 ld4g(const float* __restrict__ p) { return *reinterpret_cast<const f32x4*>(p); }
+
+// One workgroup per window. The d x d output positions (data qubits) form 16-wide MFMA
+// column blocks; for each, Y^T = Wc^T G^T over k = 4 taps x D input features, where the B
+// fragment of (tap (a,b), features 32s..32s+31) holds the state of the stabilizer at cell
+// (i+a, j+b) rounded to bf16 (zero where the cell is empty). The A fragments of Wc^T come
+// from L2. Each lane then adds sum_o w_o[i][o] ReLU(Y[o] + b_c[o]) / d over its outputs.
+template <int D>
+__global__ __launch_bounds__(RWAVES * 64) void readout_kernel(ReadoutParams p) {
+    constexpr int RT = D / 16, KSD = D / 32, KS = 4 * KSD;
     const int win = blockIdx.x;
-    const int o = threadIdx.x;            // output feature (blockDim.x == D)
-    const int D = p.D, d = p.d, gw = d + 1;
-    extern __shared__ __align__(16) float gsh[];   // [ROWS+1][d+1][D]
-    __shared__ float red[256];
-
-    const int type = p.types[win];
-    const bool bad = type > WIN_FINAL;
-    const int RT = D / 16;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int g = lane >> 4, col = lane & 15;
+    const int d = p.d, gw = d + 1, npos = d * d, npb = (npos + 15) / 16;
     const int64_t tb_base = (int64_t)win * p.nbw;
+    const float inv_d = 1.0f / (float)d;
+    __shared__ float red[RWAVES];
 
     float part = 0.f;
-    for (int i0 = 0; i0 < d; i0 += ROWS) {
-        const int nrow = min(ROWS, d - i0);
-        __syncthreads();
-        // stage grid rows i0 .. i0+nrow into LDS (thread o moves feature o of each cell)
-        for (int r = 0; r <= nrow; ++r)
-            for (int c = 0; c < gw; ++c) {
-                const int tok = p.cell_token[(i0 + r) * gw + c];
-                float v = 0.f;
-                if (tok >= 0) {
-                    const int blk = tok >> 4, cl = tok & 15;
-                    const int rt = o >> 4, g = (o & 15) >> 2, i = o & 3;
-                    v = p.X[(((tb_base + blk) * RT + rt) * 64 + g * 16 + cl) * 4 + i];
+    for (int pb0 = wave * RB; pb0 < npb; pb0 += RWAVES * RB) {
+        f32x4 acc[RT][RB];
+        int pos_i[RB], tok[RB][4];
+#pragma unroll
+        for (int b = 0; b < RB; ++b) {
+            const int pos = (pb0 + b) * 16 + col;
+            const bool ok = pos < npos && pb0 + b < npb;
+            const int i = ok ? pos / d : 0, j = ok ? pos % d : 0;
+            pos_i[b] = ok ? i : -1;
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+                tok[b][t] = ok ? p.cell_token[(i + (t >> 1)) * gw + j + (t & 1)] : -1;
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) acc[rt][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll 2
+        for (int ks = 0; ks < KS; ++ks) {
+            const int t = ks / KSD, s = ks % KSD;
+            bf16x8 gb[RB];
+#pragma unroll
+            for (int b = 0; b < RB; ++b) {
+                const int T = tok[b][t];
+                f32x4 lo = {0.f, 0.f, 0.f, 0.f}, hi = lo;
+                if (T >= 0) {
+                    const float* src = p.X + ((tb_base + (T >> 4)) * RT + 2 * s) * 256 + (g * 16 + (T & 15)) * 4;
+                    lo = ld4g(src);
+                    hi = ld4g(src + 256);
                 }
-                gsh[(r * gw + c) * D + o] = v;
+                gb[b] = pack_b(lo, hi);
             }
-        __syncthreads();
-        float acc[ROWS][MAXD];
-        const float bias = p.bc[o];
 #pragma unroll
-        for (int r = 0; r < ROWS; ++r)
+            for (int rt = 0; rt < RT; ++rt) {
+                const bf16x8 a = __builtin_bit_cast(bf16x8,
+                    *reinterpret_cast<const u16x8*>(p.Wc + (((size_t)rt * KS + ks) * 64 + lane) * 8));
 #pragma unroll
-            for (int j = 0; j < MAXD; ++j) acc[r][j] = bias;
-        for (int a = 0; a < 2; ++a)
-            for (int b = 0; b < 2; ++b)
-                for (int k = 0; k < D; ++k) {
-                    const float wv = p.Wc[(((a * 2 + b) * D) + k) * D + o];
+                for (int b = 0; b < RB; ++b) acc[rt][b] = mfma16x16x32(a, gb[b], acc[rt][b]);
+            }
+        }
 #pragma unroll
-                    for (int r = 0; r < ROWS; ++r) {
-                        const float* grow = gsh + ((r + a) * gw + b) * D + k;
+        for (int b = 0; b < RB; ++b) {
+            if (pos_i[b] < 0) continue;
+            const float* wrow = p.wo + pos_i[b] * D;
+            float s = 0.f;
 #pragma unroll
-                        for (int j = 0; j < MAXD; ++j)
-                            if (r < nrow && j < d) acc[r][j] = fmaf(grow[j * D], wv, acc[r][j]);
-                    }
-                }
+            for (int rt = 0; rt < RT; ++rt) {
+                const f32x4 bias = ld4g(p.bc + rt * 16 + 4 * g);
+                const f32x4 w = ld4g(wrow + rt * 16 + 4 * g);
 #pragma unroll
-        for (int r = 0; r < ROWS; ++r) {
-            if (r >= nrow) continue;
-            float pool = 0.f;
-#pragma unroll
-            for (int j = 0; j < MAXD; ++j)
-                if (j < d) pool += fmaxf(acc[r][j], 0.f);
-            part = fmaf(p.wo[(i0 + r) * D + o], pool / (float)d, part);
+                for (int i = 0; i < 4; ++i) s = fmaf(w[i], fmaxf(acc[rt][b][i] + bias[i], 0.f), s);
+            }
+            part += s * inv_d;
         }
     }
-    red[o] = part;
+    // fixed-order reduction: lanes, then wavefronts
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) part += __shfl_xor(part, off);
+    if (lane == 0) red[wave] = part;
     __syncthreads();
-    for (int n = 128; n > 0; n >>= 1) {
-        if (o < n && o + n < D) red[o] += red[o + n];
-        __syncthreads();
-    }
-    if (o == 0) {
-        if (bad) {
+    if (threadIdx.x == 0) {
+        float tot = 0.f;
+#pragma unroll
+        for (int w = 0; w < RWAVES; ++w) tot += red[w];
+        const int type = p.types[win];
+        if (type > WIN_FINAL) {
             p.logits[win] = __builtin_nanf("");
             p.bits[win] = 0;
             atomicOr(p.err, 1);
         } else {
-            const float logit = red[0] + p.bo + p.beta[type];
+            const float logit = tot + p.bo + p.beta[type];
             p.logits[win] = logit;
             p.bits[win] = logit > 0.f ? 1 : 0;
         }
@@ -115,12 +134,10 @@ __global__ void events_kernel(EventsParams p) {
 
 hipError_t launch_readout(const ReadoutParams& p, hipStream_t s) {
     if (p.nwin <= 0) return hipSuccess;
-    if (p.d > MAXD || p.D > 256) return hipErrorInvalidValue;
-    const size_t smem = (size_t)(ROWS + 1) * (p.d + 1) * p.D * sizeof(float);
-    hipError_t e = hipFuncSetAttribute((const void*)readout_kernel,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-    if (e != hipSuccess) return e;
-    readout_kernel<<<dim3((unsigned)p.nwin), dim3(p.D), smem, s>>>(p);
+    const dim3 grid((unsigned)p.nwin), block(RWAVES * 64);
+    if (p.D == 256) readout_kernel<256><<<grid, block, 0, s>>>(p);
+    else if (p.D == 128) readout_kernel<128><<<grid, block, 0, s>>>(p);
+    else return hipErrorInvalidValue;
     return hipGetLastError();
 }
 

@@ -12,18 +12,43 @@
 // GEMMs are transposed (Out^T = W^T In^T) so tokens lie along MFMA columns: LayerNorm
 // reduces over the four lanes that share a token, and each accumulator becomes the next
 // GEMM's B operand in registers.
+//
+// Weights reach the MFMAs through LDS: the host lays every weight fragment out in the exact
+// order the kernel consumes them (a "weight stream"), and the workgroup pulls the stream
+// through a double-buffered LDS ring in 32 KB chunks with direct global->LDS loads, one
+// chunk ahead of the MFMAs. Every fragment read from LDS feeds TB MFMAs of each wavefront.
 #include "common.h"
 #include "kernels.h"
 
 namespace {
 
-constexpr int TB = 2;        // 16-token blocks per wavefront
-constexpr int WAVES = 4;     // wavefronts per workgroup
-constexpr int CH = 64;       // feed-forward hidden units per chunk
+constexpr int TB = 2;           // 16-token blocks per wavefront
+constexpr int WAVES = 4;        // wavefronts per workgroup
+constexpr int CHUNK = 32;       // weight fragments (1 KB each) per LDS chunk
+constexpr int FRAG = 512;       // bf16 values per fragment
+
+template <int D>
+struct Shape {
+    static constexpr int RT = D / 16;                 // 16-row C tiles of a D-vector
+    static constexpr int KS = D / 32;                 // 32-deep k-steps of a D-vector
+    static constexpr int F = 4 * D;
+    static constexpr int CH = 8192 / D;               // hidden units per feed-forward chunk
+    static constexpr int NMLP = F / CH;               // feed-forward chunks
+    static constexpr int WO_CHUNKS = RT * KS / CHUNK;
+    static constexpr int QKV_CHUNKS = (3 * D / 16) * KS / CHUNK;
+    static constexpr int OG_PER_CHUNK = CHUNK / (2 * KS);
+    static constexpr int POST_CHUNKS = WO_CHUNKS + NMLP;
+    static_assert((CH / 16) * KS + RT * (CH / 32) == CHUNK, "one feed-forward chunk per LDS chunk");
+    static_assert(RT * KS % CHUNK == 0 && (3 * D / 16) * KS % CHUNK == 0, "whole chunks");
+};
 
 PWD_DEV bf16x8 ldfrag(const uint16_t* __restrict__ base, int64_t frag, int lane) {
     const u16x8 v = *reinterpret_cast<const u16x8*>(base + (frag * 64 + lane) * 8);
     return __builtin_bit_cast(bf16x8, v);
+}
+
+PWD_DEV bf16x8 lds_frag(const uint16_t* buf, int j, int lane) {
+    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(buf + j * FRAG + lane * 8));
 }
 
 PWD_DEV void stfrag(uint16_t* __restrict__ base, int64_t frag, int lane, bf16x8 v) {
@@ -34,29 +59,68 @@ PWD_DEV f32x4 ld4(const float* __restrict__ p) { return *reinterpret_cast<const 
 
 PWD_DEV f32x4 relu4(f32x4 v) {
     f32x4 r;
-    #pragma unroll
+#pragma unroll
     for (int i = 0; i < 4; ++i) r[i] = v[i] > 0.f ? v[i] : 0.f;
     return r;
 }
 
-// LayerNorm over the D features of each token (biased variance, two passes).
+// The two LDS buffers of the weight stream. They are separate objects so the compiler can
+// tell that the direct-to-LDS prefetch into one never aliases reads of the other.
+__shared__ __align__(16) uint16_t g_wbuf0[CHUNK * FRAG];
+__shared__ __align__(16) uint16_t g_wbuf1[CHUNK * FRAG];
+
+template <int PAR>
+PWD_DEV uint16_t* wbuf() { return PAR ? g_wbuf1 : g_wbuf0; }
+
+// The weight stream of one launch: `post` chunks first, then `qkv` chunks, pulled through
+// the two LDS buffers (chunk i lives in buffer i % 2). begin<i % 2>(i) makes chunk i visible
+// to every wavefront and starts the load of chunk i+1 into the other buffer.
+struct WeightPipe {
+    const uint16_t* post;
+    const uint16_t* qkv;
+    int n_post, total;
+    int lane, wave;
+
+    template <int PAR>
+    __device__ void issue(int i) const {
+        const uint16_t* src = i < n_post ? post + (size_t)i * CHUNK * FRAG
+                                         : qkv + (size_t)(i - n_post) * CHUNK * FRAG;
+        uint16_t* dst = wbuf<PAR>();
+#pragma unroll
+        for (int j = 0; j < CHUNK / WAVES; ++j) {
+            const int f = wave * (CHUNK / WAVES) + j;
+            __builtin_amdgcn_global_load_lds(
+                (const __attribute__((address_space(1))) void*)(src + (f * 64 + lane) * 8),
+                (__attribute__((address_space(3))) void*)(dst + f * FRAG), 16, 0, 0);
+        }
+    }
+    template <int PAR>
+    __device__ const uint16_t* begin(int i) const {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's part of chunk i landed
+        __syncthreads();                                   // ... and everyone's; buffer i-1 is free
+        if (i + 1 < total) issue<1 - PAR>(i + 1);
+        __builtin_amdgcn_sched_barrier(0);                 // keep the prefetch ahead of the MFMAs
+        return wbuf<PAR>();
+    }
+};
+
+// LayerNorm over the D features of each token (biased variance, two passes); gamma and
+// beta are in LDS.
 template <int RT>
-PWD_DEV void layer_norm(f32x4 (&x)[RT][TB], const float* __restrict__ gamma,
-                        const float* __restrict__ beta, float eps, int g) {
+PWD_DEV void layer_norm(f32x4 (&x)[RT][TB], const float* gamma, const float* beta, float eps, int g) {
     constexpr float inv_d = 1.0f / (RT * 16);
-    #pragma unroll
+#pragma unroll
     for (int b = 0; b < TB; ++b) {
         float s = 0.f;
-        #pragma unroll
-        for (int rt = 0; rt < RT; ++rt)
-            s += (x[rt][b][0] + x[rt][b][1]) + (x[rt][b][2] + x[rt][b][3]);
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) s += (x[rt][b][0] + x[rt][b][1]) + (x[rt][b][2] + x[rt][b][3]);
         s += __shfl_xor(s, 16);
         s += __shfl_xor(s, 32);
         const float mean = s * inv_d;
         float v = 0.f;
-        #pragma unroll
+#pragma unroll
         for (int rt = 0; rt < RT; ++rt)
-            #pragma unroll
+#pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const float c = x[rt][b][i] - mean;
                 v += c * c;
@@ -64,104 +128,152 @@ PWD_DEV void layer_norm(f32x4 (&x)[RT][TB], const float* __restrict__ gamma,
         v += __shfl_xor(v, 16);
         v += __shfl_xor(v, 32);
         const float rstd = rsqrtf(v * inv_d + eps);
-        #pragma unroll
+#pragma unroll
         for (int rt = 0; rt < RT; ++rt) {
             const f32x4 gm = ld4(gamma + rt * 16 + 4 * g);
             const f32x4 bt = ld4(beta + rt * 16 + 4 * g);
-            #pragma unroll
+#pragma unroll
             for (int i = 0; i < 4; ++i) x[rt][b][i] = (x[rt][b][i] - mean) * rstd * gm[i] + bt[i];
         }
     }
 }
 
+// Per-launch vectors staged in LDS once: [bo g1 be1 b2 g2 be2 | b1 (F) | bqkv (3D)].
+template <int D>
+struct Vecs {
+    static constexpr int BO = 0, G1 = D, BE1 = 2 * D, B2 = 3 * D, G2 = 4 * D, BE2 = 5 * D;
+    static constexpr int B1 = 6 * D, BQKV = 10 * D, SIZE = 13 * D;
+};
+
 template <int D, int FLAGS>
-__global__ __launch_bounds__(WAVES * 64) void tok_kernel(TokParams p) {
-    constexpr int RT = D / 16;   // 16-row C tiles per activation
-    constexpr int KS = D / 32;   // 32-deep k-steps per activation
+__global__ __launch_bounds__(WAVES * 64, 1) void tok_kernel(TokParams p) {
+    using S = Shape<D>;
+    using V = Vecs<D>;
+    constexpr int RT = S::RT, KS = S::KS, CH = S::CH;
+    constexpr bool POST = (FLAGS & TOK_POST) != 0, QKV = (FLAGS & TOK_QKV) != 0;
     const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
     const int g = lane >> 4;
     const int col = lane & 15;
-    const int64_t tb0 = ((int64_t)blockIdx.x * WAVES + (threadIdx.x >> 6)) * TB;
+    const int64_t tb0 = ((int64_t)blockIdx.x * WAVES + wave) * TB;
+
+    WeightPipe pipe;
+    pipe.post = p.post_stream;
+    pipe.qkv = p.qkv_stream;
+    pipe.n_post = POST ? S::POST_CHUNKS : 0;
+    pipe.total = pipe.n_post + (QKV ? S::QKV_CHUNKS : 0);
+    pipe.lane = lane;
+    pipe.wave = wave;
+    pipe.issue<0>(0);
+
+    __shared__ __align__(16) float vec[V::SIZE];
+    if (POST) {
+        const float* src[7] = {p.bo, p.g1, p.be1, p.b2, p.g2, p.be2, p.b1};
+        for (int k = 0; k < 6; ++k)
+            for (int i = threadIdx.x; i < D; i += WAVES * 64) vec[k * D + i] = src[k][i];
+        for (int i = threadIdx.x; i < 4 * D; i += WAVES * 64) vec[V::B1 + i] = src[6][i];
+    }
+    if (QKV)
+        for (int i = threadIdx.x; i < 3 * D; i += WAVES * 64) vec[V::BQKV + i] = p.bqkv[i];
+    // (the first pipe.begin's barrier publishes vec)
 
     f32x4 x[RT][TB];
 
-    if constexpr ((FLAGS & TOK_POST) != 0) {
-        // ---- out-projection + residual + LayerNorm 1; accumulators start at X + b_o
+    if constexpr (POST) {
+        // ---- out-projection + residual + LayerNorm 1; accumulators start at X (+ b_o below)
         {
             bf16x8 y[KS][TB];
-            #pragma unroll
+#pragma unroll
             for (int b = 0; b < TB; ++b)
-                #pragma unroll
+#pragma unroll
                 for (int ks = 0; ks < KS; ++ks) y[ks][b] = ldfrag(p.Y, (tb0 + b) * KS + ks, lane);
-            #pragma unroll
-            for (int rt = 0; rt < RT; ++rt) {
-                const f32x4 bias = ld4(p.bo + rt * 16 + 4 * g);
-                #pragma unroll
-                for (int b = 0; b < TB; ++b)
-                    x[rt][b] = ld4(p.X + (((tb0 + b) * RT + rt) * 64 + lane) * 4) + bias;
-            }
-            #pragma unroll
+#pragma unroll
             for (int rt = 0; rt < RT; ++rt)
-                #pragma unroll
-                for (int ks = 0; ks < KS; ++ks) {
-                    const bf16x8 a = ldfrag(p.Wo, rt * KS + ks, lane);
-                    #pragma unroll
+#pragma unroll
+                for (int b = 0; b < TB; ++b) x[rt][b] = ld4(p.X + (((tb0 + b) * RT + rt) * 64 + lane) * 4);
+            auto wo_chunk = [&](const uint16_t* buf, int c) {
+#pragma unroll
+                for (int j = 0; j < CHUNK; ++j) {
+                    const int fr = c * CHUNK + j, rt = fr / KS, ks = fr % KS;
+                    const bf16x8 a = lds_frag(buf, j, lane);
+#pragma unroll
                     for (int b = 0; b < TB; ++b) x[rt][b] = mfma16x16x32(a, y[ks][b], x[rt][b]);
                 }
+            };
+            static_assert(S::WO_CHUNKS == 1 || S::WO_CHUNKS % 2 == 0, "Wo chunks");
+            if constexpr (S::WO_CHUNKS == 1) {
+                wo_chunk(pipe.begin<0>(0), 0);
+            } else {
+#pragma unroll
+                for (int c = 0; c < S::WO_CHUNKS; c += 2) {
+                    wo_chunk(pipe.begin<0>(c), c);
+                    wo_chunk(pipe.begin<1>(c + 1), c + 1);
+                }
+            }
         }
-        layer_norm<RT>(x, p.g1, p.be1, p.eps, g);
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+            const f32x4 bias = ld4(vec + V::BO + rt * 16 + 4 * g);
+#pragma unroll
+            for (int b = 0; b < TB; ++b) x[rt][b] += bias;
+        }
+        layer_norm<RT>(x, vec + V::G1, vec + V::BE1, p.eps, g);
 
         // ---- feed-forward, hidden units in chunks of CH; accumulators start at X + b_2
         bf16x8 xb[KS][TB];
-        #pragma unroll
+#pragma unroll
         for (int ks = 0; ks < KS; ++ks)
-            #pragma unroll
+#pragma unroll
             for (int b = 0; b < TB; ++b) xb[ks][b] = pack_b(x[2 * ks][b], x[2 * ks + 1][b]);
-        #pragma unroll
+#pragma unroll
         for (int rt = 0; rt < RT; ++rt) {
-            const f32x4 bias = ld4(p.b2 + rt * 16 + 4 * g);
-            #pragma unroll
+            const f32x4 bias = ld4(vec + V::B2 + rt * 16 + 4 * g);
+#pragma unroll
             for (int b = 0; b < TB; ++b) x[rt][b] += bias;
         }
-        constexpr int F = 4 * D;
-        constexpr int FKS = F / 32;
-        for (int c = 0; c < F / CH; ++c) {
+        auto mlp_chunk = [&](const uint16_t* buf, int c) {
             f32x4 h[CH / 16][TB];
-            #pragma unroll
+#pragma unroll
             for (int rh = 0; rh < CH / 16; ++rh) {
-                const f32x4 bias = ld4(p.b1 + c * CH + rh * 16 + 4 * g);
-                #pragma unroll
+                const f32x4 bias = ld4(vec + V::B1 + c * CH + rh * 16 + 4 * g);
+#pragma unroll
                 for (int b = 0; b < TB; ++b) h[rh][b] = bias;
             }
-            #pragma unroll
+#pragma unroll
             for (int rh = 0; rh < CH / 16; ++rh)
-                #pragma unroll
+#pragma unroll
                 for (int ks = 0; ks < KS; ++ks) {
-                    const bf16x8 a = ldfrag(p.W1, (c * (CH / 16) + rh) * KS + ks, lane);
-                    #pragma unroll
+                    const bf16x8 a = lds_frag(buf, rh * KS + ks, lane);
+#pragma unroll
                     for (int b = 0; b < TB; ++b) h[rh][b] = mfma16x16x32(a, xb[ks][b], h[rh][b]);
                 }
             bf16x8 hb[CH / 32][TB];
-            #pragma unroll
+#pragma unroll
             for (int kh = 0; kh < CH / 32; ++kh)
-                #pragma unroll
-                for (int b = 0; b < TB; ++b)
-                    hb[kh][b] = pack_b(relu4(h[2 * kh][b]), relu4(h[2 * kh + 1][b]));
-            #pragma unroll
+#pragma unroll
+                for (int b = 0; b < TB; ++b) hb[kh][b] = pack_b(relu4(h[2 * kh][b]), relu4(h[2 * kh + 1][b]));
+            const uint16_t* w2 = buf + (CH / 16) * KS * FRAG;
+#pragma unroll
             for (int rt = 0; rt < RT; ++rt)
-                #pragma unroll
+#pragma unroll
                 for (int kh = 0; kh < CH / 32; ++kh) {
-                    const bf16x8 a = ldfrag(p.W2, rt * FKS + c * (CH / 32) + kh, lane);
-                    #pragma unroll
+                    const bf16x8 a = lds_frag(w2, rt * (CH / 32) + kh, lane);
+#pragma unroll
                     for (int b = 0; b < TB; ++b) x[rt][b] = mfma16x16x32(a, hb[kh][b], x[rt][b]);
                 }
+        };
+        static_assert(S::NMLP % 2 == 0, "feed-forward chunks come in pairs");
+        constexpr int P0 = S::WO_CHUNKS & 1;
+        for (int c = 0; c < S::NMLP; c += 2) {
+            mlp_chunk(pipe.begin<P0>(S::WO_CHUNKS + c), c);
+            mlp_chunk(pipe.begin<1 - P0>(S::WO_CHUNKS + c + 1), c + 1);
         }
-        layer_norm<RT>(x, p.g2, p.be2, p.eps, g);
+        layer_norm<RT>(x, vec + V::G2, vec + V::BE2, p.eps, g);
     }
 
     if constexpr ((FLAGS & TOK_EMBED) != 0) {
         // ---- embedding of round t folded into the state: X = kappa (S_t + X)
-        #pragma unroll
+#pragma unroll
         for (int b = 0; b < TB; ++b) {
             const int64_t tb = tb0 + b;
             const int64_t w = tb / p.nbw;
@@ -174,57 +286,70 @@ __global__ __launch_bounds__(WAVES * 64) void tok_kernel(TokParams p) {
                                                  p.in.b_left, p.in.d);
                 e = (float)((word >> (s & 31)) & 1u);
             }
-            #pragma unroll
+            const bool real = s < p.in.N;
+#pragma unroll
             for (int rt = 0; rt < RT; ++rt) {
                 const f32x4 s0 = ld4(p.S0 + (((int64_t)blk * RT + rt) * 64 + lane) * 4);
                 const f32x4 we = ld4(p.we + rt * 16 + 4 * g);
-                const bool real = s < p.in.N;
-                #pragma unroll
+#pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const float emb = real ? e * we[i] + s0[i] : 0.f;
-                    const float prev = (FLAGS & TOK_POST) ? x[rt][b][i] : 0.f;
+                    const float prev = POST ? x[rt][b][i] : 0.f;
                     x[rt][b][i] = p.kappa * (emb + prev);
                 }
             }
         }
     }
 
-    #pragma unroll
+#pragma unroll
     for (int b = 0; b < TB; ++b)
-        #pragma unroll
+#pragma unroll
         for (int rt = 0; rt < RT; ++rt)
             *reinterpret_cast<f32x4*>(p.X + (((tb0 + b) * RT + rt) * 64 + lane) * 4) = x[rt][b];
 
-    if constexpr ((FLAGS & TOK_QKV) != 0) {
+    if constexpr (QKV) {
         bf16x8 xb[KS][TB];
-        #pragma unroll
+#pragma unroll
         for (int ks = 0; ks < KS; ++ks)
-            #pragma unroll
+#pragma unroll
             for (int b = 0; b < TB; ++b) xb[ks][b] = pack_b(x[2 * ks][b], x[2 * ks + 1][b]);
         // 3D output features in groups of 32 (= one B fragment of Q, K or V)
-        #pragma unroll
-        for (int og = 0; og < 3 * KS; ++og) {
-            f32x4 q0[TB], q1[TB];
-            const f32x4 bias0 = ld4(p.bqkv + og * 32 + 4 * g);
-            const f32x4 bias1 = ld4(p.bqkv + og * 32 + 16 + 4 * g);
-            #pragma unroll
-            for (int b = 0; b < TB; ++b) {
-                q0[b] = bias0;
-                q1[b] = bias1;
-            }
-            #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                const bf16x8 a0 = ldfrag(p.Wqkv, (2 * og) * KS + ks, lane);
-                const bf16x8 a1 = ldfrag(p.Wqkv, (2 * og + 1) * KS + ks, lane);
-                #pragma unroll
+        auto qkv_chunk = [&](const uint16_t* buf, int qc) {
+#pragma unroll
+            for (int o2 = 0; o2 < S::OG_PER_CHUNK; ++o2) {
+                const int og = qc * S::OG_PER_CHUNK + o2;
+                f32x4 q0[TB], q1[TB];
+                const f32x4 bias0 = ld4(vec + V::BQKV + og * 32 + 4 * g);
+                const f32x4 bias1 = ld4(vec + V::BQKV + og * 32 + 16 + 4 * g);
+#pragma unroll
                 for (int b = 0; b < TB; ++b) {
-                    q0[b] = mfma16x16x32(a0, xb[ks][b], q0[b]);
-                    q1[b] = mfma16x16x32(a1, xb[ks][b], q1[b]);
+                    q0[b] = bias0;
+                    q1[b] = bias1;
                 }
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) {
+                    const bf16x8 a0 = lds_frag(buf, (o2 * KS + ks) * 2, lane);
+                    const bf16x8 a1 = lds_frag(buf, (o2 * KS + ks) * 2 + 1, lane);
+#pragma unroll
+                    for (int b = 0; b < TB; ++b) {
+                        q0[b] = mfma16x16x32(a0, xb[ks][b], q0[b]);
+                        q1[b] = mfma16x16x32(a1, xb[ks][b], q1[b]);
+                    }
+                }
+                const float sc = og < KS ? p.qscale : 1.0f;   // Q: log2(e)/sqrt(dh)
+#pragma unroll
+                for (int b = 0; b < TB; ++b)
+                    stfrag(p.QKV, (tb0 + b) * (3 * KS) + og, lane, pack_b(q0[b] * sc, q1[b] * sc));
             }
-            #pragma unroll
-            for (int b = 0; b < TB; ++b) stfrag(p.QKV, (tb0 + b) * (3 * KS) + og, lane, pack_b(q0[b], q1[b]));
+        };
+        constexpr int NP = POST ? S::POST_CHUNKS : 0;
+        constexpr int Q0 = NP & 1;
+        int qc = 0;
+        for (; qc + 1 < S::QKV_CHUNKS; qc += 2) {
+            qkv_chunk(pipe.begin<Q0>(NP + qc), qc);
+            qkv_chunk(pipe.begin<1 - Q0>(NP + qc + 1), qc + 1);
         }
+        if constexpr (S::QKV_CHUNKS % 2 == 1) qkv_chunk(pipe.begin<Q0>(NP + qc), qc);
     }
 }
 
@@ -248,6 +373,9 @@ hipError_t launch_tok_d(int flags, const TokParams& p, int64_t n_tb, hipStream_t
 // Token blocks are processed in groups of WAVES*TB; every buffer indexed here must be
 // allocated for n_tb rounded up to that multiple.
 int64_t tok_block_granule() { return (int64_t)WAVES * TB; }
+
+// Fragments of the weight streams (see tok_kernel): hidden units per feed-forward chunk.
+int tok_mlp_chunk(int D) { return 8192 / D; }
 
 hipError_t launch_tok(int D, int flags, const TokParams& p, int64_t n_tb, hipStream_t s) {
     if (n_tb <= 0) return hipSuccess;

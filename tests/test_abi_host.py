@@ -1,0 +1,87 @@
+"""Host-only checks of the C ABI: the library loads, exports every function the header
+declares, and validates configurations and weight blobs without touching a device."""
+import ctypes
+import struct
+
+import pytest
+
+from paper_2601_09921_amd import pwdec, synth
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return pwdec.load_library()
+
+
+def test_exports_every_header_function(lib):
+    names = pwdec.header_functions()
+    assert {"decoder_create", "decode_windows", "decoder_destroy", "decoder_detection_events",
+            "decoder_validate_config", "decoder_last_error", "decoder_sync_status"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def validate(lib, d=7, W=14, B=16, D=128, L=3, H=8, r=4, dt=1):
+    g, m = pwdec.geometry(d, W, B), pwdec.dims(D, L, H, r, dt)
+    return lib.decoder_validate_config(ctypes.byref(g), ctypes.byref(m))
+
+
+@pytest.mark.parametrize("wl", list(synth.WORKLOADS.values()), ids=list(synth.WORKLOADS))
+def test_workloads_are_supported(lib, wl):
+    assert validate(lib, wl.d, wl.W, wl.B, wl.D, wl.L, wl.H, wl.mlp_ratio, wl.dtype) == pwdec.PWD_OK
+
+
+@pytest.mark.parametrize("kw", [
+    dict(d=4), dict(d=1), dict(d=27), dict(W=6), dict(W=22), dict(B=0), dict(r=5), dict(L=0),
+    dict(H=3), dict(D=96, H=6), dict(D=128, H=2), dict(dt=2), dict(dt=0, D=256, H=8),
+    dict(dt=0, d=11, W=22, D=64, H=4),
+])
+def test_rejects_unsupported(lib, kw):
+    assert validate(lib, **kw) == pwdec.PWD_EUNSUPPORTED
+    assert lib.decoder_last_error()
+
+
+def test_null_arguments(lib):
+    assert lib.decoder_validate_config(None, None) == pwdec.PWD_EINVAL
+    h = ctypes.c_void_p()
+    g, m = pwdec.geometry(3, 6, 4), pwdec.dims(64, 2, 4, 4, 0)
+    assert lib.decoder_create(ctypes.byref(g), ctypes.byref(m), None, 0, ctypes.byref(h)) == pwdec.PWD_EINVAL
+    assert lib.decode_windows(None, None, None, 0, None, None, None) == pwdec.PWD_EINVAL
+    assert lib.decoder_destroy(None) == pwdec.PWD_OK
+
+
+def blob_for(name):
+    wl = synth.WORKLOADS[name]
+    return wl, pwdec.make_blob(wl.d, wl.W, wl.D, wl.L, wl.H, wl.F, wl.dtype, synth.make_weights(wl))
+
+
+@pytest.mark.parametrize("name", ["d3", "d7"])
+def test_blob_size_matches_header_formula(lib, name):
+    wl, blob = blob_for(name)
+    g, m = pwdec.geometry(wl.d, wl.W, 4), pwdec.dims(wl.D, wl.L, wl.H, wl.mlp_ratio, wl.dtype)
+    assert len(blob) == 64 + 4 * lib.decoder_blob_floats(ctypes.byref(g), ctypes.byref(m))
+
+
+def corrupt(blob, word, value):
+    b = bytearray(blob)
+    b[4 * word:4 * word + 4] = struct.pack("<I", value)
+    return bytes(b)
+
+
+@pytest.mark.parametrize("how", ["magic", "version", "distance", "layers", "dtype", "short", "long"])
+def test_bad_blobs_rejected_before_device_use(lib, how):
+    wl, blob = blob_for("d3")
+    bad = {"magic": lambda b: corrupt(b, 0, 0x12345678),
+           "version": lambda b: corrupt(b, 1, 9),
+           "distance": lambda b: corrupt(b, 2, 5),
+           "layers": lambda b: corrupt(b, 5, 3),
+           "dtype": lambda b: corrupt(b, 8, 1),
+           "short": lambda b: b[:-4],
+           "long": lambda b: b + b"\0\0\0\0"}[how](blob)
+    g, m = pwdec.geometry(wl.d, wl.W, 4), pwdec.dims(wl.D, wl.L, wl.H, wl.mlp_ratio, wl.dtype)
+    h = ctypes.c_void_p()
+    buf = ctypes.create_string_buffer(bad, len(bad))
+    rc = lib.decoder_create(ctypes.byref(g), ctypes.byref(m), buf, len(bad), ctypes.byref(h))
+    assert rc == pwdec.PWD_EBLOB
+    assert not h.value
+    assert b"blob" in lib.decoder_last_error()
