@@ -111,6 +111,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="d25")
     ap.add_argument("--cpu-sample", type=int, default=3, help="oracle windows for the CPU baseline (0: skip)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="first copy 1 GiB device-to-device 3 times (the known-size reference that "
+                         "scales rocprofv3 FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -123,6 +126,14 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     pwdec.load_library()
+    if args.copy_calibration:
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(f"copy calibration: 3 copies of {src.numel() * 4} bytes", file=sys.stderr, flush=True)
+        del src, dst
     wl = synth.WORKLOADS[args.workload]
     B = wl.B
     weights = synth.make_weights(wl)
