@@ -10,9 +10,13 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libpwdec.so")
 SOURCES = ["tok.hip", "attn.hip", "readout.hip", "f32_window.hip", "pwdec.cpp"]
+# Per-source extra flags. The attention kernel keeps its MFMA accumulators in VGPRs (it needs
+# far fewer than 256), so no copies between accumulation and arithmetic registers; the token
+# kernel needs the AGPRs as accumulators.
+EXTRA_FLAGS = {"attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 HIPCC_FLAGS = [
-    "-O3", "-std=c++17", "--offload-arch=gfx950", "-fPIC", "-shared",
+    "-O3", "-std=c++17", "--offload-arch=gfx950", "-fPIC",
     "-Wall", "-Wno-unused-function",
     # no packed-fp32 VALU instructions in device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
@@ -26,18 +30,37 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found (ROCm is required to build the decoder library)")
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every source into libpwdec.so (always recompiles)."""
-    srcs = [os.path.join(CSRC, s) for s in SOURCES]
-    tmp = LIB + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, "-x", "hip", *srcs, "-o", tmp]
+def _run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
-    res = subprocess.run(cmd, capture_output=True, text=True)
+    return subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+
+
+def _finish(proc):
+    out, _ = proc.communicate()
     noise = "is not a recognized feature for this target"
-    msgs = [ln for ln in (res.stdout + res.stderr).splitlines() if noise not in ln]
-    if res.returncode != 0:
+    msgs = [ln for ln in out.splitlines() if noise not in ln]
+    if proc.returncode != 0:
         raise RuntimeError("hipcc failed:\n" + "\n".join(msgs))
+    return msgs
+
+
+def build(verbose: bool = False) -> str:
+    """Compile every source (in parallel) and link libpwdec.so; always recompiles."""
+    objdir = os.path.join(HERE, "_build")
+    os.makedirs(objdir, exist_ok=True)
+    objs, procs = [], []
+    for src in SOURCES:
+        obj = os.path.join(objdir, src + ".o")
+        objs.append(obj)
+        cmd = [hipcc(), *HIPCC_FLAGS, *EXTRA_FLAGS.get(src, []), "-x", "hip", "-c",
+               os.path.join(CSRC, src), "-o", obj]
+        procs.append(_run(cmd, verbose))
+    msgs = []
+    for p in procs:
+        msgs += _finish(p)
+    tmp = LIB + ".tmp"
+    msgs += _finish(_run([hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp], verbose))
     if verbose and msgs:
         print("\n".join(msgs), file=sys.stderr)
     os.replace(tmp, LIB)

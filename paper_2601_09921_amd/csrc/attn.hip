@@ -21,6 +21,7 @@ namespace {
 
 constexpr int WAVES = 4;
 constexpr int QB = 2;                 // query blocks per wavefront pass
+constexpr int SBATCH = 10;            // key blocks per wavefront per staging batch (d=25: one batch)
 
 __host__ __device__ inline int vt_stride(int Npad) { return ((Npad + 31) & ~31) + 8; }   // + 8: spread banks
 
@@ -88,34 +89,46 @@ __global__ __launch_bounds__(WAVES * 64) void attn_kernel(AttnParams p) {
     const int frag = DH == 32 ? h : h / 2;
     const int slot0 = DH == 32 ? 0 : (h % 2) * 4;
 
-    // ---- stage K (A fragments) and V^T; track max |k| over the real keys
+    // ---- stage K (A fragments) and V^T; track max |k| over the real keys. All loads of a
+    // wavefront are issued before any is used, so the staging costs one memory round trip.
     float kmax2 = 0.f;
-    for (int kb = wave; kb < nbw; kb += WAVES) {
-        const u16x8 kv = *reinterpret_cast<const u16x8*>(
-            p.QKV + (((tb_base + kb) * 3 + 1) * KSD + frag) * 512 + lane * 8);
-        float n2 = 0.f;
-        u16x4 k4;
+    for (int kb0 = wave; kb0 < nbw; kb0 += WAVES * SBATCH) {
+        u16x8 kv[SBATCH], vv[SBATCH];
 #pragma unroll
-        for (int i = 0; i < NV; ++i) {
-            const uint16_t u = kv[slot0 + i];
-            const float f = (float)__builtin_bit_cast(__bf16, u);
-            n2 = fmaf(f, f, n2);
-            if (DH == 16) k4[i] = u;
+        for (int u = 0; u < SBATCH; ++u) {
+            const int kb = kb0 + u * WAVES;
+            if (kb < nbw) {
+                kv[u] = *reinterpret_cast<const u16x8*>(
+                    p.QKV + (((tb_base + kb) * 3 + 1) * KSD + frag) * 512 + lane * 8);
+                vv[u] = *reinterpret_cast<const u16x8*>(
+                    p.QKV + (((tb_base + kb) * 3 + 2) * KSD + frag) * 512 + lane * 8);
+            }
         }
-        if (DH == 32) *reinterpret_cast<u16x8*>(ks + (kb * 64 + lane) * 8) = kv;
-        else *reinterpret_cast<u16x4*>(ks + (kb * 64 + lane) * 4) = k4;
-        n2 = sum4(n2);
-        if (kb * 16 + col < N) kmax2 = fmaxf(kmax2, n2);
-
-        const u16x8 vv = *reinterpret_cast<const u16x8*>(
-            p.QKV + (((tb_base + kb) * 3 + 2) * KSD + frag) * 512 + lane * 8);
-        const int key = kb * 16 + col;
-        if (DH == 32) {
 #pragma unroll
-            for (int i = 0; i < 8; ++i) vt[kslot(g, i) * vts + key] = vv[i];
-        } else {
+        for (int u = 0; u < SBATCH; ++u) {
+            const int kb = kb0 + u * WAVES;
+            if (kb >= nbw) continue;
+            float n2 = 0.f;
+            u16x4 k4;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) vt[(4 * g + i) * vts + key] = vv[slot0 + i];
+            for (int i = 0; i < NV; ++i) {
+                const uint16_t x = kv[u][slot0 + i];
+                const float f = (float)__builtin_bit_cast(__bf16, x);
+                n2 = fmaf(f, f, n2);
+                if (DH == 16) k4[i] = x;
+            }
+            if (DH == 32) *reinterpret_cast<u16x8*>(ks + (kb * 64 + lane) * 8) = kv[u];
+            else *reinterpret_cast<u16x4*>(ks + (kb * 64 + lane) * 4) = k4;
+            n2 = sum4(n2);
+            if (kb * 16 + col < N) kmax2 = fmaxf(kmax2, n2);
+            const int key = kb * 16 + col;
+            if (DH == 32) {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) vt[kslot(g, i) * vts + key] = vv[u][i];
+            } else {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) vt[(4 * g + i) * vts + key] = vv[u][slot0 + i];
+            }
         }
     }
 #pragma unroll
@@ -134,22 +147,32 @@ __global__ __launch_bounds__(WAVES * 64) void attn_kernel(AttnParams p) {
     kmax = sqrtf(kmax);
 
     const int nsb = (nbw + 1) / 2;
-    const bool tail_mask = nsb * 32 > N;        // the last superblock holds padding keys
+    auto load_q = [&](int qb0, u16x8 (&qv)[QB]) {
+#pragma unroll
+        for (int j = 0; j < QB; ++j) {
+            const int qb = min(qb0 + j, nbw - 1);    // a lone last block computes a duplicate
+            qv[j] = *reinterpret_cast<const u16x8*>(
+                p.QKV + (((tb_base + qb) * 3 + 0) * KSD + frag) * 512 + lane * 8);
+        }
+    };
+    u16x8 qnext[QB];
+    if (wave * QB < nbw) load_q(wave * QB, qnext);
     for (int qb0 = wave * QB; qb0 < nbw; qb0 += WAVES * QB) {
+        u16x8 qv[QB];
+#pragma unroll
+        for (int j = 0; j < QB; ++j) qv[j] = qnext[j];
+        if (qb0 + WAVES * QB < nbw) load_q(qb0 + WAVES * QB, qnext);   // next pass, in flight
         FT q[QB];
         f32x4 shift[QB];
         float m[QB];
 #pragma unroll
         for (int j = 0; j < QB; ++j) {
-            const int qb = min(qb0 + j, nbw - 1);    // a lone last block computes a duplicate
-            const u16x8 qv = *reinterpret_cast<const u16x8*>(
-                p.QKV + (((tb_base + qb) * 3 + 0) * KSD + frag) * 512 + lane * 8);
             float n2 = 0.f;
 #pragma unroll
             for (int i = 0; i < NV; ++i) {
-                const float f = (float)__builtin_bit_cast(__bf16, (uint16_t)qv[slot0 + i]);
+                const float f = (float)__builtin_bit_cast(__bf16, (uint16_t)qv[j][slot0 + i]);
                 n2 = fmaf(f, f, n2);
-                q[j][i] = __builtin_bit_cast(__bf16, (uint16_t)qv[slot0 + i]);
+                q[j][i] = __builtin_bit_cast(__bf16, (uint16_t)qv[j][slot0 + i]);
             }
             m[j] = sqrtf(sum4(n2)) * kmax;
             shift[j] = f32x4{-m[j], -m[j], -m[j], -m[j]};
@@ -164,29 +187,17 @@ __global__ __launch_bounds__(WAVES * 64) void attn_kernel(AttnParams p) {
             for (int rt = 0; rt < RT; ++rt) o[j][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
         }
 
-        for (int sb = 0; sb < nsb; ++sb) {
-            f32x4 s[QB][2];
+        // S^T of a full superblock sb (two 16-key blocks, no padding keys) for every query block
+        auto scores_full = [&](int sb, f32x4 (&s)[QB][2]) {
 #pragma unroll
             for (int kk = 0; kk < 2; ++kk) {
-                const int kb = 2 * sb + kk;
-                if (kb < nbw) {
-                    const FT a = ld_kfrag<DH>(ks, kb, lane);
+                const FT a = ld_kfrag<DH>(ks, 2 * sb + kk, lane);
 #pragma unroll
-                    for (int j = 0; j < QB; ++j) s[j][kk] = Frag<DH>::mma(a, q[j], shift[j]);
-                } else {
-#pragma unroll
-                    for (int j = 0; j < QB; ++j) s[j][kk] = f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
-                }
+                for (int j = 0; j < QB; ++j) s[j][kk] = Frag<DH>::mma(a, q[j], shift[j]);
             }
-            if (tail_mask && sb == nsb - 1) {
-#pragma unroll
-                for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i)
-                        if ((2 * sb + kk) * 16 + 4 * g + i >= N)
-#pragma unroll
-                            for (int j = 0; j < QB; ++j) s[j][kk][i] = -INFINITY;
-            }
+        };
+        // P = exp2(S), row sums, and O^T += V^T P^T for superblock sb
+        auto accumulate = [&](int sb, const f32x4 (&s)[QB][2]) {
             bf16x8 pb[QB];
 #pragma unroll
             for (int j = 0; j < QB; ++j) {
@@ -204,6 +215,41 @@ __global__ __launch_bounds__(WAVES * 64) void attn_kernel(AttnParams p) {
 #pragma unroll
                 for (int j = 0; j < QB; ++j) o[j][rt] = mfma16x16x32(v, pb[j], o[j][rt]);
             }
+        };
+        // Every superblock but the last is full; the loop is software-pipelined (the score
+        // MFMAs of sb+1 are issued before the exponentials of sb) and unrolled by two.
+        f32x4 sa[QB][2], sbuf[QB][2];
+        const int nfull = nsb - 1;
+        if (nfull > 0) scores_full(0, sa);
+        int sb = 0;
+        for (; sb + 2 <= nfull; sb += 2) {
+            scores_full(sb + 1, sbuf);
+            accumulate(sb, sa);
+            if (sb + 2 < nfull) scores_full(sb + 2, sa);
+            accumulate(sb + 1, sbuf);
+        }
+        if (sb < nfull) accumulate(sb, sa);
+        {   // last superblock: missing key block and padding keys are -inf
+            const int last = nsb - 1;
+            f32x4 s[QB][2];
+#pragma unroll
+            for (int kk = 0; kk < 2; ++kk) {
+                const int kb = 2 * last + kk;
+                if (kb < nbw) {
+                    const FT a = ld_kfrag<DH>(ks, kb, lane);
+#pragma unroll
+                    for (int j = 0; j < QB; ++j) s[j][kk] = Frag<DH>::mma(a, q[j], shift[j]);
+                } else {
+#pragma unroll
+                    for (int j = 0; j < QB; ++j) s[j][kk] = f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+                }
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (kb * 16 + 4 * g + i >= N)
+#pragma unroll
+                        for (int j = 0; j < QB; ++j) s[j][kk][i] = -INFINITY;
+            }
+            accumulate(last, s);
         }
 
 #pragma unroll

@@ -64,6 +64,19 @@ PWD_DEV f32x4 relu4(f32x4 v) {
     return r;
 }
 
+// Scheduling shape of a chunk: LA LDS reads first, then (MPR MFMAs, 1 LDS read) pairs, then
+// the last MFMAs, so LA fragment reads stay in flight ahead of the matrix core.
+template <int NREAD, int MPR, int LA>
+PWD_DEV void sched_pipeline() {
+    __builtin_amdgcn_sched_group_barrier(0x100, LA, 0);
+#pragma unroll
+    for (int k = 0; k < NREAD - LA; ++k) {
+        __builtin_amdgcn_sched_group_barrier(0x008, MPR, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, MPR * LA, 0);
+}
+
 // The two LDS buffers of the weight stream. They are separate objects so the compiler can
 // tell that the direct-to-LDS prefetch into one never aliases reads of the other.
 __shared__ __align__(16) uint16_t g_wbuf0[CHUNK * FRAG];
@@ -199,6 +212,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void tok_kernel(TokParams p) {
 #pragma unroll
                     for (int b = 0; b < TB; ++b) x[rt][b] = mfma16x16x32(a, y[ks][b], x[rt][b]);
                 }
+                sched_pipeline<CHUNK, TB, 4>();
             };
             static_assert(S::WO_CHUNKS == 1 || S::WO_CHUNKS % 2 == 0, "Wo chunks");
             if constexpr (S::WO_CHUNKS == 1) {
@@ -261,6 +275,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void tok_kernel(TokParams p) {
 #pragma unroll
                     for (int b = 0; b < TB; ++b) x[rt][b] = mfma16x16x32(a, hb[kh][b], x[rt][b]);
                 }
+            sched_pipeline<CH / 16 + CHUNK, TB, 6>();
         };
         static_assert(S::NMLP % 2 == 0, "feed-forward chunks come in pairs");
         constexpr int P0 = S::WO_CHUNKS & 1;
@@ -341,6 +356,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void tok_kernel(TokParams p) {
                 for (int b = 0; b < TB; ++b)
                     stfrag(p.QKV, (tb0 + b) * (3 * KS) + og, lane, pack_b(q0[b] * sc, q1[b] * sc));
             }
+            sched_pipeline<CHUNK + 2 * S::OG_PER_CHUNK, TB, 6>();
         };
         constexpr int NP = POST ? S::POST_CHUNKS : 0;
         constexpr int Q0 = NP & 1;
