@@ -16,29 +16,40 @@
 // Weights reach the MFMAs through LDS: the host lays every weight fragment out in the exact
 // order the kernel consumes them (a "weight stream"), and the workgroup pulls the stream
 // through a double-buffered LDS ring in 32 KB chunks with direct global->LDS loads, one
-// chunk ahead of the MFMAs. Every fragment read from LDS feeds TB MFMAs of each wavefront.
+// chunk ahead of the MFMAs. Every fragment read from LDS feeds 2-3 MFMAs of each wavefront
+// (one per 16-token block the wavefront owns).
 #include "common.h"
 #include "kernels.h"
 
+#include <type_traits>
+
 namespace {
 
-constexpr int TB = 2;           // 16-token blocks per wavefront
 constexpr int WAVES = 4;        // wavefronts per workgroup
-constexpr int CHUNK = 32;       // weight fragments (1 KB each) per LDS chunk
+constexpr int MAX_CHUNK = 64;   // weight fragments (1 KB each) per LDS chunk, at most
 constexpr int FRAG = 512;       // bf16 values per fragment
 
-template <int D>
+// 16-token blocks per wavefront: three where the registers allow it (more tokens per
+// workgroup share each streamed weight chunk), else two.
+template <int D, int FLAGS>
+constexpr int tok_tb() { return (D == 256 && (FLAGS & TOK_EMBED) == 0) ? 3 : 2; }
+
+template <int D, int TB>
 struct Shape {
+    static constexpr int CHUNK = (D == 256 && TB == 2) ? 64 : 32;  // weight fragments per LDS chunk
     static constexpr int RT = D / 16;                 // 16-row C tiles of a D-vector
     static constexpr int KS = D / 32;                 // 32-deep k-steps of a D-vector
     static constexpr int F = 4 * D;
     static constexpr int CH = 8192 / D;               // hidden units per feed-forward chunk
-    static constexpr int NMLP = F / CH;               // feed-forward chunks
+    static constexpr int NMLP = F / CH;               // feed-forward sub-chunks (32 fragments each)
+    static constexpr int MLP_PER = CHUNK / 32;        // feed-forward sub-chunks per LDS chunk
+    static constexpr int MLP_CHUNKS = NMLP / MLP_PER;
     static constexpr int WO_CHUNKS = RT * KS / CHUNK;
     static constexpr int QKV_CHUNKS = (3 * D / 16) * KS / CHUNK;
     static constexpr int OG_PER_CHUNK = CHUNK / (2 * KS);
-    static constexpr int POST_CHUNKS = WO_CHUNKS + NMLP;
-    static_assert((CH / 16) * KS + RT * (CH / 32) == CHUNK, "one feed-forward chunk per LDS chunk");
+    static constexpr int POST_CHUNKS = WO_CHUNKS + MLP_CHUNKS;
+    static_assert((CH / 16) * KS + RT * (CH / 32) == 32, "32 fragments per feed-forward sub-chunk");
+    static_assert(NMLP % MLP_PER == 0 && CHUNK <= MAX_CHUNK, "whole feed-forward chunks");
     static_assert(RT * KS % CHUNK == 0 && (3 * D / 16) * KS % CHUNK == 0, "whole chunks");
 };
 
@@ -79,15 +90,17 @@ PWD_DEV void sched_pipeline() {
 
 // The two LDS buffers of the weight stream. They are separate objects so the compiler can
 // tell that the direct-to-LDS prefetch into one never aliases reads of the other.
-__shared__ __align__(16) uint16_t g_wbuf0[CHUNK * FRAG];
-__shared__ __align__(16) uint16_t g_wbuf1[CHUNK * FRAG];
-
-template <int PAR>
-PWD_DEV uint16_t* wbuf() { return PAR ? g_wbuf1 : g_wbuf0; }
+template <int PAR, int CHUNK>
+PWD_DEV uint16_t* wbuf() {
+    static_assert(CHUNK <= MAX_CHUNK, "chunk size");
+    __shared__ __align__(16) uint16_t buf[CHUNK * FRAG];   // one object per (buffer, size)
+    return buf;
+}
 
 // The weight stream of one launch: `post` chunks first, then `qkv` chunks, pulled through
 // the two LDS buffers (chunk i lives in buffer i % 2). begin<i % 2>(i) makes chunk i visible
 // to every wavefront and starts the load of chunk i+1 into the other buffer.
+template <int CHUNK>
 struct WeightPipe {
     const uint16_t* post;
     const uint16_t* qkv;
@@ -98,7 +111,7 @@ struct WeightPipe {
     __device__ void issue(int i) const {
         const uint16_t* src = i < n_post ? post + (size_t)i * CHUNK * FRAG
                                          : qkv + (size_t)(i - n_post) * CHUNK * FRAG;
-        uint16_t* dst = wbuf<PAR>();
+        uint16_t* dst = wbuf<PAR, CHUNK>();
 #pragma unroll
         for (int j = 0; j < CHUNK / WAVES; ++j) {
             const int f = wave * (CHUNK / WAVES) + j;
@@ -107,19 +120,31 @@ struct WeightPipe {
                 (__attribute__((address_space(3))) void*)(dst + f * FRAG), 16, 0, 0);
         }
     }
+    // Chunk i is visible to every wavefront after sync(i); prefetch(i) then starts chunk
+    // i+1. LDS reads of other tables belong between the two: no prefetch is in flight then,
+    // so the compiler has nothing to wait for.
     template <int PAR>
-    __device__ const uint16_t* begin(int i) const {
+    __device__ const uint16_t* sync(int) const {
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's part of chunk i landed
         __syncthreads();                                   // ... and everyone's; buffer i-1 is free
+        return wbuf<PAR, CHUNK>();
+    }
+    template <int PAR>
+    __device__ void prefetch(int i) const {
         if (i + 1 < total) issue<1 - PAR>(i + 1);
         __builtin_amdgcn_sched_barrier(0);                 // keep the prefetch ahead of the MFMAs
-        return wbuf<PAR>();
+    }
+    template <int PAR>
+    __device__ const uint16_t* begin(int i) const {
+        const uint16_t* b = sync<PAR>(i);
+        prefetch<PAR>(i);
+        return b;
     }
 };
 
 // LayerNorm over the D features of each token (biased variance, two passes); gamma and
 // beta are in LDS.
-template <int RT>
+template <int RT, int TB>
 PWD_DEV void layer_norm(f32x4 (&x)[RT][TB], const float* gamma, const float* beta, float eps, int g) {
     constexpr float inv_d = 1.0f / (RT * 16);
 #pragma unroll
@@ -160,7 +185,8 @@ struct Vecs {
 
 template <int D, int FLAGS>
 __global__ __launch_bounds__(WAVES * 64, 1) void tok_kernel(TokParams p) {
-    using S = Shape<D>;
+    constexpr int TB = tok_tb<D, FLAGS>();
+    using S = Shape<D, TB>;
     using V = Vecs<D>;
     constexpr int RT = S::RT, KS = S::KS, CH = S::CH;
     constexpr bool POST = (FLAGS & TOK_POST) != 0, QKV = (FLAGS & TOK_QKV) != 0;
@@ -170,14 +196,15 @@ __global__ __launch_bounds__(WAVES * 64, 1) void tok_kernel(TokParams p) {
     const int col = lane & 15;
     const int64_t tb0 = ((int64_t)blockIdx.x * WAVES + wave) * TB;
 
-    WeightPipe pipe;
+    constexpr int CHUNK = S::CHUNK;
+    WeightPipe<CHUNK> pipe;
     pipe.post = p.post_stream;
     pipe.qkv = p.qkv_stream;
     pipe.n_post = POST ? S::POST_CHUNKS : 0;
     pipe.total = pipe.n_post + (QKV ? S::QKV_CHUNKS : 0);
     pipe.lane = lane;
     pipe.wave = wave;
-    pipe.issue<0>(0);
+    pipe.template issue<0>(0);
 
     __shared__ __align__(16) float vec[V::SIZE];
     if (POST) {
@@ -216,12 +243,12 @@ __global__ __launch_bounds__(WAVES * 64, 1) void tok_kernel(TokParams p) {
             };
             static_assert(S::WO_CHUNKS == 1 || S::WO_CHUNKS % 2 == 0, "Wo chunks");
             if constexpr (S::WO_CHUNKS == 1) {
-                wo_chunk(pipe.begin<0>(0), 0);
+                wo_chunk(pipe.template begin<0>(0), 0);
             } else {
 #pragma unroll
                 for (int c = 0; c < S::WO_CHUNKS; c += 2) {
-                    wo_chunk(pipe.begin<0>(c), c);
-                    wo_chunk(pipe.begin<1>(c + 1), c + 1);
+                    wo_chunk(pipe.template begin<0>(c), c);
+                    wo_chunk(pipe.template begin<1>(c + 1), c + 1);
                 }
             }
         }
@@ -231,7 +258,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void tok_kernel(TokParams p) {
 #pragma unroll
             for (int b = 0; b < TB; ++b) x[rt][b] += bias;
         }
-        layer_norm<RT>(x, vec + V::G1, vec + V::BE1, p.eps, g);
+        layer_norm<RT, TB>(x, vec + V::G1, vec + V::BE1, p.eps, g);
 
         // ---- feed-forward, hidden units in chunks of CH; accumulators start at X + b_2
         bf16x8 xb[KS][TB];
@@ -245,14 +272,12 @@ __global__ __launch_bounds__(WAVES * 64, 1) void tok_kernel(TokParams p) {
 #pragma unroll
             for (int b = 0; b < TB; ++b) x[rt][b] += bias;
         }
-        auto mlp_chunk = [&](const uint16_t* buf, int c) {
+        auto mlp_sub = [&](const uint16_t* buf, const f32x4 (&bias)[CH / 16]) {
             f32x4 h[CH / 16][TB];
 #pragma unroll
-            for (int rh = 0; rh < CH / 16; ++rh) {
-                const f32x4 bias = ld4(vec + V::B1 + c * CH + rh * 16 + 4 * g);
+            for (int rh = 0; rh < CH / 16; ++rh)
 #pragma unroll
-                for (int b = 0; b < TB; ++b) h[rh][b] = bias;
-            }
+                for (int b = 0; b < TB; ++b) h[rh][b] = bias[rh];
 #pragma unroll
             for (int rh = 0; rh < CH / 16; ++rh)
 #pragma unroll
@@ -275,15 +300,30 @@ __global__ __launch_bounds__(WAVES * 64, 1) void tok_kernel(TokParams p) {
 #pragma unroll
                     for (int b = 0; b < TB; ++b) x[rt][b] = mfma16x16x32(a, hb[kh][b], x[rt][b]);
                 }
-            sched_pipeline<CH / 16 + CHUNK, TB, 6>();
         };
-        static_assert(S::NMLP % 2 == 0, "feed-forward chunks come in pairs");
+        constexpr int MP = S::MLP_PER;
+        auto mlp_chunk = [&](auto par, int c) {
+            constexpr int PAR = decltype(par)::value;
+            const int ci = S::WO_CHUNKS + c;
+            const uint16_t* buf = pipe.template sync<PAR>(ci);
+            f32x4 bias[MP][CH / 16];
+#pragma unroll
+            for (int u = 0; u < MP; ++u)
+#pragma unroll
+                for (int rh = 0; rh < CH / 16; ++rh)
+                    bias[u][rh] = ld4(vec + V::B1 + (c * MP + u) * CH + rh * 16 + 4 * g);
+            pipe.template prefetch<PAR>(ci);
+#pragma unroll
+            for (int u = 0; u < MP; ++u) mlp_sub(buf + u * 32 * FRAG, bias[u]);
+            sched_pipeline<MP * (CH / 16 + 32), TB, 6>();
+        };
+        static_assert(S::MLP_CHUNKS % 2 == 0, "feed-forward chunks come in pairs");
         constexpr int P0 = S::WO_CHUNKS & 1;
-        for (int c = 0; c < S::NMLP; c += 2) {
-            mlp_chunk(pipe.begin<P0>(S::WO_CHUNKS + c), c);
-            mlp_chunk(pipe.begin<1 - P0>(S::WO_CHUNKS + c + 1), c + 1);
+        for (int c = 0; c < S::MLP_CHUNKS; c += 2) {
+            mlp_chunk(std::integral_constant<int, P0>{}, c);
+            mlp_chunk(std::integral_constant<int, 1 - P0>{}, c + 1);
         }
-        layer_norm<RT>(x, vec + V::G2, vec + V::BE2, p.eps, g);
+        layer_norm<RT, TB>(x, vec + V::G2, vec + V::BE2, p.eps, g);
     }
 
     if constexpr ((FLAGS & TOK_EMBED) != 0) {
@@ -316,12 +356,15 @@ __global__ __launch_bounds__(WAVES * 64, 1) void tok_kernel(TokParams p) {
         }
     }
 
+    auto store_x = [&]() {
 #pragma unroll
-    for (int b = 0; b < TB; ++b)
+        for (int b = 0; b < TB; ++b)
 #pragma unroll
-        for (int rt = 0; rt < RT; ++rt)
-            *reinterpret_cast<f32x4*>(p.X + (((tb0 + b) * RT + rt) * 64 + lane) * 4) = x[rt][b];
+            for (int rt = 0; rt < RT; ++rt)
+                *reinterpret_cast<f32x4*>(p.X + (((tb0 + b) * RT + rt) * 64 + lane) * 4) = x[rt][b];
+    };
 
+    store_x();
     if constexpr (QKV) {
         bf16x8 xb[KS][TB];
 #pragma unroll
@@ -329,17 +372,26 @@ __global__ __launch_bounds__(WAVES * 64, 1) void tok_kernel(TokParams p) {
 #pragma unroll
             for (int b = 0; b < TB; ++b) xb[ks][b] = pack_b(x[2 * ks][b], x[2 * ks + 1][b]);
         // 3D output features in groups of 32 (= one B fragment of Q, K or V)
-        auto qkv_chunk = [&](const uint16_t* buf, int qc) {
+        constexpr int NP = POST ? S::POST_CHUNKS : 0;
+        constexpr int OPC = S::OG_PER_CHUNK;
+        auto qkv_chunk = [&](auto par, int qc) {
+            constexpr int PAR = decltype(par)::value;
+            const uint16_t* buf = pipe.template sync<PAR>(NP + qc);
+            f32x4 bias[OPC][2];
 #pragma unroll
-            for (int o2 = 0; o2 < S::OG_PER_CHUNK; ++o2) {
-                const int og = qc * S::OG_PER_CHUNK + o2;
+            for (int o2 = 0; o2 < OPC; ++o2)
+#pragma unroll
+                for (int hh = 0; hh < 2; ++hh)
+                    bias[o2][hh] = ld4(vec + V::BQKV + (qc * OPC + o2) * 32 + hh * 16 + 4 * g);
+            pipe.template prefetch<PAR>(NP + qc);
+#pragma unroll
+            for (int o2 = 0; o2 < OPC; ++o2) {
+                const int og = qc * OPC + o2;
                 f32x4 q0[TB], q1[TB];
-                const f32x4 bias0 = ld4(vec + V::BQKV + og * 32 + 4 * g);
-                const f32x4 bias1 = ld4(vec + V::BQKV + og * 32 + 16 + 4 * g);
 #pragma unroll
                 for (int b = 0; b < TB; ++b) {
-                    q0[b] = bias0;
-                    q1[b] = bias1;
+                    q0[b] = bias[o2][0];
+                    q1[b] = bias[o2][1];
                 }
 #pragma unroll
                 for (int ks = 0; ks < KS; ++ks) {
@@ -356,29 +408,32 @@ __global__ __launch_bounds__(WAVES * 64, 1) void tok_kernel(TokParams p) {
                 for (int b = 0; b < TB; ++b)
                     stfrag(p.QKV, (tb0 + b) * (3 * KS) + og, lane, pack_b(q0[b] * sc, q1[b] * sc));
             }
-            sched_pipeline<CHUNK + 2 * S::OG_PER_CHUNK, TB, 6>();
+            sched_pipeline<CHUNK, TB, 6>();
         };
-        constexpr int NP = POST ? S::POST_CHUNKS : 0;
         constexpr int Q0 = NP & 1;
         int qc = 0;
         for (; qc + 1 < S::QKV_CHUNKS; qc += 2) {
-            qkv_chunk(pipe.begin<Q0>(NP + qc), qc);
-            qkv_chunk(pipe.begin<1 - Q0>(NP + qc + 1), qc + 1);
+            qkv_chunk(std::integral_constant<int, Q0>{}, qc);
+            qkv_chunk(std::integral_constant<int, 1 - Q0>{}, qc + 1);
         }
-        if constexpr (S::QKV_CHUNKS % 2 == 1) qkv_chunk(pipe.begin<Q0>(NP + qc), qc);
+        if constexpr (S::QKV_CHUNKS % 2 == 1) qkv_chunk(std::integral_constant<int, Q0>{}, qc);
     }
+}
+
+template <int D, int FLAGS>
+void launch_variant(const TokParams& p, int64_t n_tb, hipStream_t s) {
+    const int64_t per_wg = (int64_t)WAVES * tok_tb<D, FLAGS>();
+    const dim3 grid((unsigned)((n_tb + per_wg - 1) / per_wg)), block(WAVES * 64);
+    tok_kernel<D, FLAGS><<<grid, block, 0, s>>>(p);
 }
 
 template <int D>
 hipError_t launch_tok_d(int flags, const TokParams& p, int64_t n_tb, hipStream_t s) {
-    const int64_t per_wg = (int64_t)WAVES * TB;
-    const dim3 grid((unsigned)((n_tb + per_wg - 1) / per_wg)), block(WAVES * 64);
     switch (flags) {
-        case TOK_EMBED | TOK_QKV: tok_kernel<D, TOK_EMBED | TOK_QKV><<<grid, block, 0, s>>>(p); break;
-        case TOK_POST | TOK_QKV: tok_kernel<D, TOK_POST | TOK_QKV><<<grid, block, 0, s>>>(p); break;
-        case TOK_POST | TOK_EMBED | TOK_QKV:
-            tok_kernel<D, TOK_POST | TOK_EMBED | TOK_QKV><<<grid, block, 0, s>>>(p); break;
-        case TOK_POST: tok_kernel<D, TOK_POST><<<grid, block, 0, s>>>(p); break;
+        case TOK_EMBED | TOK_QKV: launch_variant<D, TOK_EMBED | TOK_QKV>(p, n_tb, s); break;
+        case TOK_POST | TOK_QKV: launch_variant<D, TOK_POST | TOK_QKV>(p, n_tb, s); break;
+        case TOK_POST | TOK_EMBED | TOK_QKV: launch_variant<D, TOK_POST | TOK_EMBED | TOK_QKV>(p, n_tb, s); break;
+        case TOK_POST: launch_variant<D, TOK_POST>(p, n_tb, s); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -386,9 +441,9 @@ hipError_t launch_tok_d(int flags, const TokParams& p, int64_t n_tb, hipStream_t
 
 }  // namespace
 
-// Token blocks are processed in groups of WAVES*TB; every buffer indexed here must be
-// allocated for n_tb rounded up to that multiple.
-int64_t tok_block_granule() { return (int64_t)WAVES * TB; }
+// Token blocks are processed in groups of WAVES*TB (TB = 2 or 3 by variant); every buffer
+// indexed here must be allocated for n_tb rounded up to a multiple of all of them.
+int64_t tok_block_granule() { return (int64_t)WAVES * 6; }
 
 // Fragments of the weight streams (see tok_kernel): hidden units per feed-forward chunk.
 int tok_mlp_chunk(int D) { return 8192 / D; }
