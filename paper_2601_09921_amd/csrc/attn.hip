@@ -1,9 +1,9 @@
 // Multi-head self-attention across the stabilizer tokens of each window (App. A.2; the
 // model table's Multi-Head Attention), bf16 MFMA with fp32 softmax statistics.
 //
-// One workgroup per (window, head). K_h (as MFMA A fragments) and V_h^T are staged in LDS
-// once; each wavefront then takes pairs of 16-query blocks and streams the keys in steps of
-// 32:
+// One workgroup per (window, head), of 1, 2 or 4 wavefronts by window size. K_h (as MFMA A
+// fragments) and V_h^T are staged in LDS once; each wavefront then takes pairs of 16-query
+// blocks and streams the keys in steps of 32:
 //   S^T = K Q'^T - m      (16 keys x 16 queries per MFMA, lanes hold queries)
 //   P^T = exp2(S^T)       (P^T is the S^T accumulator rounded to bf16, no shuffle)
 //   O^T += V^T P^T,  l += sum P
@@ -19,7 +19,6 @@
 
 namespace {
 
-constexpr int WAVES = 4;
 constexpr int QB = 2;                 // query blocks per wavefront pass
 constexpr int SBATCH = 10;            // key blocks per wavefront per staging batch (d=25: one batch)
 
@@ -67,7 +66,7 @@ PWD_DEV float sum4(float v) {
     return v + __shfl_xor(v, 32);
 }
 
-template <int DH>
+template <int DH, int WAVES>
 __global__ __launch_bounds__(WAVES * 64) void attn_kernel(AttnParams p) {
     using FT = typename Frag<DH>::T;
     constexpr int RT = DH / 16;                 // 16-row tiles of O^T
@@ -314,22 +313,28 @@ size_t attn_smem_bytes(int dh, int Npad, int nbw) {
     return (size_t)nbw * 64 * (dh == 32 ? 8 : 4) * 2 + (size_t)dh * vt_stride(Npad) * 2;
 }
 
+template <int DH, int WAVES>
+hipError_t launch_shape(const AttnParams& p, int nwin, hipStream_t s) {
+    const size_t smem = attn_smem_bytes(DH, p.Npad, p.nbw);
+    hipError_t e = hipFuncSetAttribute((const void*)attn_kernel<DH, WAVES>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+    if (e != hipSuccess) return e;
+    attn_kernel<DH, WAVES><<<dim3((unsigned)nwin * p.H), dim3(WAVES * 64), smem, s>>>(p);
+    return hipGetLastError();
+}
+
+template <int DH>
+hipError_t launch_dh(const AttnParams& p, int nwin, hipStream_t s) {
+    // wavefronts per (window, head): enough for two query blocks each, at most four, so
+    // small windows run as many small workgroups rather than idle wavefronts
+    if (p.nbw <= 2 * QB) return launch_shape<DH, 1>(p, nwin, s);
+    if (p.nbw <= 4 * QB) return launch_shape<DH, 2>(p, nwin, s);
+    return launch_shape<DH, 4>(p, nwin, s);
+}
+
 hipError_t launch_attn(int dh, const AttnParams& p, int nwin, hipStream_t s) {
     if (nwin <= 0) return hipSuccess;
-    const size_t smem = attn_smem_bytes(dh, p.Npad, p.nbw);
-    const dim3 grid((unsigned)nwin * p.H), block(WAVES * 64);
-    if (dh == 32) {
-        hipError_t e = hipFuncSetAttribute((const void*)attn_kernel<32>,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-        if (e != hipSuccess) return e;
-        attn_kernel<32><<<grid, block, smem, s>>>(p);
-    } else if (dh == 16) {
-        hipError_t e = hipFuncSetAttribute((const void*)attn_kernel<16>,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-        if (e != hipSuccess) return e;
-        attn_kernel<16><<<grid, block, smem, s>>>(p);
-    } else {
-        return hipErrorInvalidValue;
-    }
-    return hipGetLastError();
+    if (dh == 32) return launch_dh<32>(p, nwin, s);
+    if (dh == 16) return launch_dh<16>(p, nwin, s);
+    return hipErrorInvalidValue;
 }

@@ -3,12 +3,15 @@
 // App. A model). Used for the fp32 configurations (d_model <= 64, about d <= 5), where a
 // window is a few kilobytes and the batch is small, so one launch per decode is the point.
 //
-// All matrix products are plain fp32 FMA loops; every output element is produced by one
-// thread in a fixed order, so results do not depend on the batch.
+// All matrix products are fp32 FMA loops with the model width as a compile-time constant,
+// unrolled with four independent partial sums so the weight loads overlap. Every output
+// element is produced by one thread in a fixed order, so results do not depend on the batch.
 #include "common.h"
 #include "kernels.h"
 
 namespace {
+
+constexpr int THREADS = 512;
 
 struct LayerPtrs {
     const float *Wq, *bq, *Wk, *bk, *Wv, *bv, *Wo, *bo, *g1, *be1, *W1, *b1, *W2, *b2, *g2, *be2;
@@ -28,13 +31,27 @@ __device__ const float* layer_ptrs(const float* w, int D, int F, int l, LayerPtr
     return q;
 }
 
-// out[n][o] = bias[o] + sum_k in[n][k] W[k][o]  (+ res[n][o] when res != nullptr)
-__device__ void linear(const float* in, int N, int K, const float* W, const float* bias, int O,
-                       float* out, const float* res, bool relu) {
-    for (int idx = threadIdx.x; idx < N * O; idx += blockDim.x) {
+// sum_k in[k] W[k*O + o] for a compile-time K, four interleaved partial sums
+template <int K>
+PWD_DEV float dot_col(const float* in, const float* __restrict__ W, int O, int o) {
+    float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+#pragma unroll 8
+    for (int k = 0; k < K; k += 4) {
+        a0 = fmaf(in[k + 0], W[(size_t)(k + 0) * O + o], a0);
+        a1 = fmaf(in[k + 1], W[(size_t)(k + 1) * O + o], a1);
+        a2 = fmaf(in[k + 2], W[(size_t)(k + 2) * O + o], a2);
+        a3 = fmaf(in[k + 3], W[(size_t)(k + 3) * O + o], a3);
+    }
+    return (a0 + a1) + (a2 + a3);
+}
+
+// out[n][o] = bias[o] + sum_k in[n][k] W[k][o]  (+ res[n][o]); optional ReLU before res
+template <int K, int O>
+PWD_DEV void linear(const float* in, int N, const float* __restrict__ W, const float* __restrict__ bias,
+                    float* out, const float* res, bool relu) {
+    for (int idx = threadIdx.x; idx < N * O; idx += THREADS) {
         const int n = idx / O, o = idx % O;
-        float acc = bias[o];
-        for (int k = 0; k < K; ++k) acc = fmaf(in[n * K + k], W[(size_t)k * O + o], acc);
+        float acc = bias[o] + dot_col<K>(in + n * K, W, O, o);
         if (relu) acc = fmaxf(acc, 0.f);
         if (res) acc += res[idx];
         out[idx] = acc;
@@ -42,22 +59,28 @@ __device__ void linear(const float* in, int N, int K, const float* W, const floa
 }
 
 // x[n][:] = LayerNorm(x[n][:]) for each token (one thread per token, two passes)
-__device__ void layer_norm_rows(float* x, int N, int D, const float* g, const float* b, float eps) {
-    for (int n = threadIdx.x; n < N; n += blockDim.x) {
+template <int D>
+PWD_DEV void layer_norm_rows(float* x, int N, const float* g, const float* b, float eps) {
+    for (int n = threadIdx.x; n < N; n += THREADS) {
         float* r = x + n * D;
         float s = 0.f;
+#pragma unroll
         for (int k = 0; k < D; ++k) s += r[k];
         const float mean = s / D;
         float v = 0.f;
+#pragma unroll
         for (int k = 0; k < D; ++k) v += (r[k] - mean) * (r[k] - mean);
         const float rstd = rsqrtf(v / D + eps);
+#pragma unroll
         for (int k = 0; k < D; ++k) r[k] = (r[k] - mean) * rstd * g[k] + b[k];
     }
 }
 
-__global__ __launch_bounds__(256) void f32_window_kernel(F32Params p) {
+template <int D>
+__global__ __launch_bounds__(THREADS) void f32_window_kernel(F32Params p) {
+    constexpr int F = 4 * D;
     const int win = blockIdx.x;
-    const int N = p.in.N, D = p.D, F = p.F, H = p.H, dh = D / H, d = p.in.d;
+    const int N = p.in.N, H = p.H, dh = D / H, d = p.in.d;
     extern __shared__ __align__(16) float sm[];
     float* X = sm;                 // [N][D] state / residual stream
     float* Z = X + N * D;          // [N][D] scratch
@@ -68,7 +91,7 @@ __global__ __launch_bounds__(256) void f32_window_kernel(F32Params p) {
     float* Hd = A + N * D;         // [N][F] feed-forward hidden
     float* S = Hd + N * F;         // [H][N][N] scores / probabilities
     __shared__ uint32_t ev[32];    // event words of one round (N <= 1024)
-    __shared__ float red[256];
+    __shared__ float red[THREADS];
 
     const int type = p.in.types[win];
     const uint32_t* meas = p.in.meas + (int64_t)win * (p.in.W + 1) * p.in.words;
@@ -76,11 +99,11 @@ __global__ __launch_bounds__(256) void f32_window_kernel(F32Params p) {
     const float scale = rsqrtf((float)dh);
 
     for (int t = 0; t < p.in.W; ++t) {
-        for (int wd = threadIdx.x; wd < p.in.words; wd += blockDim.x)
+        for (int wd = threadIdx.x; wd < p.in.words; wd += THREADS)
             ev[wd] = type > WIN_FINAL ? 0u : event_word(meas, p.in.words, t, wd, type, p.in.b_left, d);
         __syncthreads();
         // embedding + fold: X = kappa (E w_e + b_e + PE + X), X = 0 before round 0
-        for (int idx = threadIdx.x; idx < N * D; idx += blockDim.x) {
+        for (int idx = threadIdx.x; idx < N * D; idx += THREADS) {
             const int n = idx / D, k = idx % D;
             const float e = (float)((ev[n >> 5] >> (n & 31)) & 1u);
             const float s = fmaf(e, we[k], p.S0[idx]);
@@ -90,18 +113,18 @@ __global__ __launch_bounds__(256) void f32_window_kernel(F32Params p) {
         for (int l = 0; l < p.L; ++l) {
             LayerPtrs L;
             layer_ptrs(p.w, D, F, l, L);
-            linear(X, N, D, L.Wq, L.bq, D, Q, nullptr, false);
-            linear(X, N, D, L.Wk, L.bk, D, K, nullptr, false);
-            linear(X, N, D, L.Wv, L.bv, D, V, nullptr, false);
+            linear<D, D>(X, N, L.Wq, L.bq, Q, nullptr, false);
+            linear<D, D>(X, N, L.Wk, L.bk, K, nullptr, false);
+            linear<D, D>(X, N, L.Wv, L.bv, V, nullptr, false);
             __syncthreads();
-            for (int idx = threadIdx.x; idx < H * N * N; idx += blockDim.x) {
+            for (int idx = threadIdx.x; idx < H * N * N; idx += THREADS) {
                 const int h = idx / (N * N), q = (idx / N) % N, k = idx % N;
                 float acc = 0.f;
                 for (int e = 0; e < dh; ++e) acc = fmaf(Q[q * D + h * dh + e], K[k * D + h * dh + e], acc);
                 S[idx] = acc * scale;
             }
             __syncthreads();
-            for (int row = threadIdx.x; row < H * N; row += blockDim.x) {
+            for (int row = threadIdx.x; row < H * N; row += THREADS) {
                 float* r = S + row * N;
                 float mx = r[0];
                 for (int k = 1; k < N; ++k) mx = fmaxf(mx, r[k]);
@@ -114,22 +137,22 @@ __global__ __launch_bounds__(256) void f32_window_kernel(F32Params p) {
                 for (int k = 0; k < N; ++k) r[k] *= inv;
             }
             __syncthreads();
-            for (int idx = threadIdx.x; idx < N * D; idx += blockDim.x) {
+            for (int idx = threadIdx.x; idx < N * D; idx += THREADS) {
                 const int q = idx / D, c = idx % D, h = c / dh;
                 float acc = 0.f;
                 for (int k = 0; k < N; ++k) acc = fmaf(S[(h * N + q) * N + k], V[k * D + c], acc);
                 A[idx] = acc;
             }
             __syncthreads();
-            linear(A, N, D, L.Wo, L.bo, D, Z, X, false);      // Z = X + A Wo + bo
+            linear<D, D>(A, N, L.Wo, L.bo, Z, X, false);      // Z = X + A Wo + bo
             __syncthreads();
-            layer_norm_rows(Z, N, D, L.g1, L.be1, p.eps);
+            layer_norm_rows<D>(Z, N, L.g1, L.be1, p.eps);
             __syncthreads();
-            linear(Z, N, D, L.W1, L.b1, F, Hd, nullptr, true);
+            linear<D, F>(Z, N, L.W1, L.b1, Hd, nullptr, true);
             __syncthreads();
-            linear(Hd, N, F, L.W2, L.b2, D, X, Z, false);     // X = Z + FF(Z)
+            linear<F, D>(Hd, N, L.W2, L.b2, X, Z, false);     // X = Z + FF(Z)
             __syncthreads();
-            layer_norm_rows(X, N, D, L.g2, L.be2, p.eps);
+            layer_norm_rows<D>(X, N, L.g2, L.be2, p.eps);
             __syncthreads();
         }
     }
@@ -143,7 +166,7 @@ __global__ __launch_bounds__(256) void f32_window_kernel(F32Params p) {
     const float* beta = wo + (size_t)d * D + 1;
     const int gw = d + 1;
     float part = 0.f;
-    for (int idx = threadIdx.x; idx < d * D; idx += blockDim.x) {
+    for (int idx = threadIdx.x; idx < d * D; idx += THREADS) {
         const int i = idx / D, o = idx % D;
         float pool = 0.f;
         for (int j = 0; j < d; ++j) {
@@ -152,8 +175,7 @@ __global__ __launch_bounds__(256) void f32_window_kernel(F32Params p) {
                 for (int b = 0; b < 2; ++b) {
                     const int tok = p.cell_token[(i + a) * gw + (j + b)];
                     if (tok < 0) continue;
-                    const float* wab = Wc + (size_t)(a * 2 + b) * D * D;
-                    for (int k = 0; k < D; ++k) acc = fmaf(X[tok * D + k], wab[(size_t)k * D + o], acc);
+                    acc += dot_col<D>(X + tok * D, Wc + (size_t)(a * 2 + b) * D * D, D, o);
                 }
             pool += fmaxf(acc, 0.f);
         }
@@ -161,7 +183,7 @@ __global__ __launch_bounds__(256) void f32_window_kernel(F32Params p) {
     }
     red[threadIdx.x] = part;
     __syncthreads();
-    for (int n = blockDim.x / 2; n > 0; n >>= 1) {
+    for (int n = THREADS / 2; n > 0; n >>= 1) {
         if ((int)threadIdx.x < n) red[threadIdx.x] += red[threadIdx.x + n];
         __syncthreads();
     }
@@ -178,6 +200,16 @@ __global__ __launch_bounds__(256) void f32_window_kernel(F32Params p) {
     }
 }
 
+template <int D>
+hipError_t launch_d(const F32Params& p, hipStream_t s) {
+    const size_t smem = f32_window_smem_bytes(p.in.N, p.D, p.H, p.F);
+    hipError_t e = hipFuncSetAttribute((const void*)f32_window_kernel<D>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+    if (e != hipSuccess) return e;
+    f32_window_kernel<D><<<dim3((unsigned)p.in.nwin), dim3(THREADS), smem, s>>>(p);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 size_t f32_window_smem_bytes(int N, int D, int H, int F) {
@@ -186,10 +218,10 @@ size_t f32_window_smem_bytes(int N, int D, int H, int F) {
 
 hipError_t launch_f32_window(const F32Params& p, hipStream_t s) {
     if (p.in.nwin <= 0) return hipSuccess;
-    const size_t smem = f32_window_smem_bytes(p.in.N, p.D, p.H, p.F);
-    hipError_t e = hipFuncSetAttribute((const void*)f32_window_kernel,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-    if (e != hipSuccess) return e;
-    f32_window_kernel<<<dim3((unsigned)p.in.nwin), dim3(256), smem, s>>>(p);
-    return hipGetLastError();
+    switch (p.D) {
+        case 16: return launch_d<16>(p, s);
+        case 32: return launch_d<32>(p, s);
+        case 64: return launch_d<64>(p, s);
+        default: return hipErrorInvalidValue;
+    }
 }
