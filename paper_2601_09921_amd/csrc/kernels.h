@@ -28,7 +28,7 @@ struct TokParams {
     // weight streams: bf16 A fragments in consumption order (see tok.hip)
     const uint16_t* post_stream;   // out-projection + feed-forward of the POST layer
     const uint16_t* qkv_stream;    // Q/K/V projection of the layer that follows
-    const float *bo, *g1, *be1, *b1, *b2, *g2, *be2;   // POST layer vectors
+    const float* post_vecs;   // POST layer vectors [b_o g1 be1 b2 g2 be2 | b1], 10 D floats
     const float* bqkv;                                  // [3D] bias of the Q/K/V projection
 };
 

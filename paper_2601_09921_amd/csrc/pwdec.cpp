@@ -138,7 +138,7 @@ struct pwd_decoder {
     // views into `weights`
     struct Layer {
         const uint16_t *post, *qkv;
-        const float *bo, *g1, *be1, *b1, *b2, *g2, *be2, *bqkv;
+        const float *post_vecs, *bqkv;   // [b_o g1 be1 b2 g2 be2 | b1] (10 D) and [b_q b_k b_v]
     };
     std::vector<Layer> layers;
     const float* S0 = nullptr;
@@ -300,7 +300,7 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
     };
     const size_t off_cell = put(cell_token.data(), cell_token.size() * sizeof(int));
 
-    struct LayerOff { size_t post, qkv, bo, g1, be1, b1, b2, g2, be2, bqkv; };
+    struct LayerOff { size_t post, qkv, post_vecs, bqkv; };
     std::vector<LayerOff> loff(L);
     size_t off_S0 = 0, off_we = 0, off_Wc = 0, off_bc = 0, off_wo = 0, off_f32 = 0;
     const size_t lf = layer_floats(D, F);
@@ -341,13 +341,10 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
             fr.clear();
             append_qkv_stream(fr, wqkv.data(), D);
             loff[l].qkv = put(fr.data(), fr.size() * 2);
-            loff[l].bo = put(bo, D * 4);
-            loff[l].g1 = put(g1, D * 4);
-            loff[l].be1 = put(be1, D * 4);
-            loff[l].b1 = put(b1, F * 4);
-            loff[l].b2 = put(b2, D * 4);
-            loff[l].g2 = put(g2, D * 4);
-            loff[l].be2 = put(be2, D * 4);
+            std::vector<float> pv;   // the token kernel's LDS vector table order
+            for (const float* v : {bo, g1, be1, b2, g2, be2}) pv.insert(pv.end(), v, v + D);
+            pv.insert(pv.end(), b1, b1 + F);
+            loff[l].post_vecs = put(pv.data(), pv.size() * 4);
             loff[l].bqkv = put(bqkv.data(), 3 * D * 4);
         }
         {
@@ -395,8 +392,8 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
         for (int l = 0; l < L; ++l) {
             pwd_decoder::Layer ly;
             ly.post = hptr(loff[l].post); ly.qkv = hptr(loff[l].qkv);
-            ly.bo = fptr(loff[l].bo); ly.g1 = fptr(loff[l].g1); ly.be1 = fptr(loff[l].be1); ly.b1 = fptr(loff[l].b1);
-            ly.b2 = fptr(loff[l].b2); ly.g2 = fptr(loff[l].g2); ly.be2 = fptr(loff[l].be2); ly.bqkv = fptr(loff[l].bqkv);
+            ly.post_vecs = fptr(loff[l].post_vecs);
+            ly.bqkv = fptr(loff[l].bqkv);
             dec->layers.push_back(ly);
         }
         const int64_t gran = tok_block_granule();
@@ -493,7 +490,7 @@ int decode_windows(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_ty
     auto set_post = [&](int l) {
         const auto& ly = dec->layers[l];
         tp.post_stream = ly.post;
-        tp.bo = ly.bo; tp.g1 = ly.g1; tp.be1 = ly.be1; tp.b1 = ly.b1; tp.b2 = ly.b2; tp.g2 = ly.g2; tp.be2 = ly.be2;
+        tp.post_vecs = ly.post_vecs;
     };
     auto set_qkv = [&](int l) {
         tp.qkv_stream = dec->layers[l].qkv;

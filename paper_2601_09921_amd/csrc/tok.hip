@@ -15,13 +15,16 @@
 //
 // Weights reach the MFMAs through LDS: the host lays every weight fragment out in the exact
 // order the kernel consumes them (a "weight stream"), and the workgroup pulls the stream
-// through a double-buffered LDS ring in 32 KB chunks with direct global->LDS loads, one
-// chunk ahead of the MFMAs. Every fragment read from LDS feeds 2-3 MFMAs of each wavefront
-// (one per 16-token block the wavefront owns).
+// through a double-buffered LDS ring in 32 or 64 KB chunks with direct global->LDS loads.
+// The loads of chunk i+1 are interleaved with the fragment reads of chunk i, and the reads
+// are software-pipelined in program order (a ring of fragments in flight ahead of the MFMAs).
+// Every fragment read from LDS feeds 2-3 MFMAs of each wavefront (one per 16-token block the
+// wavefront owns). Activations (X, Y, Q/K/V) are streamed with non-temporal accesses.
 #include "common.h"
 #include "kernels.h"
 
 #include <type_traits>
+#include <utility>
 
 namespace {
 
@@ -53,8 +56,24 @@ struct Shape {
     static_assert(RT * KS % CHUNK == 0 && (3 * D / 16) * KS % CHUNK == 0, "whole chunks");
 };
 
+#ifndef TOK_NT
+#define TOK_NT 1
+#endif
+// Activations are read and written once per launch; with TOK_NT their loads and stores are
+// non-temporal so they do not push the weight stream out of the L2 cache.
+template <typename T>
+PWD_DEV T ld_stream(const T* p) {
+    if constexpr (TOK_NT) return __builtin_nontemporal_load(p);
+    else return *p;
+}
+template <typename T>
+PWD_DEV void st_stream(T* p, T v) {
+    if constexpr (TOK_NT) __builtin_nontemporal_store(v, p);
+    else *p = v;
+}
+
 PWD_DEV bf16x8 ldfrag(const uint16_t* __restrict__ base, int64_t frag, int lane) {
-    const u16x8 v = *reinterpret_cast<const u16x8*>(base + (frag * 64 + lane) * 8);
+    const u16x8 v = ld_stream(reinterpret_cast<const u16x8*>(base + (frag * 64 + lane) * 8));
     return __builtin_bit_cast(bf16x8, v);
 }
 
@@ -63,7 +82,7 @@ PWD_DEV bf16x8 lds_frag(const uint16_t* buf, int j, int lane) {
 }
 
 PWD_DEV void stfrag(uint16_t* __restrict__ base, int64_t frag, int lane, bf16x8 v) {
-    *reinterpret_cast<u16x8*>(base + (frag * 64 + lane) * 8) = __builtin_bit_cast(u16x8, v);
+    st_stream(reinterpret_cast<u16x8*>(base + (frag * 64 + lane) * 8), __builtin_bit_cast(u16x8, v));
 }
 
 PWD_DEV f32x4 ld4(const float* __restrict__ p) { return *reinterpret_cast<const f32x4*>(p); }
@@ -75,8 +94,71 @@ PWD_DEV f32x4 relu4(f32x4 v) {
     return r;
 }
 
-// Scheduling shape of a chunk: LA LDS reads first, then (MPR MFMAs, 1 LDS read) pairs, then
-// the last MFMAs, so LA fragment reads stay in flight ahead of the matrix core.
+// Spacing, in fragment reads, of the NDMA direct-to-LDS loads spread over a chunk of NREAD
+// reads whose first LA reads are issued up front.
+template <int NREAD, int LA, int NDMA>
+constexpr int dma_spacing() { return NDMA > 1 ? (NREAD - 1 - LA) / (NDMA - 1) : 1; }
+
+// Load j of the next chunk follows fragment read LA + j * SP in program order and in the
+// schedule below.
+template <int NREAD, int LA, int NDMA>
+constexpr int dma_after_read(int r) {
+    constexpr int SP = dma_spacing<NREAD, LA, NDMA>();
+    return (r >= LA && (r - LA) % SP == 0 && (r - LA) / SP < NDMA) ? (r - LA) / SP : -1;
+}
+
+template <int MPR, int LA, int SP, int NDMA, int... K>
+PWD_DEV void sched_pairs(std::integer_sequence<int, K...>) {
+    auto pair = [](auto k) {
+        constexpr int kk = decltype(k)::value;
+        __builtin_amdgcn_sched_group_barrier(0x008, MPR, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        if constexpr (kk % SP == 0 && kk / SP < NDMA) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    };
+    (pair(std::integral_constant<int, K>{}), ...);
+}
+
+// Look-ahead of the fragment reads (fragments in flight ahead of the MFMAs that use them).
+#ifndef TOK_LA_WO
+#define TOK_LA_WO 6
+#endif
+#ifndef TOK_LA_MLP
+#define TOK_LA_MLP 6
+#endif
+#ifndef TOK_LA_QKV
+#define TOK_LA_QKV 6
+#endif
+// Spacing, in fragment reads, of the next chunk's loads (0: spread over the whole chunk).
+#ifndef TOK_DMA_SP
+#define TOK_DMA_SP 2
+#endif
+
+// The fragment reads of one chunk, software-pipelined in program order: LA reads are in
+// flight ahead of the MFMAs; read r + LA is issued right after the MFMAs that consume read
+// r. read(r) loads fragment r of the chunk, use(r, a) issues the MFMAs of fragment r, and
+// after(r) runs right after read r is issued. Every loop is fully unrolled, so the ring
+// indices are compile-time constants and the ring lives in registers.
+template <int NREAD, int LA, typename Read, typename Use, typename After>
+PWD_DEV void pipelined(const Read& read, const Use& use, const After& after) {
+    static_assert(LA >= 1 && LA <= NREAD, "look-ahead");
+    bf16x8 ring[LA];
+#pragma unroll
+    for (int r = 0; r < LA; ++r) {
+        ring[r] = read(r);
+        after(r);
+    }
+#pragma unroll
+    for (int r = 0; r < NREAD; ++r) {
+        use(r, ring[r % LA]);
+        if (r + LA < NREAD) {
+            ring[r % LA] = read(r + LA);
+            after(r + LA);
+        }
+    }
+}
+
+// Keeps the scheduler on the program order above: LA reads, then (MPR MFMAs, one read)
+// pairs, then the MFMAs of the last LA fragments.
 template <int NREAD, int MPR, int LA>
 PWD_DEV void sched_pipeline() {
     __builtin_amdgcn_sched_group_barrier(0x100, LA, 0);
@@ -97,48 +179,82 @@ PWD_DEV uint16_t* wbuf() {
     return buf;
 }
 
+// A wavefront-uniform pointer, pinned to scalar registers.
+PWD_DEV const uint16_t* uniform_ptr(const uint16_t* p) {
+    const uint64_t v = reinterpret_cast<uint64_t>(p);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+    return reinterpret_cast<const uint16_t*>(((uint64_t)hi << 32) | lo);
+}
+
 // The weight stream of one launch: `post` chunks first, then `qkv` chunks, pulled through
-// the two LDS buffers (chunk i lives in buffer i % 2). begin<i % 2>(i) makes chunk i visible
-// to every wavefront and starts the load of chunk i+1 into the other buffer.
+// the two LDS buffers (chunk i lives in buffer i % 2). sync<i % 2>(i) makes chunk i visible
+// to every wavefront. While the wavefronts compute on chunk i, the CHUNK / WAVES fragments
+// of chunk i+1 that each wavefront loads go out one at a time between its fragment reads
+// (after_read), rather than in one burst, so LDS reads and direct-to-LDS writes do not queue
+// behind each other. The last chunk reloads itself into the idle buffer so that the loads
+// stay branch-free; the kernel waits for them before it ends.
 template <int CHUNK>
 struct WeightPipe {
+    static constexpr int PER_WAVE = CHUNK / WAVES;
     const uint16_t* post;
     const uint16_t* qkv;
     int n_post, total;
-    int lane, wave;
+    int wave;            // wavefront index, wavefront-uniform
+    uint32_t lane_off;   // this lane's byte offset within a fragment
 
+    __device__ const uint16_t* src(int i) const {
+        return i < n_post ? post + (size_t)i * CHUNK * FRAG : qkv + (size_t)(i - n_post) * CHUNK * FRAG;
+    }
+    // source of the chunk loaded while chunk i is in use
+    __device__ const uint16_t* next(int i) const { return src(i + 1 < total ? i + 1 : i); }
+
+    // One direct global->LDS load: 64 lanes x 16 bytes of fragment f of the chunk at `s`
+    // into fragment slot f of buffer PAR (M0 holds the slot's LDS address). It is inline
+    // assembly because the compiler's wait-count pass treats a pending direct-to-LDS load
+    // builtin as outstanding LDS traffic and then waits for every fragment read before each
+    // MFMA. Completion is awaited explicitly (vmcnt(0) in sync() and at kernel end); the
+    // memory clobber keeps each load in program order relative to the fragment reads.
+    template <int PAR>
+    __device__ void part(const uint16_t* s, int j) const {
+        const int f = wave * PER_WAVE + j;
+        const uint16_t* frag = uniform_ptr(s + f * FRAG);
+        const uint32_t lds = (uint32_t)reinterpret_cast<uintptr_t>(
+            (__attribute__((address_space(3))) uint16_t*)(wbuf<PAR, CHUNK>() + f * FRAG));
+        asm volatile("global_load_lds_dwordx4 %0, %1" :: "v"(lane_off), "s"(frag), "{m0}"(lds) : "memory");
+    }
     template <int PAR>
     __device__ void issue(int i) const {
-        const uint16_t* src = i < n_post ? post + (size_t)i * CHUNK * FRAG
-                                         : qkv + (size_t)(i - n_post) * CHUNK * FRAG;
-        uint16_t* dst = wbuf<PAR, CHUNK>();
 #pragma unroll
-        for (int j = 0; j < CHUNK / WAVES; ++j) {
-            const int f = wave * (CHUNK / WAVES) + j;
-            __builtin_amdgcn_global_load_lds(
-                (const __attribute__((address_space(1))) void*)(src + (f * 64 + lane) * 8),
-                (__attribute__((address_space(3))) void*)(dst + f * FRAG), 16, 0, 0);
-        }
+        for (int j = 0; j < PER_WAVE; ++j) part<PAR>(src(i), j);
     }
-    // Chunk i is visible to every wavefront after sync(i); prefetch(i) then starts chunk
-    // i+1. LDS reads of other tables belong between the two: no prefetch is in flight then,
-    // so the compiler has nothing to wait for.
-    template <int PAR>
+    // Runs after fragment read r of a chunk of NREAD reads pipelined with look-ahead LA: the
+    // PER_WAVE loads of the next chunk follow reads LA, LA + SP, LA + 2 SP, ...
+    template <int NREAD, int LA>
+    static constexpr int spacing() {
+        constexpr int SP_MAX = PER_WAVE > 1 ? (NREAD - 1 - LA) / (PER_WAVE - 1) : 1;
+        return TOK_DMA_SP > 0 && TOK_DMA_SP < SP_MAX ? TOK_DMA_SP : SP_MAX;
+    }
+    // Read index after which the last load of the next chunk is issued.
+    template <int NREAD, int LA>
+    static constexpr int last_load_read() { return LA + spacing<NREAD, LA>() * (PER_WAVE - 1); }
+
+    template <int PAR, int NREAD, int LA>
+    __device__ void after_read(const uint16_t* s, int r) const {
+        constexpr int SP = spacing<NREAD, LA>();
+        static_assert(SP >= 1, "loads fit in the chunk");
+        if (r >= LA && (r - LA) % SP == 0 && (r - LA) / SP < PER_WAVE) part<PAR>(s, (r - LA) / SP);
+    }
+    // Chunk i becomes visible to every wavefront. Vector memory operations retire in issue
+    // order, so this wavefront's loads of chunk i have landed once at most YOUNGER of its
+    // vector memory operations are outstanding: YOUNGER counts what it issued after its last
+    // load of chunk i (global stores), which therefore need not complete here.
+    template <int PAR, int YOUNGER>
     __device__ const uint16_t* sync(int) const {
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's part of chunk i landed
-        __syncthreads();                                   // ... and everyone's; buffer i-1 is free
+        static_assert(YOUNGER >= 0 && YOUNGER < 64, "vmcnt range");
+        asm volatile("s_waitcnt vmcnt(%0)" :: "n"(YOUNGER) : "memory");
+        __syncthreads();                                   // everyone's part landed; buffer i-1 is free
         return wbuf<PAR, CHUNK>();
-    }
-    template <int PAR>
-    __device__ void prefetch(int i) const {
-        if (i + 1 < total) issue<1 - PAR>(i + 1);
-        __builtin_amdgcn_sched_barrier(0);                 // keep the prefetch ahead of the MFMAs
-    }
-    template <int PAR>
-    __device__ const uint16_t* begin(int i) const {
-        const uint16_t* b = sync<PAR>(i);
-        prefetch<PAR>(i);
-        return b;
     }
 };
 
@@ -183,6 +299,18 @@ struct Vecs {
     static constexpr int B1 = 6 * D, BQKV = 10 * D, SIZE = 13 * D;
 };
 
+// Global stores a wavefront issues in one Q/K/V chunk after its last load of the next
+// chunk. Output group o2 is stored in the MFMA step of its last fragment read,
+// r = (o2 + 1) * 2 KS - 1, which follows the loads issued after reads up to r + LA - 1.
+template <int CHUNK, int KS, int TB, int LA>
+constexpr int qkv_stores_after_last_load() {
+    constexpr int LAST = WeightPipe<CHUNK>::template last_load_read<CHUNK, LA>();
+    int n = 0;
+    for (int o2 = 0; o2 < CHUNK / (2 * KS); ++o2)
+        if ((o2 + 1) * 2 * KS - 1 + LA - 1 >= LAST) n += TB;
+    return n;
+}
+
 template <int D, int FLAGS>
 __global__ __launch_bounds__(WAVES * 64, 1) void tok_kernel(TokParams p) {
     constexpr int TB = tok_tb<D, FLAGS>();
@@ -202,53 +330,71 @@ __global__ __launch_bounds__(WAVES * 64, 1) void tok_kernel(TokParams p) {
     pipe.qkv = p.qkv_stream;
     pipe.n_post = POST ? S::POST_CHUNKS : 0;
     pipe.total = pipe.n_post + (QKV ? S::QKV_CHUNKS : 0);
-    pipe.lane = lane;
-    pipe.wave = wave;
+    pipe.wave = __builtin_amdgcn_readfirstlane(wave);
+    pipe.lane_off = (uint32_t)lane * 16;
+
+    // The activations come from HBM and are issued first, so their latency overlaps that of
+    // the first weight chunk and of the vector staging below (all of it is awaited at the
+    // first chunk's sync).
+    f32x4 x[RT][TB];
+    bf16x8 y[POST ? KS : 1][TB];
+    if constexpr (POST) {
+#pragma unroll
+        for (int b = 0; b < TB; ++b)
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) y[ks][b] = ldfrag(p.Y, (tb0 + b) * KS + ks, lane);
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+            for (int b = 0; b < TB; ++b)
+                x[rt][b] = ld_stream(reinterpret_cast<const f32x4*>(p.X + (((tb0 + b) * RT + rt) * 64 + lane) * 4));
+    }
     pipe.template issue<0>(0);
 
+    // Per-launch vectors, staged in LDS by direct loads of 256 bytes (64 lanes x 4 bytes):
+    // vec[0, 10 D) from the POST layer's vector table, vec[10 D, 13 D) the Q/K/V biases. The
+    // first chunk's sync awaits and publishes them.
     __shared__ __align__(16) float vec[V::SIZE];
-    if (POST) {
-        const float* src[7] = {p.bo, p.g1, p.be1, p.b2, p.g2, p.be2, p.b1};
-        for (int k = 0; k < 6; ++k)
-            for (int i = threadIdx.x; i < D; i += WAVES * 64) vec[k * D + i] = src[k][i];
-        for (int i = threadIdx.x; i < 4 * D; i += WAVES * 64) vec[V::B1 + i] = src[6][i];
+    {
+        constexpr int NP_V = POST ? V::BQKV / 64 : 0, NQ_V = QKV ? 3 * D / 64 : 0;
+        static_assert(V::BQKV % 64 == 0 && (3 * D) % 64 == 0, "whole 256-byte pieces");
+        for (int k = pipe.wave; k < NP_V + NQ_V; k += WAVES) {
+            const float* src = k < NP_V ? p.post_vecs + k * 64 : p.bqkv + (k - NP_V) * 64;
+            const int dst = k < NP_V ? k * 64 : V::BQKV + (k - NP_V) * 64;
+            const uint32_t lds = (uint32_t)reinterpret_cast<uintptr_t>(
+                (__attribute__((address_space(3))) float*)(vec + dst));
+            asm volatile("global_load_lds_dword %0, %1" :: "v"((uint32_t)lane * 4),
+                         "s"(reinterpret_cast<const float*>(uniform_ptr(reinterpret_cast<const uint16_t*>(src)))),
+                         "{m0}"(lds) : "memory");
+        }
     }
-    if (QKV)
-        for (int i = threadIdx.x; i < 3 * D; i += WAVES * 64) vec[V::BQKV + i] = p.bqkv[i];
-    // (the first pipe.begin's barrier publishes vec)
-
-    f32x4 x[RT][TB];
 
     if constexpr (POST) {
         // ---- out-projection + residual + LayerNorm 1; accumulators start at X (+ b_o below)
         {
-            bf16x8 y[KS][TB];
+            constexpr int LA = TOK_LA_WO;
+            auto wo_chunk = [&](auto par, int c) {
+                constexpr int PAR = decltype(par)::value;
+                const uint16_t* buf = pipe.template sync<PAR, 0>(c);
+                const uint16_t* nx = pipe.next(c);
+                pipelined<CHUNK, LA>(
+                    [&](int r) { return lds_frag(buf, r, lane); },
+                    [&](int r, const bf16x8& a) {
+                        const int fr = c * CHUNK + r, rt = fr / KS, ks = fr % KS;
 #pragma unroll
-            for (int b = 0; b < TB; ++b)
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks) y[ks][b] = ldfrag(p.Y, (tb0 + b) * KS + ks, lane);
-#pragma unroll
-            for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-                for (int b = 0; b < TB; ++b) x[rt][b] = ld4(p.X + (((tb0 + b) * RT + rt) * 64 + lane) * 4);
-            auto wo_chunk = [&](const uint16_t* buf, int c) {
-#pragma unroll
-                for (int j = 0; j < CHUNK; ++j) {
-                    const int fr = c * CHUNK + j, rt = fr / KS, ks = fr % KS;
-                    const bf16x8 a = lds_frag(buf, j, lane);
-#pragma unroll
-                    for (int b = 0; b < TB; ++b) x[rt][b] = mfma16x16x32(a, y[ks][b], x[rt][b]);
-                }
-                sched_pipeline<CHUNK, TB, 4>();
+                        for (int b = 0; b < TB; ++b) x[rt][b] = mfma16x16x32(a, y[ks][b], x[rt][b]);
+                    },
+                    [&](int r) { pipe.template after_read<1 - PAR, CHUNK, LA>(nx, r); });
+                sched_pipeline<CHUNK, TB, LA>();
             };
             static_assert(S::WO_CHUNKS == 1 || S::WO_CHUNKS % 2 == 0, "Wo chunks");
             if constexpr (S::WO_CHUNKS == 1) {
-                wo_chunk(pipe.template begin<0>(0), 0);
+                wo_chunk(std::integral_constant<int, 0>{}, 0);
             } else {
 #pragma unroll
                 for (int c = 0; c < S::WO_CHUNKS; c += 2) {
-                    wo_chunk(pipe.template begin<0>(c), c);
-                    wo_chunk(pipe.template begin<1>(c + 1), c + 1);
+                    wo_chunk(std::integral_constant<int, 0>{}, c);
+                    wo_chunk(std::integral_constant<int, 1>{}, c + 1);
                 }
             }
         }
@@ -272,50 +418,51 @@ __global__ __launch_bounds__(WAVES * 64, 1) void tok_kernel(TokParams p) {
 #pragma unroll
             for (int b = 0; b < TB; ++b) x[rt][b] += bias;
         }
-        auto mlp_sub = [&](const uint16_t* buf, const f32x4 (&bias)[CH / 16]) {
-            f32x4 h[CH / 16][TB];
-#pragma unroll
-            for (int rh = 0; rh < CH / 16; ++rh)
-#pragma unroll
-                for (int b = 0; b < TB; ++b) h[rh][b] = bias[rh];
-#pragma unroll
-            for (int rh = 0; rh < CH / 16; ++rh)
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks) {
-                    const bf16x8 a = lds_frag(buf, rh * KS + ks, lane);
-#pragma unroll
-                    for (int b = 0; b < TB; ++b) h[rh][b] = mfma16x16x32(a, xb[ks][b], h[rh][b]);
-                }
-            bf16x8 hb[CH / 32][TB];
-#pragma unroll
-            for (int kh = 0; kh < CH / 32; ++kh)
-#pragma unroll
-                for (int b = 0; b < TB; ++b) hb[kh][b] = pack_b(relu4(h[2 * kh][b]), relu4(h[2 * kh + 1][b]));
-            const uint16_t* w2 = buf + (CH / 16) * KS * FRAG;
-#pragma unroll
-            for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-                for (int kh = 0; kh < CH / 32; ++kh) {
-                    const bf16x8 a = lds_frag(w2, rt * (CH / 32) + kh, lane);
-#pragma unroll
-                    for (int b = 0; b < TB; ++b) x[rt][b] = mfma16x16x32(a, hb[kh][b], x[rt][b]);
-                }
-        };
+        // One LDS chunk holds MP feed-forward sub-chunks of CH hidden units, each 32 fragments:
+        // (CH / 16) * KS fragments of W1 (hidden = W1^T x), then RT * (CH / 32) of W2
+        // (x += W2^T relu(hidden)).
         constexpr int MP = S::MLP_PER;
+        constexpr int LA = TOK_LA_MLP;
+        constexpr int NW1 = (CH / 16) * KS;
         auto mlp_chunk = [&](auto par, int c) {
             constexpr int PAR = decltype(par)::value;
             const int ci = S::WO_CHUNKS + c;
-            const uint16_t* buf = pipe.template sync<PAR>(ci);
-            f32x4 bias[MP][CH / 16];
+            const uint16_t* buf = pipe.template sync<PAR, 0>(ci);
+            f32x4 h[MP][CH / 16][TB];
 #pragma unroll
             for (int u = 0; u < MP; ++u)
 #pragma unroll
-                for (int rh = 0; rh < CH / 16; ++rh)
-                    bias[u][rh] = ld4(vec + V::B1 + (c * MP + u) * CH + rh * 16 + 4 * g);
-            pipe.template prefetch<PAR>(ci);
+                for (int rh = 0; rh < CH / 16; ++rh) {
+                    const f32x4 bias = ld4(vec + V::B1 + (c * MP + u) * CH + rh * 16 + 4 * g);
 #pragma unroll
-            for (int u = 0; u < MP; ++u) mlp_sub(buf + u * 32 * FRAG, bias[u]);
-            sched_pipeline<MP * (CH / 16 + 32), TB, 6>();
+                    for (int b = 0; b < TB; ++b) h[u][rh][b] = bias;
+                }
+            const uint16_t* nx = pipe.next(ci);
+            __builtin_amdgcn_sched_barrier(0);
+            bf16x8 hb[MP][CH / 32][TB];
+            pipelined<MP * 32, LA>(
+                [&](int r) { return lds_frag(buf, r, lane); },
+                [&](int r, const bf16x8& a) {
+                    const int u = r / 32, k = r % 32;
+                    if (k < NW1) {
+                        const int rh = k / KS, ks = k % KS;
+#pragma unroll
+                        for (int b = 0; b < TB; ++b) h[u][rh][b] = mfma16x16x32(a, xb[ks][b], h[u][rh][b]);
+                        if (k == NW1 - 1) {
+#pragma unroll
+                            for (int kh = 0; kh < CH / 32; ++kh)
+#pragma unroll
+                                for (int b = 0; b < TB; ++b)
+                                    hb[u][kh][b] = pack_b(relu4(h[u][2 * kh][b]), relu4(h[u][2 * kh + 1][b]));
+                        }
+                    } else {
+                        const int rt = (k - NW1) / (CH / 32), kh = (k - NW1) % (CH / 32);
+#pragma unroll
+                        for (int b = 0; b < TB; ++b) x[rt][b] = mfma16x16x32(a, hb[u][kh][b], x[rt][b]);
+                    }
+                },
+                [&](int r) { pipe.template after_read<1 - PAR, MP * 32, LA>(nx, r); });
+            sched_pipeline<MP * 32, TB, LA>();
         };
         static_assert(S::MLP_CHUNKS % 2 == 0, "feed-forward chunks come in pairs");
         constexpr int P0 = S::WO_CHUNKS & 1;
@@ -361,7 +508,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void tok_kernel(TokParams p) {
         for (int b = 0; b < TB; ++b)
 #pragma unroll
             for (int rt = 0; rt < RT; ++rt)
-                *reinterpret_cast<f32x4*>(p.X + (((tb0 + b) * RT + rt) * 64 + lane) * 4) = x[rt][b];
+                st_stream(reinterpret_cast<f32x4*>(p.X + (((tb0 + b) * RT + rt) * 64 + lane) * 4), x[rt][b]);
     };
 
     store_x();
@@ -374,50 +521,60 @@ __global__ __launch_bounds__(WAVES * 64, 1) void tok_kernel(TokParams p) {
         // 3D output features in groups of 32 (= one B fragment of Q, K or V)
         constexpr int NP = POST ? S::POST_CHUNKS : 0;
         constexpr int OPC = S::OG_PER_CHUNK;
-        auto qkv_chunk = [&](auto par, int qc) {
+        constexpr int LA = TOK_LA_QKV;
+        constexpr int STORES_AFTER = qkv_stores_after_last_load<CHUNK, KS, TB, LA>();
+        auto qkv_chunk = [&](auto par, auto first, int qc) {
             constexpr int PAR = decltype(par)::value;
-            const uint16_t* buf = pipe.template sync<PAR>(NP + qc);
-            f32x4 bias[OPC][2];
+            // before the first QKV chunk, the residual stream store (RT * TB stores) follows
+            // the last load of this chunk
+            constexpr int YOUNGER = decltype(first)::value ? RT * TB : STORES_AFTER;
+            const uint16_t* buf = pipe.template sync<PAR, YOUNGER>(NP + qc);
+            // fragment r = (o2 * KS + ks) * 2 + hh: rows 16 hh .. 16 hh + 15 of output group
+            // qc * OPC + o2, k-step ks
+            f32x4 q[OPC][2][TB];
 #pragma unroll
             for (int o2 = 0; o2 < OPC; ++o2)
 #pragma unroll
-                for (int hh = 0; hh < 2; ++hh)
-                    bias[o2][hh] = ld4(vec + V::BQKV + (qc * OPC + o2) * 32 + hh * 16 + 4 * g);
-            pipe.template prefetch<PAR>(NP + qc);
+                for (int hh = 0; hh < 2; ++hh) {
+                    const f32x4 bias = ld4(vec + V::BQKV + (qc * OPC + o2) * 32 + hh * 16 + 4 * g);
 #pragma unroll
-            for (int o2 = 0; o2 < OPC; ++o2) {
-                const int og = qc * OPC + o2;
-                f32x4 q0[TB], q1[TB];
-#pragma unroll
-                for (int b = 0; b < TB; ++b) {
-                    q0[b] = bias[o2][0];
-                    q1[b] = bias[o2][1];
+                    for (int b = 0; b < TB; ++b) q[o2][hh][b] = bias;
                 }
+            const uint16_t* nx = pipe.next(NP + qc);
+            __builtin_amdgcn_sched_barrier(0);
+            pipelined<CHUNK, LA>(
+                [&](int r) { return lds_frag(buf, r, lane); },
+                [&](int r, const bf16x8& a) {
+                    const int hh = r & 1, ks = (r >> 1) % KS, o2 = (r >> 1) / KS;
 #pragma unroll
-                for (int ks = 0; ks < KS; ++ks) {
-                    const bf16x8 a0 = lds_frag(buf, (o2 * KS + ks) * 2, lane);
-                    const bf16x8 a1 = lds_frag(buf, (o2 * KS + ks) * 2 + 1, lane);
+                    for (int b = 0; b < TB; ++b) q[o2][hh][b] = mfma16x16x32(a, xb[ks][b], q[o2][hh][b]);
+                    if (hh == 1 && ks == KS - 1) {
+                        const int og = qc * OPC + o2;
+                        const float sc = og < KS ? p.qscale : 1.0f;   // Q: log2(e)/sqrt(dh)
 #pragma unroll
-                    for (int b = 0; b < TB; ++b) {
-                        q0[b] = mfma16x16x32(a0, xb[ks][b], q0[b]);
-                        q1[b] = mfma16x16x32(a1, xb[ks][b], q1[b]);
+                        for (int b = 0; b < TB; ++b)
+                            stfrag(p.QKV, (tb0 + b) * (3 * KS) + og, lane,
+                                   pack_b(q[o2][0][b] * sc, q[o2][1][b] * sc));
                     }
-                }
-                const float sc = og < KS ? p.qscale : 1.0f;   // Q: log2(e)/sqrt(dh)
-#pragma unroll
-                for (int b = 0; b < TB; ++b)
-                    stfrag(p.QKV, (tb0 + b) * (3 * KS) + og, lane, pack_b(q0[b] * sc, q1[b] * sc));
-            }
-            sched_pipeline<CHUNK, TB, 6>();
+                },
+                [&](int r) { pipe.template after_read<1 - PAR, CHUNK, LA>(nx, r); });
+            sched_pipeline<CHUNK, TB, LA>();
         };
         constexpr int Q0 = NP & 1;
-        int qc = 0;
+        using first = std::true_type;
+        using later = std::false_type;
+        qkv_chunk(std::integral_constant<int, Q0>{}, first{}, 0);
+        int qc = 1;
         for (; qc + 1 < S::QKV_CHUNKS; qc += 2) {
-            qkv_chunk(std::integral_constant<int, Q0>{}, qc);
-            qkv_chunk(std::integral_constant<int, 1 - Q0>{}, qc + 1);
+            qkv_chunk(std::integral_constant<int, 1 - Q0>{}, later{}, qc);
+            qkv_chunk(std::integral_constant<int, Q0>{}, later{}, qc + 1);
         }
-        if constexpr (S::QKV_CHUNKS % 2 == 1) qkv_chunk(std::integral_constant<int, Q0>{}, qc);
+        if constexpr (S::QKV_CHUNKS % 2 == 0) qkv_chunk(std::integral_constant<int, 1 - Q0>{}, later{}, qc);
     }
+    // The last chunk's reload into the idle buffer must land before the workgroup's LDS is
+    // freed; the global stores issued after it need not.
+    constexpr int END_YOUNGER = QKV ? qkv_stores_after_last_load<CHUNK, KS, TB, TOK_LA_QKV>() : RT * TB;
+    asm volatile("s_waitcnt vmcnt(%0)" :: "n"(END_YOUNGER) : "memory");
 }
 
 template <int D, int FLAGS>
