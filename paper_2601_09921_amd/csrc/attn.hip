@@ -6,14 +6,16 @@
 // blocks and streams the keys in steps of 32:
 //   S^T = K Q'^T - m      (16 keys x 16 queries per MFMA, lanes hold queries)
 //   P^T = exp2(S^T)       (P^T is the S^T accumulator rounded to bf16, no shuffle)
-//   O^T += V^T P^T,  l += sum P
+//   O^T += V^T P^T,  l += 1^T P^T
 // Q' = Q log2(e)/sqrt(dh) comes pre-scaled from the Q/K/V projection, so S is in log2 units.
 // The shift m of a query is the Cauchy-Schwarz bound |q'| max_k |k| >= every score of the
 // row; softmax is shift-invariant, so this is the exact softmax without a running maximum
 // or rescaling, and m enters as the initial value of the MFMA accumulator. Should a row's
 // sum underflow (a bound far above the true maximum), that query block is recomputed with
-// the running-maximum form. Padding keys (index >= N) get probability 0. The output is
-// written as the B fragments the out-projection consumes.
+// the running-maximum form. Padding keys (index >= N) get probability 0. The row sums l come
+// from the matrix core too: an A fragment whose row 0 is all ones turns P^T into its column
+// sums, so numerator and denominator use the same bf16 probabilities and the VALU is left to
+// the exponentials. The output is written as the B fragments the out-projection consumes.
 #include "common.h"
 #include "kernels.h"
 
@@ -146,6 +148,10 @@ __global__ __launch_bounds__(WAVES * 64) void attn_kernel(AttnParams p) {
     kmax = sqrtf(kmax);
 
     const int nsb = (nbw + 1) / 2;
+    // A fragment with row 0 all ones (lanes 0-15 hold row 0's k values)
+    bf16x8 ones;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) ones[i] = (__bf16)(col == 0 ? 1.0f : 0.0f);
     auto load_q = [&](int qb0, u16x8 (&qv)[QB]) {
 #pragma unroll
         for (int j = 0; j < QB; ++j) {
@@ -178,25 +184,34 @@ __global__ __launch_bounds__(WAVES * 64) void attn_kernel(AttnParams p) {
         }
 
         f32x4 o[QB][RT];
-        float l[QB];
+        f32x4 ls[QB];     // row 0 (lanes 0-15, element 0): sum of P over the keys
 #pragma unroll
         for (int j = 0; j < QB; ++j) {
-            l[j] = 0.f;
+            ls[j] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int rt = 0; rt < RT; ++rt) o[j][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
         }
 
-        // S^T of a full superblock sb (two 16-key blocks, no padding keys) for every query block
-        auto scores_full = [&](int sb, f32x4 (&s)[QB][2]) {
+        // K and V^T fragments of superblock sb (two 16-key blocks). Indices up to nsb - 1
+        // stay inside the LDS image (a missing last key block reads the start of V^T), so the
+        // prefetches below never need a bounds branch; such values are never used.
+        auto load_k = [&](int sb, FT (&kf)[2]) {
 #pragma unroll
-            for (int kk = 0; kk < 2; ++kk) {
-                const FT a = ld_kfrag<DH>(ks, 2 * sb + kk, lane);
-#pragma unroll
-                for (int j = 0; j < QB; ++j) s[j][kk] = Frag<DH>::mma(a, q[j], shift[j]);
-            }
+            for (int kk = 0; kk < 2; ++kk) kf[kk] = ld_kfrag<DH>(ks, 2 * sb + kk, lane);
         };
-        // P = exp2(S), row sums, and O^T += V^T P^T for superblock sb
-        auto accumulate = [&](int sb, const f32x4 (&s)[QB][2]) {
+        auto load_v = [&](int sb, bf16x8 (&vf)[RT]) {
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) vf[rt] = ld_vfrag(vt, vts, rt, sb, col, g);
+        };
+        // S^T - m of one superblock for every query block
+        auto scores = [&](const FT (&kf)[2], f32x4 (&s)[QB][2]) {
+#pragma unroll
+            for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+                for (int j = 0; j < QB; ++j) s[j][kk] = Frag<DH>::mma(kf[kk], q[j], shift[j]);
+        };
+        // P = exp2(S), row sums, and O^T += V^T P^T for one superblock
+        auto accumulate = [&](const f32x4 (&s)[QB][2], const bf16x8 (&vf)[RT]) {
             bf16x8 pb[QB];
 #pragma unroll
             for (int j = 0; j < QB; ++j) {
@@ -205,29 +220,38 @@ __global__ __launch_bounds__(WAVES * 64) void attn_kernel(AttnParams p) {
                 for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
                     for (int i = 0; i < 4; ++i) pr[kk][i] = exp2_fast(s[j][kk][i]);
-                l[j] += ((pr[0][0] + pr[0][1]) + (pr[0][2] + pr[0][3])) + ((pr[1][0] + pr[1][1]) + (pr[1][2] + pr[1][3]));
                 pb[j] = pack_b(pr[0], pr[1]);
+                ls[j] = mfma16x16x32(ones, pb[j], ls[j]);
             }
 #pragma unroll
-            for (int rt = 0; rt < RT; ++rt) {
-                const bf16x8 v = ld_vfrag(vt, vts, rt, sb, col, g);
+            for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-                for (int j = 0; j < QB; ++j) o[j][rt] = mfma16x16x32(v, pb[j], o[j][rt]);
-            }
+                for (int j = 0; j < QB; ++j) o[j][rt] = mfma16x16x32(vf[rt], pb[j], o[j][rt]);
         };
-        // Every superblock but the last is full; the loop is software-pipelined (the score
-        // MFMAs of sb+1 are issued before the exponentials of sb) and unrolled by two.
-        f32x4 sa[QB][2], sbuf[QB][2];
+        // Every superblock but the last is full. Software pipeline over them, unrolled by two:
+        // while the exponentials of sb run, the scores of sb+1 are on the matrix core, K of
+        // sb+2 and V of sb+1 are in flight from LDS.
         const int nfull = nsb - 1;
-        if (nfull > 0) scores_full(0, sa);
+        const int lastsb = nsb - 1;
+        FT kA[2], kB[2];
+        bf16x8 vA[RT], vB[RT];
+        f32x4 sA[QB][2], sB[QB][2];
+        load_k(0, kA);
+        load_v(0, vA);
+        load_k(min(1, lastsb), kB);
+        scores(kA, sA);
         int sb = 0;
         for (; sb + 2 <= nfull; sb += 2) {
-            scores_full(sb + 1, sbuf);
-            accumulate(sb, sa);
-            if (sb + 2 < nfull) scores_full(sb + 2, sa);
-            accumulate(sb + 1, sbuf);
+            scores(kB, sB);                              // sb + 1
+            load_k(min(sb + 2, lastsb), kA);
+            load_v(sb + 1, vB);
+            accumulate(sA, vA);                          // sb
+            scores(kA, sA);                              // sb + 2 (unused past nfull)
+            load_k(min(sb + 3, lastsb), kB);
+            load_v(min(sb + 2, lastsb), vA);
+            accumulate(sB, vB);                          // sb + 1
         }
-        if (sb < nfull) accumulate(sb, sa);
+        if (sb < nfull) accumulate(sA, vA);
         {   // last superblock: missing key block and padding keys are -inf
             const int last = nsb - 1;
             f32x4 s[QB][2];
@@ -248,13 +272,15 @@ __global__ __launch_bounds__(WAVES * 64) void attn_kernel(AttnParams p) {
 #pragma unroll
                         for (int j = 0; j < QB; ++j) s[j][kk][i] = -INFINITY;
             }
-            accumulate(last, s);
+            bf16x8 vl[RT];
+            load_v(last, vl);
+            accumulate(s, vl);
         }
 
 #pragma unroll
         for (int j = 0; j < QB; ++j) {
             const int qb = qb0 + j;
-            float lt = sum4(l[j]);
+            float lt = __shfl(ls[j][0], col);   // row 0 of the sums lives in lane col
             // underflowed row sums: redo this block with a running maximum (wave-uniform)
             if (__builtin_amdgcn_ballot_w64(lt < 1e-30f) != 0) {
                 float mm = -INFINITY, ll = 0.f;
