@@ -2,8 +2,8 @@
 // model table's Multi-Head Attention), bf16 MFMA with fp32 softmax statistics.
 //
 // One workgroup per (window, head), of 1, 2 or 4 wavefronts by window size. K_h (as MFMA A
-// fragments) and V_h^T are staged in LDS once; each wavefront then takes pairs of 16-query
-// blocks and streams the keys in steps of 32:
+// fragments) and V_h^T are staged in LDS once; each wavefront then takes its quarter of the
+// 16-query blocks, four (the last pass two) at a time, and streams the keys in steps of 32:
 //   S^T = K Q'^T - m      (16 keys x 16 queries per MFMA, lanes hold queries)
 //   P^T = exp2(S^T)       (P^T is the S^T accumulator rounded to bf16, no shuffle)
 //   O^T += V^T P^T,  l += 1^T P^T
@@ -21,7 +21,10 @@
 
 namespace {
 
-constexpr int QB = 2;                 // query blocks per wavefront pass
+#ifndef ATTN_QMAX
+#define ATTN_QMAX 4
+#endif
+constexpr int QMAX = ATTN_QMAX;       // query blocks per wavefront pass (the last takes QMAX / 2)
 constexpr int SBATCH = 10;            // key blocks per wavefront per staging batch (d=25: one batch)
 
 __host__ __device__ inline int vt_stride(int Npad) { return ((Npad + 31) & ~31) + 8; }   // + 8: spread banks
@@ -152,21 +155,27 @@ __global__ __launch_bounds__(WAVES * 64) void attn_kernel(AttnParams p) {
     bf16x8 ones;
 #pragma unroll
     for (int i = 0; i < 8; ++i) ones[i] = (__bf16)(col == 0 ? 1.0f : 0.0f);
-    auto load_q = [&](int qb0, u16x8 (&qv)[QB]) {
+    // Each wavefront owns a contiguous quarter of the window's query blocks and walks it in
+    // passes of QMAX blocks, the last pass with QMAX / 2 (a lone leftover block computes a
+    // duplicate that is not stored). Q of the next pass is loaded during the current one.
+    const int qend = (wave + 1) * nbw / WAVES;
+    auto load_q = [&](int qb0, u16x8 (&qv)[QMAX]) {
 #pragma unroll
-        for (int j = 0; j < QB; ++j) {
-            const int qb = min(qb0 + j, nbw - 1);    // a lone last block computes a duplicate
+        for (int j = 0; j < QMAX; ++j) {
+            const int qb = min(qb0 + j, qend - 1);
             qv[j] = *reinterpret_cast<const u16x8*>(
                 p.QKV + (((tb_base + qb) * 3 + 0) * KSD + frag) * 512 + lane * 8);
         }
     };
-    u16x8 qnext[QB];
-    if (wave * QB < nbw) load_q(wave * QB, qnext);
-    for (int qb0 = wave * QB; qb0 < nbw; qb0 += WAVES * QB) {
+    u16x8 qnext[QMAX];
+    int qbeg = wave * nbw / WAVES;
+    if (qbeg < qend) load_q(qbeg, qnext);
+    auto pass = [&](auto qbc, int qb0) {
+        constexpr int QB = decltype(qbc)::value;
         u16x8 qv[QB];
 #pragma unroll
         for (int j = 0; j < QB; ++j) qv[j] = qnext[j];
-        if (qb0 + WAVES * QB < nbw) load_q(qb0 + WAVES * QB, qnext);   // next pass, in flight
+        if (qb0 + QB < qend) load_q(qb0 + QB, qnext);   // next pass, in flight
         FT q[QB];
         f32x4 shift[QB];
         float m[QB];
@@ -317,7 +326,7 @@ __global__ __launch_bounds__(WAVES * 64) void attn_kernel(AttnParams p) {
                 }
                 lt = sum4(ll);
             }
-            if (qb >= nbw) continue;
+            if (qb >= qend) continue;
             const float inv = 1.0f / lt;
             uint16_t* dst = p.Y + ((tb_base + qb) * KSD + frag) * 512 + lane * 8;
             if constexpr (DH == 32) {
@@ -330,7 +339,10 @@ __global__ __launch_bounds__(WAVES * 64) void attn_kernel(AttnParams p) {
                 *reinterpret_cast<u16x4*>(dst + slot0) = out;
             }
         }
-    }
+    };
+    int qb = qbeg;
+    for (; qend - qb >= QMAX - 1; qb += QMAX) pass(std::integral_constant<int, QMAX>{}, qb);
+    if (qb < qend) pass(std::integral_constant<int, QMAX / 2>{}, qb);
 }
 
 }  // namespace
@@ -351,10 +363,10 @@ hipError_t launch_shape(const AttnParams& p, int nwin, hipStream_t s) {
 
 template <int DH>
 hipError_t launch_dh(const AttnParams& p, int nwin, hipStream_t s) {
-    // wavefronts per (window, head): enough for two query blocks each, at most four, so
-    // small windows run as many small workgroups rather than idle wavefronts
-    if (p.nbw <= 2 * QB) return launch_shape<DH, 1>(p, nwin, s);
-    if (p.nbw <= 4 * QB) return launch_shape<DH, 2>(p, nwin, s);
+    // wavefronts per (window, head): enough for a pass of QMAX query blocks each, at most
+    // four, so small windows run as many small workgroups rather than idle wavefronts
+    if (p.nbw <= QMAX) return launch_shape<DH, 1>(p, nwin, s);
+    if (p.nbw <= 2 * QMAX) return launch_shape<DH, 2>(p, nwin, s);
     return launch_shape<DH, 4>(p, nwin, s);
 }
 
