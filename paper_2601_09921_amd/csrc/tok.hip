@@ -28,18 +28,19 @@
 
 namespace {
 
-constexpr int WAVES = 4;        // wavefronts per workgroup
 constexpr int MAX_CHUNK = 64;   // weight fragments (1 KB each) per LDS chunk, at most
 constexpr int FRAG = 512;       // bf16 values per fragment
 
-// 16-token blocks per wavefront: three where the registers allow it (more tokens per
-// workgroup share each streamed weight chunk), else two.
+// Two 16-token blocks per wavefront, and per workgroup 8 wavefronts (two per SIMD, so one
+// hides the other's latencies; 16 blocks share each streamed weight chunk) where the
+// registers fit 256 per wavefront, else 4 (the variant that also embeds at D = 256).
 template <int D, int FLAGS>
-constexpr int tok_tb() { return (D == 256 && (FLAGS & TOK_EMBED) == 0) ? 3 : 2; }
+constexpr int tok_waves() { return (D == 256 && (FLAGS & TOK_EMBED) == 0) ? 8 : 4; }
+constexpr int TB = 2;
 
-template <int D, int TB>
+template <int D, int NW>
 struct Shape {
-    static constexpr int CHUNK = (D == 256 && TB == 2) ? 64 : 32;  // weight fragments per LDS chunk
+    static constexpr int CHUNK = (D == 256 && NW == 4) ? 64 : 32;  // weight fragments per LDS chunk
     static constexpr int RT = D / 16;                 // 16-row C tiles of a D-vector
     static constexpr int KS = D / 32;                 // 32-deep k-steps of a D-vector
     static constexpr int F = 4 * D;
@@ -189,14 +190,14 @@ PWD_DEV const uint16_t* uniform_ptr(const uint16_t* p) {
 
 // The weight stream of one launch: `post` chunks first, then `qkv` chunks, pulled through
 // the two LDS buffers (chunk i lives in buffer i % 2). sync<i % 2>(i) makes chunk i visible
-// to every wavefront. While the wavefronts compute on chunk i, the CHUNK / WAVES fragments
+// to every wavefront. While the wavefronts compute on chunk i, the CHUNK / NW fragments
 // of chunk i+1 that each wavefront loads go out one at a time between its fragment reads
 // (after_read), rather than in one burst, so LDS reads and direct-to-LDS writes do not queue
 // behind each other. The last chunk reloads itself into the idle buffer so that the loads
 // stay branch-free; the kernel waits for them before it ends.
-template <int CHUNK>
+template <int CHUNK, int NW>
 struct WeightPipe {
-    static constexpr int PER_WAVE = CHUNK / WAVES;
+    static constexpr int PER_WAVE = CHUNK / NW;
     const uint16_t* post;
     const uint16_t* qkv;
     int n_post, total;
@@ -302,9 +303,9 @@ struct Vecs {
 // Global stores a wavefront issues in one Q/K/V chunk after its last load of the next
 // chunk. Output group o2 is stored in the MFMA step of its last fragment read,
 // r = (o2 + 1) * 2 KS - 1, which follows the loads issued after reads up to r + LA - 1.
-template <int CHUNK, int KS, int TB, int LA>
+template <int CHUNK, int NW, int KS, int LA>
 constexpr int qkv_stores_after_last_load() {
-    constexpr int LAST = WeightPipe<CHUNK>::template last_load_read<CHUNK, LA>();
+    constexpr int LAST = WeightPipe<CHUNK, NW>::template last_load_read<CHUNK, LA>();
     int n = 0;
     for (int o2 = 0; o2 < CHUNK / (2 * KS); ++o2)
         if ((o2 + 1) * 2 * KS - 1 + LA - 1 >= LAST) n += TB;
@@ -312,9 +313,14 @@ constexpr int qkv_stores_after_last_load() {
 }
 
 template <int D, int FLAGS>
-__global__ __launch_bounds__(WAVES * 64, 1) void tok_kernel(TokParams p) {
-    constexpr int TB = tok_tb<D, FLAGS>();
-    using S = Shape<D, TB>;
+__global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 1) void tok_kernel(TokParams p) {
+    constexpr int WAVES = tok_waves<D, FLAGS>();
+    using S = Shape<D, WAVES>;
+    // fragment-read look-ahead per phase: with two wavefronts per SIMD a shorter ring suffices
+    // and keeps the kernel within 256 registers
+    constexpr int LA_WO = WAVES == 8 ? 4 : TOK_LA_WO;
+    constexpr int LA_MLP = WAVES == 8 ? 4 : TOK_LA_MLP;
+    constexpr int LA_QKV = WAVES == 8 ? 4 : TOK_LA_QKV;
     using V = Vecs<D>;
     constexpr int RT = S::RT, KS = S::KS, CH = S::CH;
     constexpr bool POST = (FLAGS & TOK_POST) != 0, QKV = (FLAGS & TOK_QKV) != 0;
@@ -325,7 +331,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void tok_kernel(TokParams p) {
     const int64_t tb0 = ((int64_t)blockIdx.x * WAVES + wave) * TB;
 
     constexpr int CHUNK = S::CHUNK;
-    WeightPipe<CHUNK> pipe;
+    WeightPipe<CHUNK, WAVES> pipe;
     pipe.post = p.post_stream;
     pipe.qkv = p.qkv_stream;
     pipe.n_post = POST ? S::POST_CHUNKS : 0;
@@ -372,7 +378,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void tok_kernel(TokParams p) {
     if constexpr (POST) {
         // ---- out-projection + residual + LayerNorm 1; accumulators start at X (+ b_o below)
         {
-            constexpr int LA = TOK_LA_WO;
+            constexpr int LA = LA_WO;
             auto wo_chunk = [&](auto par, int c) {
                 constexpr int PAR = decltype(par)::value;
                 const uint16_t* buf = pipe.template sync<PAR, 0>(c);
@@ -422,7 +428,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void tok_kernel(TokParams p) {
         // (CH / 16) * KS fragments of W1 (hidden = W1^T x), then RT * (CH / 32) of W2
         // (x += W2^T relu(hidden)).
         constexpr int MP = S::MLP_PER;
-        constexpr int LA = TOK_LA_MLP;
+        constexpr int LA = LA_MLP;
         constexpr int NW1 = (CH / 16) * KS;
         auto mlp_chunk = [&](auto par, int c) {
             constexpr int PAR = decltype(par)::value;
@@ -521,8 +527,8 @@ __global__ __launch_bounds__(WAVES * 64, 1) void tok_kernel(TokParams p) {
         // 3D output features in groups of 32 (= one B fragment of Q, K or V)
         constexpr int NP = POST ? S::POST_CHUNKS : 0;
         constexpr int OPC = S::OG_PER_CHUNK;
-        constexpr int LA = TOK_LA_QKV;
-        constexpr int STORES_AFTER = qkv_stores_after_last_load<CHUNK, KS, TB, LA>();
+        constexpr int LA = LA_QKV;
+        constexpr int STORES_AFTER = qkv_stores_after_last_load<CHUNK, WAVES, KS, LA>();
         auto qkv_chunk = [&](auto par, auto first, int qc) {
             constexpr int PAR = decltype(par)::value;
             // before the first QKV chunk, the residual stream store (RT * TB stores) follows
@@ -573,13 +579,14 @@ __global__ __launch_bounds__(WAVES * 64, 1) void tok_kernel(TokParams p) {
     }
     // The last chunk's reload into the idle buffer must land before the workgroup's LDS is
     // freed; the global stores issued after it need not.
-    constexpr int END_YOUNGER = QKV ? qkv_stores_after_last_load<CHUNK, KS, TB, TOK_LA_QKV>() : RT * TB;
+    constexpr int END_YOUNGER = QKV ? qkv_stores_after_last_load<CHUNK, WAVES, KS, LA_QKV>() : RT * TB;
     asm volatile("s_waitcnt vmcnt(%0)" :: "n"(END_YOUNGER) : "memory");
 }
 
 template <int D, int FLAGS>
 void launch_variant(const TokParams& p, int64_t n_tb, hipStream_t s) {
-    const int64_t per_wg = (int64_t)WAVES * tok_tb<D, FLAGS>();
+    constexpr int WAVES = tok_waves<D, FLAGS>();
+    const int64_t per_wg = (int64_t)WAVES * TB;
     const dim3 grid((unsigned)((n_tb + per_wg - 1) / per_wg)), block(WAVES * 64);
     tok_kernel<D, FLAGS><<<grid, block, 0, s>>>(p);
 }
@@ -598,9 +605,9 @@ hipError_t launch_tok_d(int flags, const TokParams& p, int64_t n_tb, hipStream_t
 
 }  // namespace
 
-// Token blocks are processed in groups of WAVES*TB (TB = 2 or 3 by variant); every buffer
+// Token blocks are processed in groups of 8 or 16 (wavefronts x TB by variant); every buffer
 // indexed here must be allocated for n_tb rounded up to a multiple of all of them.
-int64_t tok_block_granule() { return (int64_t)WAVES * 6; }
+int64_t tok_block_granule() { return 48; }
 
 // Fragments of the weight streams (see tok_kernel): hidden units per feed-forward chunk.
 int tok_mlp_chunk(int D) { return 8192 / D; }
