@@ -1,8 +1,11 @@
 // Multi-head self-attention across the stabilizer tokens of each window (App. A.2; the
 // model table's Multi-Head Attention), bf16 MFMA with fp32 softmax statistics.
 //
-// One workgroup per (window, head), of 1, 2 or 4 wavefronts by window size. K_h (as MFMA A
-// fragments) and V_h^T are staged in LDS once; each wavefront then takes its quarter of the
+// One workgroup per (window, head), of 1, 2 or 4 wavefronts by window size. K_h and V_h are
+// copied to LDS once, by direct global->LDS loads of the fragments the Q/K/V projection wrote
+// (K as B fragments of K^T, which serve as A fragments of K; V as 16x16 tiles with tokens as
+// rows, whose per-lane halves of two key blocks form an A fragment of V^T); each wavefront
+// then takes its quarter of the
 // 16-query blocks, four (the last pass two) at a time, and streams the keys in steps of 32:
 //   S^T = K Q'^T - m      (16 keys x 16 queries per MFMA, lanes hold queries)
 //   P^T = exp2(S^T)       (P^T is the S^T accumulator rounded to bf16, no shuffle)
@@ -27,8 +30,6 @@ namespace {
 constexpr int QMAX = ATTN_QMAX;       // query blocks per wavefront pass (the last takes QMAX / 2)
 constexpr int SBATCH = 10;            // key blocks per wavefront per staging batch (d=25: one batch)
 
-__host__ __device__ inline int vt_stride(int Npad) { return ((Npad + 31) & ~31) + 8; }   // + 8: spread banks
-
 PWD_DEV float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
 template <int DH>
@@ -44,19 +45,23 @@ struct Frag<16> {
     static __device__ __forceinline__ f32x4 mma(T a, T b, f32x4 c) { return mfma16x16x16(a, b, c); }
 };
 
+// K fragment of key block kb (LDS holds whole 1 KB fragments; with dh = 16 one fragment
+// carries two heads and slot0 selects this head's four values).
 template <int DH>
-PWD_DEV typename Frag<DH>::T ld_kfrag(const uint16_t* ks, int kb, int lane) {
+PWD_DEV typename Frag<DH>::T ld_kfrag(const uint16_t* ks, int kb, int lane, int slot0) {
     if constexpr (DH == 32)
         return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(ks + (kb * 64 + lane) * 8));
     else
-        return __builtin_bit_cast(bf16x4, *reinterpret_cast<const u16x4*>(ks + (kb * 64 + lane) * 4));
+        return __builtin_bit_cast(bf16x4, *reinterpret_cast<const u16x4*>(ks + (kb * 64 + lane) * 8 + slot0));
 }
 
-// V^T A fragment of row tile rt for the 32 keys of superblock sb (k slots kslot(g, i)).
-PWD_DEV bf16x8 ld_vfrag(const uint16_t* vt, int vts, int rt, int sb, int col, int g) {
-    const uint16_t* row = vt + (rt * 16 + col) * vts + 32 * sb + 4 * g;
-    const u16x4 lo = *reinterpret_cast<const u16x4*>(row);
-    const u16x4 hi = *reinterpret_cast<const u16x4*>(row + 16);
+// V^T A fragment of the 32 keys of superblock sb for dh columns 16 half .. 16 half + 15: this
+// lane's four keys of key block 2 sb (k slots 0-3) and of key block 2 sb + 1 (k slots 4-7),
+// i.e. the lane's 8 bytes of tile half `half` of both V fragments.
+PWD_DEV bf16x8 ld_vfrag(const uint16_t* vs, int half, int sb, int lane) {
+    const uint16_t* t = vs + (2 * sb) * 512 + half * 256 + lane * 4;
+    const u16x4 lo = *reinterpret_cast<const u16x4*>(t);
+    const u16x4 hi = *reinterpret_cast<const u16x4*>(t + 512);
     u16x8 v;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -82,68 +87,43 @@ __global__ __launch_bounds__(WAVES * 64) void attn_kernel(AttnParams p) {
     const int nbw = p.nbw, N = p.N;
     const int KSD = p.H * DH / 32;              // fragments per Q/K/V of a token block
     const int64_t tb_base = (int64_t)win * nbw;
-    const int vts = vt_stride(p.Npad);
-
     extern __shared__ __align__(16) unsigned char smem[];
-    uint16_t* ks = reinterpret_cast<uint16_t*>(smem);
-    uint16_t* vt = ks + (size_t)nbw * 64 * NV;
+    uint16_t* ks = reinterpret_cast<uint16_t*>(smem);   // [nbw][512]: K fragments
+    uint16_t* vs = ks + (size_t)nbw * 512;               // [nbw + 1][512]: V tiles, + a zero block
     __shared__ float kmax_w[WAVES];
 
     // fragment and slot range of head h inside a Q/K/V fragment
     const int frag = DH == 32 ? h : h / 2;
     const int slot0 = DH == 32 ? 0 : (h % 2) * 4;
+    const int vhalf = DH == 32 ? 0 : h % 2;     // V tile half of this head (dh = 16)
 
-    // ---- stage K (A fragments) and V^T; track max |k| over the real keys. All loads of a
-    // wavefront are issued before any is used, so the staging costs one memory round trip.
+    // ---- stage K and V: one 1 KB direct load per fragment; an odd key-block count gets a
+    // zero V block so the last superblock's missing keys meet P = 0 and V = 0
+    for (int kb = wave; kb < nbw; kb += WAVES) {
+        const uint16_t* src = p.QKV + (((tb_base + kb) * 3 + 1) * KSD + frag) * 512;
+        lds_load_1k(uniform_ptr(src), lds_addr(ks + kb * 512), lane);
+        lds_load_1k(uniform_ptr(src + KSD * 512), lds_addr(vs + kb * 512), lane);
+    }
+    if (nbw & 1)
+        for (int i = threadIdx.x; i < 256; i += blockDim.x) reinterpret_cast<uint32_t*>(vs + nbw * 512)[i] = 0u;
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    // max |k| over the real keys
     float kmax2 = 0.f;
-    for (int kb0 = wave; kb0 < nbw; kb0 += WAVES * SBATCH) {
-        u16x8 kv[SBATCH], vv[SBATCH];
+    for (int kb = wave; kb < nbw; kb += WAVES) {
+        const u16x8 kv = *reinterpret_cast<const u16x8*>(ks + (kb * 64 + lane) * 8);
+        float n2 = 0.f;
 #pragma unroll
-        for (int u = 0; u < SBATCH; ++u) {
-            const int kb = kb0 + u * WAVES;
-            if (kb < nbw) {
-                kv[u] = *reinterpret_cast<const u16x8*>(
-                    p.QKV + (((tb_base + kb) * 3 + 1) * KSD + frag) * 512 + lane * 8);
-                vv[u] = *reinterpret_cast<const u16x8*>(
-                    p.QKV + (((tb_base + kb) * 3 + 2) * KSD + frag) * 512 + lane * 8);
-            }
+        for (int i = 0; i < NV; ++i) {
+            const float f = (float)__builtin_bit_cast(__bf16, (uint16_t)kv[slot0 + i]);
+            n2 = fmaf(f, f, n2);
         }
-#pragma unroll
-        for (int u = 0; u < SBATCH; ++u) {
-            const int kb = kb0 + u * WAVES;
-            if (kb >= nbw) continue;
-            float n2 = 0.f;
-            u16x4 k4;
-#pragma unroll
-            for (int i = 0; i < NV; ++i) {
-                const uint16_t x = kv[u][slot0 + i];
-                const float f = (float)__builtin_bit_cast(__bf16, x);
-                n2 = fmaf(f, f, n2);
-                if (DH == 16) k4[i] = x;
-            }
-            if (DH == 32) *reinterpret_cast<u16x8*>(ks + (kb * 64 + lane) * 8) = kv[u];
-            else *reinterpret_cast<u16x4*>(ks + (kb * 64 + lane) * 4) = k4;
-            n2 = sum4(n2);
-            if (kb * 16 + col < N) kmax2 = fmaxf(kmax2, n2);
-            const int key = kb * 16 + col;
-            if (DH == 32) {
-#pragma unroll
-                for (int i = 0; i < 8; ++i) vt[kslot(g, i) * vts + key] = vv[u][i];
-            } else {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) vt[(4 * g + i) * vts + key] = vv[u][slot0 + i];
-            }
-        }
+        n2 = sum4(n2);
+        if (kb * 16 + col < N) kmax2 = fmaxf(kmax2, n2);
     }
 #pragma unroll
     for (int off = 1; off < 16; off <<= 1) kmax2 = fmaxf(kmax2, __shfl_xor(kmax2, off));
     if (lane == 0) kmax_w[wave] = kmax2;
-    // zero the key tail [Npad, 32*ceil(Npad/32)) so P = 0 never meets garbage
-    const int kpad = (p.Npad + 31) & ~31;
-    for (int idx = threadIdx.x; idx < DH * (kpad - p.Npad); idx += blockDim.x) {
-        const int r = idx / (kpad - p.Npad), k = p.Npad + idx % (kpad - p.Npad);
-        vt[r * vts + k] = 0;
-    }
     __syncthreads();
     float kmax = 0.f;
 #pragma unroll
@@ -206,11 +186,11 @@ __global__ __launch_bounds__(WAVES * 64) void attn_kernel(AttnParams p) {
         // prefetches below never need a bounds branch; such values are never used.
         auto load_k = [&](int sb, FT (&kf)[2]) {
 #pragma unroll
-            for (int kk = 0; kk < 2; ++kk) kf[kk] = ld_kfrag<DH>(ks, 2 * sb + kk, lane);
+            for (int kk = 0; kk < 2; ++kk) kf[kk] = ld_kfrag<DH>(ks, 2 * sb + kk, lane, slot0);
         };
         auto load_v = [&](int sb, bf16x8 (&vf)[RT]) {
 #pragma unroll
-            for (int rt = 0; rt < RT; ++rt) vf[rt] = ld_vfrag(vt, vts, rt, sb, col, g);
+            for (int rt = 0; rt < RT; ++rt) vf[rt] = ld_vfrag(vs, DH == 32 ? rt : vhalf, sb, lane);
         };
         // S^T - m of one superblock for every query block
         auto scores = [&](const FT (&kf)[2], f32x4 (&s)[QB][2]) {
@@ -268,7 +248,7 @@ __global__ __launch_bounds__(WAVES * 64) void attn_kernel(AttnParams p) {
             for (int kk = 0; kk < 2; ++kk) {
                 const int kb = 2 * last + kk;
                 if (kb < nbw) {
-                    const FT a = ld_kfrag<DH>(ks, kb, lane);
+                    const FT a = ld_kfrag<DH>(ks, kb, lane, slot0);
 #pragma unroll
                     for (int j = 0; j < QB; ++j) s[j][kk] = Frag<DH>::mma(a, q[j], shift[j]);
                 } else {
@@ -300,7 +280,7 @@ __global__ __launch_bounds__(WAVES * 64) void attn_kernel(AttnParams p) {
                     f32x4 s2[2];
                     for (int kk = 0; kk < 2; ++kk) {
                         const int kb = 2 * sb + kk;
-                        if (kb < nbw) s2[kk] = Frag<DH>::mma(ld_kfrag<DH>(ks, kb, lane), q[j], zero);
+                        if (kb < nbw) s2[kk] = Frag<DH>::mma(ld_kfrag<DH>(ks, kb, lane, slot0), q[j], zero);
                         else s2[kk] = f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
                         for (int i = 0; i < 4; ++i)
                             if (kb * 16 + 4 * g + i >= N) s2[kk][i] = -INFINITY;
@@ -322,7 +302,7 @@ __global__ __launch_bounds__(WAVES * 64) void attn_kernel(AttnParams p) {
                     mm = mnew;
                     const bf16x8 pb2 = pack_b(pr[0], pr[1]);
                     for (int rt = 0; rt < RT; ++rt)
-                        o[j][rt] = mfma16x16x32(ld_vfrag(vt, vts, rt, sb, col, g), pb2, o[j][rt] * alpha);
+                        o[j][rt] = mfma16x16x32(ld_vfrag(vs, DH == 32 ? rt : vhalf, sb, lane), pb2, o[j][rt] * alpha);
                 }
                 lt = sum4(ll);
             }
@@ -348,7 +328,9 @@ __global__ __launch_bounds__(WAVES * 64) void attn_kernel(AttnParams p) {
 }  // namespace
 
 size_t attn_smem_bytes(int dh, int Npad, int nbw) {
-    return (size_t)nbw * 64 * (dh == 32 ? 8 : 4) * 2 + (size_t)dh * vt_stride(Npad) * 2;
+    (void)dh;
+    (void)Npad;
+    return (size_t)(2 * nbw + 1) * 1024;   // K [nbw] and V [nbw + 1] fragments of 1 KB
 }
 
 template <int DH, int WAVES>

@@ -36,6 +36,31 @@ typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
 #define WIN_BULK 1
 #define WIN_FINAL 2
 
+// A wavefront-uniform pointer, pinned to scalar registers.
+template <typename T>
+PWD_DEV const T* uniform_ptr(const T* p) {
+    const uint64_t v = reinterpret_cast<uint64_t>(p);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+    return reinterpret_cast<const T*>(((uint64_t)hi << 32) | lo);
+}
+
+// 32-bit LDS address of a __shared__ location.
+template <typename T>
+PWD_DEV uint32_t lds_addr(T* p) {
+    return (uint32_t)reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) T*)p);
+}
+
+// One direct global->LDS load of 1 KB: lane l copies bytes [16 l, 16 l + 16) of the
+// wavefront-uniform `src` to LDS address `lds` + 16 l. Inline assembly, because the compiler's
+// wait-count pass treats a pending direct-to-LDS builtin as outstanding LDS traffic and then
+// waits for every LDS read before each use; callers await completion with s_waitcnt vmcnt.
+// The memory clobber keeps the load in program order relative to other memory accesses.
+PWD_DEV void lds_load_1k(const void* src, uint32_t lds, int lane) {
+    asm volatile("global_load_lds_dwordx4 %0, %1" :: "v"((uint32_t)lane * 16), "s"(src), "{m0}"(lds)
+                 : "memory");
+}
+
 PWD_DEV int kslot(int g, int i) { return i < 4 ? 4 * g + i : 16 + 4 * g + (i - 4); }
 
 PWD_DEV f32x4 mfma16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {

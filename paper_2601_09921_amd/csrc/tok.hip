@@ -88,6 +88,13 @@ PWD_DEV void stfrag(uint16_t* __restrict__ base, int64_t frag, int lane, bf16x8 
 
 PWD_DEV f32x4 ld4(const float* __restrict__ p) { return *reinterpret_cast<const f32x4*>(p); }
 
+PWD_DEV u16x4 to_bf16x4(f32x4 v) {
+    u16x4 r;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) r[i] = __builtin_bit_cast(uint16_t, (__bf16)v[i]);
+    return r;
+}
+
 PWD_DEV f32x4 relu4(f32x4 v) {
     f32x4 r;
 #pragma unroll
@@ -180,14 +187,6 @@ PWD_DEV uint16_t* wbuf() {
     return buf;
 }
 
-// A wavefront-uniform pointer, pinned to scalar registers.
-PWD_DEV const uint16_t* uniform_ptr(const uint16_t* p) {
-    const uint64_t v = reinterpret_cast<uint64_t>(p);
-    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
-    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
-    return reinterpret_cast<const uint16_t*>(((uint64_t)hi << 32) | lo);
-}
-
 // The weight stream of one launch: `post` chunks first, then `qkv` chunks, pulled through
 // the two LDS buffers (chunk i lives in buffer i % 2). sync<i % 2>(i) makes chunk i visible
 // to every wavefront. While the wavefronts compute on chunk i, the CHUNK / NW fragments
@@ -202,7 +201,7 @@ struct WeightPipe {
     const uint16_t* qkv;
     int n_post, total;
     int wave;            // wavefront index, wavefront-uniform
-    uint32_t lane_off;   // this lane's byte offset within a fragment
+    int lane;
 
     __device__ const uint16_t* src(int i) const {
         return i < n_post ? post + (size_t)i * CHUNK * FRAG : qkv + (size_t)(i - n_post) * CHUNK * FRAG;
@@ -210,19 +209,12 @@ struct WeightPipe {
     // source of the chunk loaded while chunk i is in use
     __device__ const uint16_t* next(int i) const { return src(i + 1 < total ? i + 1 : i); }
 
-    // One direct global->LDS load: 64 lanes x 16 bytes of fragment f of the chunk at `s`
-    // into fragment slot f of buffer PAR (M0 holds the slot's LDS address). It is inline
-    // assembly because the compiler's wait-count pass treats a pending direct-to-LDS load
-    // builtin as outstanding LDS traffic and then waits for every fragment read before each
-    // MFMA. Completion is awaited explicitly (vmcnt(0) in sync() and at kernel end); the
-    // memory clobber keeps each load in program order relative to the fragment reads.
+    // Fragment f of the chunk at `s` into fragment slot f of buffer PAR (one 1 KB direct
+    // load; awaited in sync() and at kernel end).
     template <int PAR>
     __device__ void part(const uint16_t* s, int j) const {
         const int f = wave * PER_WAVE + j;
-        const uint16_t* frag = uniform_ptr(s + f * FRAG);
-        const uint32_t lds = (uint32_t)reinterpret_cast<uintptr_t>(
-            (__attribute__((address_space(3))) uint16_t*)(wbuf<PAR, CHUNK>() + f * FRAG));
-        asm volatile("global_load_lds_dwordx4 %0, %1" :: "v"(lane_off), "s"(frag), "{m0}"(lds) : "memory");
+        lds_load_1k(uniform_ptr(s + f * FRAG), lds_addr(wbuf<PAR, CHUNK>() + f * FRAG), lane);
     }
     template <int PAR>
     __device__ void issue(int i) const {
@@ -303,14 +295,22 @@ struct Vecs {
 // Global stores a wavefront issues in one Q/K/V chunk after its last load of the next
 // chunk. Output group o2 is stored in the MFMA step of its last fragment read,
 // r = (o2 + 1) * 2 KS - 1, which follows the loads issued after reads up to r + LA - 1.
-template <int CHUNK, int NW, int KS, int LA>
+template <int CHUNK, int NW, int KS, int LA, int STORES_PER_GROUP>
 constexpr int qkv_stores_after_last_load() {
     constexpr int LAST = WeightPipe<CHUNK, NW>::template last_load_read<CHUNK, LA>();
     int n = 0;
     for (int o2 = 0; o2 < CHUNK / (2 * KS); ++o2)
-        if ((o2 + 1) * 2 * KS - 1 + LA - 1 >= LAST) n += TB;
+        if ((o2 + 1) * 2 * KS - 1 + LA - 1 >= LAST) n += STORES_PER_GROUP;
     return n;
 }
+
+template <typename F, int... I>
+PWD_DEV void static_for_impl(const F& f, std::integer_sequence<int, I...>) {
+    (f(std::integral_constant<int, I>{}), ...);
+}
+// f(integral_constant<int, i>) for i = 0 .. N-1, unrolled at compile time
+template <int N, typename F>
+PWD_DEV void static_for(const F& f) { static_for_impl(f, std::make_integer_sequence<int, N>{}); }
 
 template <int D, int FLAGS>
 __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 1) void tok_kernel(TokParams p) {
@@ -337,7 +337,7 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 1) void tok_kernel(To
     pipe.n_post = POST ? S::POST_CHUNKS : 0;
     pipe.total = pipe.n_post + (QKV ? S::QKV_CHUNKS : 0);
     pipe.wave = __builtin_amdgcn_readfirstlane(wave);
-    pipe.lane_off = (uint32_t)lane * 16;
+    pipe.lane = lane;
 
     // The activations come from HBM and are issued first, so their latency overlaps that of
     // the first weight chunk and of the vector staging below (all of it is awaited at the
@@ -367,11 +367,9 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 1) void tok_kernel(To
         for (int k = pipe.wave; k < NP_V + NQ_V; k += WAVES) {
             const float* src = k < NP_V ? p.post_vecs + k * 64 : p.bqkv + (k - NP_V) * 64;
             const int dst = k < NP_V ? k * 64 : V::BQKV + (k - NP_V) * 64;
-            const uint32_t lds = (uint32_t)reinterpret_cast<uintptr_t>(
-                (__attribute__((address_space(3))) float*)(vec + dst));
-            asm volatile("global_load_lds_dword %0, %1" :: "v"((uint32_t)lane * 4),
-                         "s"(reinterpret_cast<const float*>(uniform_ptr(reinterpret_cast<const uint16_t*>(src)))),
-                         "{m0}"(lds) : "memory");
+            // (inline assembly for the reason given at lds_load_1k)
+            asm volatile("global_load_lds_dword %0, %1" :: "v"((uint32_t)lane * 4), "s"(uniform_ptr(src)),
+                         "{m0}"(lds_addr(vec + dst)) : "memory");
         }
     }
 
@@ -528,12 +526,21 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 1) void tok_kernel(To
         constexpr int NP = POST ? S::POST_CHUNKS : 0;
         constexpr int OPC = S::OG_PER_CHUNK;
         constexpr int LA = LA_QKV;
-        constexpr int STORES_AFTER = qkv_stores_after_last_load<CHUNK, WAVES, KS, LA>();
-        auto qkv_chunk = [&](auto par, auto first, int qc) {
-            constexpr int PAR = decltype(par)::value;
+        // Q and K are stored as B fragments of their transposes (one 1 KB store per group and
+        // token block); V as two 16x16 tiles with tokens as rows (its MFMA takes the
+        // activations as the A operand), each 512 B, which the attention kernel copies to LDS
+        // unchanged as the A fragments of V^T.
+        constexpr int NQK = 2 * S::QKV_CHUNKS / 3;
+        static_assert(S::QKV_CHUNKS % 3 == 0, "Q, K and V in whole chunks");
+        constexpr int STORES_QK = qkv_stores_after_last_load<CHUNK, WAVES, KS, LA, TB>();
+        constexpr int STORES_V = qkv_stores_after_last_load<CHUNK, WAVES, KS, LA, 2 * TB>();
+        auto qkv_chunk = [&](auto qcc) {
+            constexpr int qc = decltype(qcc)::value;
+            constexpr int PAR = (NP + qc) & 1;
+            constexpr bool VOUT = qc >= NQK;
             // before the first QKV chunk, the residual stream store (RT * TB stores) follows
-            // the last load of this chunk
-            constexpr int YOUNGER = decltype(first)::value ? RT * TB : STORES_AFTER;
+            // the last load of this chunk; later, the previous chunk's output stores do
+            constexpr int YOUNGER = qc == 0 ? RT * TB : (qc - 1 >= NQK ? STORES_V : STORES_QK);
             const uint16_t* buf = pipe.template sync<PAR, YOUNGER>(NP + qc);
             // fragment r = (o2 * KS + ks) * 2 + hh: rows 16 hh .. 16 hh + 15 of output group
             // qc * OPC + o2, k-step ks
@@ -542,9 +549,14 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 1) void tok_kernel(To
             for (int o2 = 0; o2 < OPC; ++o2)
 #pragma unroll
                 for (int hh = 0; hh < 2; ++hh) {
-                    const f32x4 bias = ld4(vec + V::BQKV + (qc * OPC + o2) * 32 + hh * 16 + 4 * g);
+                    if constexpr (VOUT) {   // bias (along the tile's columns) added at the store
 #pragma unroll
-                    for (int b = 0; b < TB; ++b) q[o2][hh][b] = bias;
+                        for (int b = 0; b < TB; ++b) q[o2][hh][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+                    } else {
+                        const f32x4 bias = ld4(vec + V::BQKV + (qc * OPC + o2) * 32 + hh * 16 + 4 * g);
+#pragma unroll
+                        for (int b = 0; b < TB; ++b) q[o2][hh][b] = bias;
+                    }
                 }
             const uint16_t* nx = pipe.next(NP + qc);
             __builtin_amdgcn_sched_barrier(0);
@@ -553,33 +565,37 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 1) void tok_kernel(To
                 [&](int r, const bf16x8& a) {
                     const int hh = r & 1, ks = (r >> 1) % KS, o2 = (r >> 1) / KS;
 #pragma unroll
-                    for (int b = 0; b < TB; ++b) q[o2][hh][b] = mfma16x16x32(a, xb[ks][b], q[o2][hh][b]);
+                    for (int b = 0; b < TB; ++b) {
+                        if constexpr (VOUT) q[o2][hh][b] = mfma16x16x32(xb[ks][b], a, q[o2][hh][b]);
+                        else q[o2][hh][b] = mfma16x16x32(a, xb[ks][b], q[o2][hh][b]);
+                    }
                     if (hh == 1 && ks == KS - 1) {
                         const int og = qc * OPC + o2;
-                        const float sc = og < KS ? p.qscale : 1.0f;   // Q: log2(e)/sqrt(dh)
 #pragma unroll
-                        for (int b = 0; b < TB; ++b)
-                            stfrag(p.QKV, (tb0 + b) * (3 * KS) + og, lane,
-                                   pack_b(q[o2][0][b] * sc, q[o2][1][b] * sc));
+                        for (int b = 0; b < TB; ++b) {
+                            if constexpr (VOUT) {
+                                uint16_t* t = p.QKV + ((tb0 + b) * (3 * KS) + og) * FRAG + lane * 4;
+#pragma unroll
+                                for (int h2 = 0; h2 < 2; ++h2) {
+                                    const float bias = vec[V::BQKV + og * 32 + h2 * 16 + col];
+                                    st_stream(reinterpret_cast<u16x4*>(t + h2 * (FRAG / 2)), to_bf16x4(q[o2][h2][b] + bias));
+                                }
+                            } else {
+                                const float sc = og < KS ? p.qscale : 1.0f;   // Q: log2(e)/sqrt(dh)
+                                stfrag(p.QKV, (tb0 + b) * (3 * KS) + og, lane,
+                                       pack_b(q[o2][0][b] * sc, q[o2][1][b] * sc));
+                            }
+                        }
                     }
                 },
                 [&](int r) { pipe.template after_read<1 - PAR, CHUNK, LA>(nx, r); });
             sched_pipeline<CHUNK, TB, LA>();
         };
-        constexpr int Q0 = NP & 1;
-        using first = std::true_type;
-        using later = std::false_type;
-        qkv_chunk(std::integral_constant<int, Q0>{}, first{}, 0);
-        int qc = 1;
-        for (; qc + 1 < S::QKV_CHUNKS; qc += 2) {
-            qkv_chunk(std::integral_constant<int, 1 - Q0>{}, later{}, qc);
-            qkv_chunk(std::integral_constant<int, Q0>{}, later{}, qc + 1);
-        }
-        if constexpr (S::QKV_CHUNKS % 2 == 0) qkv_chunk(std::integral_constant<int, 1 - Q0>{}, later{}, qc);
+        static_for<S::QKV_CHUNKS>(qkv_chunk);
     }
     // The last chunk's reload into the idle buffer must land before the workgroup's LDS is
     // freed; the global stores issued after it need not.
-    constexpr int END_YOUNGER = QKV ? qkv_stores_after_last_load<CHUNK, WAVES, KS, LA_QKV>() : RT * TB;
+    constexpr int END_YOUNGER = QKV ? qkv_stores_after_last_load<CHUNK, WAVES, KS, LA_QKV, 2 * TB>() : RT * TB;
     asm volatile("s_waitcnt vmcnt(%0)" :: "n"(END_YOUNGER) : "memory");
 }
 
