@@ -38,6 +38,8 @@ STAGE_KERNELS = {
     "post": "tok_kernel<256, 1>",
     "readout": "readout_kernel<256>",
     "fp32_window": "f32_window_kernel",
+    "stream_split": "stream_split_kernel",
+    "stream_combine": "stream_combine_kernel",
 }
 
 
@@ -80,6 +82,36 @@ def load_traffic(stage):
     return t.get("bytes_per_launch", {}).get(stage)
 
 
+def stream_measurement(dec, wl, torch, pwdec, synth):
+    """One decode_stream of a memory experiment as long as the batch (B windows of d rounds,
+    the last one ragged): on-device windowing, decoding and XOR / soft-XOR combination."""
+    T = wl.B * wl.d - 7
+    R = synth.make_stream(wl.N, T, wl.p, seed=2025)
+    rounds = torch.from_numpy(np.ascontiguousarray(synth.pack_bits(R)).view(np.int32)).cuda()
+    del R
+    bit = torch.zeros(1, dtype=torch.uint8, device="cuda")
+    prob = torch.zeros(1, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    dec.decode_stream(rounds, bit, prob, stream=stream)          # warm-up
+    torch.cuda.synchronize()
+    dec.profile(True)
+    t0 = time.perf_counter()
+    dec.decode_stream(rounds, bit, prob, stream=stream)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    stages = dec.profile_read()
+    dec.profile(False)
+    m = -(-T // wl.d)
+    split_ms = stages["stream_split"][0]
+    split_bytes = T * wl.words * 4 + m * (wl.W + 1) * wl.words * 4 + m
+    return {
+        "rounds": T, "windows": m, "ms": round(dt * 1e3, 2), "us_per_round": dt / T * 1e6,
+        "split_ms": round(split_ms, 4), "split_GBps": round(split_bytes / (split_ms * 1e-3) / 1e9, 1),
+        "combine_ms": round(stages["stream_combine"][0], 4),
+        "bit": int(bit.item()), "soft_xor": float(prob.item()),
+    }
+
+
 def cpu_baseline(wl, weights, sample):
     """The fp64 oracle on `sample` windows (one per window type) on the host cores."""
     from oracle import decoder as O
@@ -113,6 +145,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="d25")
     ap.add_argument("--cpu-sample", type=int, default=3, help="oracle windows for the CPU baseline (0: skip)")
+    ap.add_argument("--no-stream", action="store_true", help="skip the decode_stream measurement")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first copy 1 GiB device-to-device 3 times (the known-size reference that "
                          "scales rocprofv3 FETCH_SIZE / WRITE_SIZE counters)")
@@ -222,6 +255,8 @@ def main():
             "traffic": load_traffic(dom),
         },
     }
+    if not args.no_stream:
+        out["stream"] = stream_measurement(dec, wl, torch, pwdec, synth)
     dec.close()
     if args.cpu_sample > 0:
         out["cpu_baseline"] = cpu_baseline(wl, weights, args.cpu_sample)

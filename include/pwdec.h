@@ -134,6 +134,25 @@ int decode_windows(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_ty
 int decoder_detection_events(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_types,
                              int64_t n_windows, uint32_t* d_events, void* hip_stream);
 
+/* Decodes a whole memory experiment (Sec. 3.1 windowing; eq. global_xor and eq. soft_xor).
+ * The stream of T measurement rounds is cut on the device into m = ceil(T / distance)
+ * windows: window i has core rounds [i d, i d + d) and rows R[i d - b_left - 1 + k] for
+ * k = 0..window_rounds, b_left = (window_rounds - distance) / 2; rows before the stream read
+ * as zeros and rows after it repeat round T-1 (the stream padded to m d rounds by holding its
+ * last round). Window 0 is initial, window m-1 final, the others bulk. The windows are
+ * decoded as by decode_windows and their results combined:
+ *   d_stream:        uint32 [T][words] packed rounds, as the rows of decode_windows.
+ *   d_window_logits: float [m] out, or NULL; d_window_bits: uint8 [m] out, or NULL.
+ *   d_bit:           uint8 [1] out: XOR of the window bits, the global logical correction.
+ *   d_prob:          float [1] out, or NULL: soft-XOR (1 - prod_k (1 - 2 y_k)) / 2 of the
+ *                    window probabilities y_k = 1 / (1 + exp(-logit_k)), accumulated in
+ *                    double in a fixed order.
+ * PWD_EINVAL if dec, d_stream or d_bit is NULL or T <= 0; PWD_EBATCH unless
+ * 2 <= m <= max_windows. The window scratch (allocated by decoder_create) belongs to the
+ * handle, so calls on one handle must not overlap. */
+int decode_stream(pwd_decoder* dec, const uint32_t* d_stream, int64_t T, float* d_window_logits,
+                  uint8_t* d_window_bits, uint8_t* d_bit, float* d_prob, void* hip_stream);
+
 /* Synchronises hip_stream, then reports PWD_EDEVICE if a device-side check fired since
  * the previous call (and clears it), PWD_EHIP on a stream error, else PWD_OK. */
 int decoder_sync_status(pwd_decoder* dec, void* hip_stream);
@@ -151,7 +170,9 @@ enum {
     PWD_STAGE_POST = 4,           /* last layer of the last round */
     PWD_STAGE_READOUT = 5,        /* readout */
     PWD_STAGE_FP32_WINDOW = 6,    /* the whole fp32 decoder (fp32 configurations) */
-    PWD_NUM_STAGES = 7
+    PWD_STAGE_STREAM_SPLIT = 7,   /* decode_stream: cutting the stream into windows */
+    PWD_STAGE_STREAM_COMBINE = 8, /* decode_stream: XOR and soft-XOR of the window results */
+    PWD_NUM_STAGES = 9
 };
 
 typedef struct {

@@ -80,3 +80,21 @@ hipError_t launch_readout(const ReadoutParams& p, hipStream_t s);
 hipError_t launch_f32_window(const F32Params& p, hipStream_t s);
 size_t f32_window_smem_bytes(int N, int D, int H, int F);
 size_t attn_smem_bytes(int dh, int Npad, int nbw);
+
+// Stream decoding (stream.hip)
+struct StreamSplitParams {
+    const uint32_t* stream;   // [T][words]
+    int64_t T;
+    int m, d, W, b_left, words;
+    uint32_t* meas;           // [m][W + 1][words] out
+    uint8_t* types;           // [m] out
+};
+struct StreamCombineParams {
+    const float* logits;      // [m]
+    const uint8_t* bits;      // [m]
+    int m;
+    uint8_t* bit;             // [1] out
+    float* prob;              // [1] out, or null
+};
+hipError_t launch_stream_split(const StreamSplitParams& p, hipStream_t s);
+hipError_t launch_stream_combine(const StreamCombineParams& p, hipStream_t s);

@@ -135,6 +135,11 @@ struct pwd_decoder {
     uint16_t* QKV = nullptr;
     uint16_t* Y = nullptr;
     int* err = nullptr;
+    // decode_stream scratch: the windows cut from a stream and their results
+    uint32_t* stream_meas = nullptr;   // [max_windows][W + 1][words]
+    uint8_t* stream_types = nullptr;   // [max_windows]
+    float* stream_logits = nullptr;    // [max_windows]
+    uint8_t* stream_bits = nullptr;    // [max_windows]
     // views into `weights`
     struct Layer {
         const uint16_t *post, *qkv;
@@ -412,6 +417,14 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
     } else {
         dec->f32w = fptr(off_f32);
     }
+    {
+        const size_t mw = (size_t)dec->max_windows;
+        const size_t mb = mw * (dec->W + 1) * dec->words * sizeof(uint32_t);
+        if ((e = hipMalloc(&dec->stream_meas, mb)) != hipSuccess || (e = hipMalloc(&dec->stream_types, mw)) != hipSuccess ||
+            (e = hipMalloc(&dec->stream_logits, mw * sizeof(float))) != hipSuccess ||
+            (e = hipMalloc(&dec->stream_bits, mw)) != hipSuccess)
+            return cleanup_fail(fail(PWD_ENOMEM, "stream scratch for %d windows: %s", dec->max_windows, hipGetErrorString(e)));
+    }
     *out = dec;
     return PWD_OK;
 }
@@ -424,6 +437,10 @@ int decoder_destroy(pwd_decoder* dec) {
     (void)hipFree(dec->QKV);
     (void)hipFree(dec->Y);
     (void)hipFree(dec->err);
+    (void)hipFree(dec->stream_meas);
+    (void)hipFree(dec->stream_types);
+    (void)hipFree(dec->stream_logits);
+    (void)hipFree(dec->stream_bits);
     for (auto& m : dec->marks) {
         (void)hipEventDestroy(m.begin);
         (void)hipEventDestroy(m.end);
@@ -558,6 +575,43 @@ int decoder_detection_events(pwd_decoder* dec, const uint32_t* d_meas, const uin
     p.events = d_events;
     p.err = dec->err;
     HIP_OK(launch_events(p, static_cast<hipStream_t>(hip_stream)));
+    return PWD_OK;
+}
+
+int decode_stream(pwd_decoder* dec, const uint32_t* d_stream, int64_t T, float* d_window_logits,
+                  uint8_t* d_window_bits, uint8_t* d_bit, float* d_prob, void* hip_stream) {
+    if (!dec) return fail(PWD_EINVAL, "null decoder");
+    if (!d_stream || !d_bit) return fail(PWD_EINVAL, "null buffer");
+    if (T <= 0) return fail(PWD_EINVAL, "stream of %lld rounds", (long long)T);
+    const int64_t m = (T + dec->d - 1) / dec->d;
+    if (m < 2 || m > dec->max_windows)
+        return fail(PWD_EBATCH, "a stream of %lld rounds makes %lld windows; need 2..%d", (long long)T, (long long)m,
+                    dec->max_windows);
+    DeviceGuard dg(dec->device);
+    HIP_OK(dg.err);
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+    StreamSplitParams sp;
+    sp.stream = d_stream;
+    sp.T = T;
+    sp.m = (int)m;
+    sp.d = dec->d;
+    sp.W = dec->W;
+    sp.b_left = dec->b_left;
+    sp.words = dec->words;
+    sp.meas = dec->stream_meas;
+    sp.types = dec->stream_types;
+    HIP_OK(timed(dec, PWD_STAGE_STREAM_SPLIT, s, [&] { return launch_stream_split(sp, s); }));
+    float* logits = d_window_logits ? d_window_logits : dec->stream_logits;
+    uint8_t* bits = d_window_bits ? d_window_bits : dec->stream_bits;
+    const int rc = decode_windows(dec, dec->stream_meas, dec->stream_types, m, logits, bits, hip_stream);
+    if (rc != PWD_OK) return rc;
+    StreamCombineParams cp;
+    cp.logits = logits;
+    cp.bits = bits;
+    cp.m = (int)m;
+    cp.bit = d_bit;
+    cp.prob = d_prob;
+    HIP_OK(timed(dec, PWD_STAGE_STREAM_COMBINE, s, [&] { return launch_stream_combine(cp, s); }));
     return PWD_OK;
 }
 

@@ -39,8 +39,9 @@ class ModelDims(ctypes.Structure):
                 ("mlp_ratio", ctypes.c_int32), ("dtype", ctypes.c_int32)]
 
 
-NUM_STAGES = 7
-STAGE_NAMES = ["embed_qkv", "attention", "post_qkv", "post_embed_qkv", "post", "readout", "fp32_window"]
+NUM_STAGES = 9
+STAGE_NAMES = ["embed_qkv", "attention", "post_qkv", "post_embed_qkv", "post", "readout", "fp32_window",
+               "stream_split", "stream_combine"]
 
 
 class StageTimes(ctypes.Structure):
@@ -65,6 +66,7 @@ def load_library() -> ctypes.CDLL:
         "decoder_create": (ctypes.c_int, [P(Geometry), P(ModelDims), ctypes.c_void_p, ctypes.c_size_t, P(VP)]),
         "decode_windows": (ctypes.c_int, [VP, VP, VP, I64, VP, VP, VP]),
         "decoder_detection_events": (ctypes.c_int, [VP, VP, VP, I64, VP, VP]),
+        "decode_stream": (ctypes.c_int, [VP, VP, I64, VP, VP, VP, VP, VP]),
         "decoder_sync_status": (ctypes.c_int, [VP, VP]),
         "decoder_last_error": (ctypes.c_char_p, []),
         "decoder_destroy": (ctypes.c_int, [VP]),
@@ -149,6 +151,14 @@ class Decoder:
                                         ctypes.c_void_p(types.data_ptr()), n,
                                         ctypes.c_void_p(logits.data_ptr()), ctypes.c_void_p(bits.data_ptr()),
                                         _stream_ptr(stream)))
+
+    def decode_stream(self, rounds, bit, prob=None, window_logits=None, window_bits=None, stream=None):
+        """rounds: int32/uint32 [T][words] cuda tensor of packed measurement rounds; bit: uint8 [1]
+        out; prob: float32 [1] out or None; window_logits / window_bits: float32 / uint8
+        [ceil(T/d)] out or None."""
+        ptr = lambda t: ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+        _check(self._lib.decode_stream(self._h, ptr(rounds), rounds.shape[0], ptr(window_logits),
+                                       ptr(window_bits), ptr(bit), ptr(prob), _stream_ptr(stream)))
 
     def detection_events(self, meas, types, events, stream=None):
         n = types.shape[0]

@@ -1,0 +1,116 @@
+"""GPU parity of decode_stream, the decoding of a whole memory experiment: windowing of the
+stream (Sec. 3.1), per-window decoding, XOR of the window bits (eq. global_xor) and soft-XOR
+of the window probabilities (eq. soft_xor), against the oracle's split_stream,
+forward_windows, combine_bits and soft_xor on the same seeded streams."""
+import numpy as np
+import pytest
+
+from gpu_helpers import BF16_ATOL, BIT_MARGIN, FP32_ATOL, FP32_RTOL, say, weights
+from oracle import decoder as O
+from paper_2601_09921_amd import pwdec, synth
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def sigmoid(x):
+    return 1.0 / (1.0 + np.exp(-np.asarray(x, dtype=np.float64)))
+
+
+def run_stream(dec, R, m, with_windows=True):
+    rounds = torch.from_numpy(np.ascontiguousarray(synth.pack_bits(R)).view(np.int32)).cuda()
+    bit = torch.full((1,), 7, dtype=torch.uint8, device="cuda")
+    prob = torch.full((1,), float("nan"), dtype=torch.float32, device="cuda")
+    wl = torch.full((m,), float("nan"), dtype=torch.float32, device="cuda") if with_windows else None
+    wb = torch.full((m,), 7, dtype=torch.uint8, device="cuda") if with_windows else None
+    dec.decode_stream(rounds, bit, prob, wl, wb)
+    torch.cuda.synchronize()
+    out = [int(bit.item()), float(prob.item())]
+    if with_windows:
+        out += [wl.cpu().numpy(), wb.cpu().numpy()]
+    return out
+
+
+def logit_bound(wl, o):
+    return FP32_RTOL * np.abs(o) + FP32_ATOL if wl.dtype == synth.DTYPE_F32 else np.full_like(o, BF16_ATOL)
+
+
+# (workload, stream rounds): ragged tails (T not a multiple of d), the two-window minimum and an
+# exact multiple of d
+CASES = [("d3", 3 * 7 + 2), ("d3", 3 + 1), ("d7", 7 * 12), ("d7", 7 * 5 + 3)]
+
+
+@pytest.mark.parametrize("name,T", CASES, ids=[f"{c[0]}_T{c[1]}" for c in CASES])
+@pytest.mark.parametrize("zero", [False, True], ids=["events", "zero"])
+def test_stream_parity(name, T, zero):
+    wl = synth.WORKLOADS[name]
+    w = weights(name)
+    R = np.zeros((T, wl.N), np.uint8) if zero else synth.make_stream(wl.N, T, 0.05, seed=31 + T)
+    m = -(-T // wl.d)
+    say(f"stream {name} T={T} m={m} zero={zero}")
+    dec = pwdec.Decoder.from_workload(wl, w, max_windows=m)
+    bit, prob, glog, gbits = run_stream(dec, R, m)
+    assert dec.sync_status() == pwdec.PWD_OK
+    meas, types = O.split_stream(R, wl.d, wl.W)
+    olog, _ = O.forward_windows(meas, types, w, wl.d, wl.H)
+    bound = logit_bound(wl, olog)
+    assert np.isfinite(glog).all()
+    assert (np.abs(glog - olog) <= bound).all(), (glog, olog)
+    assert np.array_equal(gbits, (glog > 0).astype(np.uint8))
+    # global correction: exactly the XOR of the decoder's own window bits, and the oracle's
+    # whenever every window is decided with margin
+    assert bit == O.combine_bits(gbits)
+    if (np.abs(olog) > BIT_MARGIN).all():
+        assert bit == O.combine_bits((olog > 0).astype(np.uint8))
+    # soft-XOR: the device's double accumulation of its own logits; against the oracle, each
+    # window moves the soft-XOR by at most |d sigmoid| <= |d logit| / 4
+    assert prob == pytest.approx(O.soft_xor(sigmoid(glog)), rel=1e-5, abs=1e-6)
+    assert abs(prob - O.soft_xor(sigmoid(olog))) <= float(np.sum(bound)) / 4 + 1e-6
+    # the same stream without the per-window outputs gives the same combined results
+    bit2, prob2 = run_stream(dec, R, m, with_windows=False)
+    assert bit2 == bit and np.float32(prob2) == np.float32(prob)
+    dec.close()
+
+
+def test_stream_rejects_bad_lengths():
+    wl = synth.WORKLOADS["d3"]
+    dec = pwdec.Decoder.from_workload(wl, weights("d3"), max_windows=4)
+    bit = torch.zeros(1, dtype=torch.uint8, device="cuda")
+    for T, rc in ((wl.d, pwdec.PWD_EBATCH), (4 * wl.d + 1, pwdec.PWD_EBATCH)):   # 1 window; 5 > 4
+        rounds = torch.zeros((T, wl.words), dtype=torch.int32, device="cuda")
+        with pytest.raises(pwdec.PwdError) as e:
+            dec.decode_stream(rounds, bit)
+        assert e.value.code == rc
+    rounds = torch.zeros((0, wl.words), dtype=torch.int32, device="cuda")
+    with pytest.raises(pwdec.PwdError) as e:
+        dec.decode_stream(rounds, bit)
+    assert e.value.code == pwdec.PWD_EINVAL
+    dec.close()
+
+
+def test_stream_full_size_sampled():
+    """The benchmark's d=25 batch size as one stream of 8192 windows (ragged last window):
+    the initial, one bulk and the final window against the oracle, and the XOR of all."""
+    wl = synth.WORKLOADS["d25"]
+    w = weights("d25")
+    T = wl.B * wl.d - 7
+    m = -(-T // wl.d)
+    R = synth.make_stream(wl.N, T, wl.p, seed=2025)
+    say(f"stream d25 T={T} m={m}")
+    dec = pwdec.Decoder.from_workload(wl, w, max_windows=m)
+    bit, prob, glog, gbits = run_stream(dec, R, m)
+    assert dec.sync_status() == pwdec.PWD_OK
+    assert np.isfinite(glog).all() and bit == O.combine_bits(gbits)
+    assert prob == pytest.approx(O.soft_xor(sigmoid(glog)), rel=1e-5, abs=1e-6)
+    dec.close()
+    meas, types = O.split_stream(R, wl.d, wl.W)
+    sample = np.array([0, m // 2, m - 1])
+    say("  oracle on 3 windows")
+    olog, _ = O.forward_windows(meas[sample], types[sample], w, wl.d, wl.H)
+    assert (np.abs(glog[sample] - olog) <= BF16_ATOL).all(), (glog[sample], olog)

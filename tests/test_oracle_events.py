@@ -117,6 +117,21 @@ def test_soft_xor():
     assert O.soft_xor(np.array([0.5, 0.1])) == pytest.approx(0.5)
 
 
+def test_soft_xor_is_the_probability_of_an_odd_count():
+    """Brute force over every outcome of m independent bits: P(XOR = 1) = sum of the
+    probabilities of the outcomes with an odd number of ones."""
+    import itertools
+    rng = np.random.default_rng(9)
+    for m in range(1, 7):
+        p = rng.random(m)
+        odd = 0.0
+        for bits in itertools.product((0, 1), repeat=m):
+            pr = np.prod([pk if b else 1.0 - pk for pk, b in zip(p, bits)])
+            if sum(bits) % 2:
+                odd += pr
+        assert O.soft_xor(p) == pytest.approx(odd, rel=1e-12, abs=1e-15)
+
+
 def test_synth_windows_follow_boundary_conventions():
     wl = synth.with_batch(synth.WORKLOADS["d7"], 9)
     meas, types = synth.make_windows(wl)
