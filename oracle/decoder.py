@@ -287,6 +287,30 @@ def forward_windows(meas: np.ndarray, types: np.ndarray, w: dict, d: int, H: int
     return logits, bits
 
 
+def forward_windows_recurrent(meas: np.ndarray, types: np.ndarray, w: dict, d: int, H: int):
+    """Algorithm 1, recurrent branch: the same pass over the window's rounds, with a readout
+    of the decoder state after every round n > 2b (Sec. recurrent training), i.e. after the
+    rounds that complete a window of b left buffer, tau core and b right buffer rounds,
+    tau = 1..c. With left and right buffers b_L, b_R (W = b_L + c + b_R) these are the rounds
+    n = W - c + 1 .. W. Returns logits [B][c] (column tau-1) and bits; the last column is the
+    inference-branch result.
+    """
+    meas = np.asarray(meas, dtype=np.uint8)
+    B, W1, N = meas.shape
+    Wr = W1 - 1
+    D = w["w_e"].shape[0]
+    ev = detection_events(meas, types, d)
+    pe = positional_encoding((d + 1) ** 2, D)[grid_positions(d)]
+    state = np.zeros((B, N, D), dtype=np.float64)
+    logits = np.zeros((B, d), dtype=np.float64)
+    for n in range(1, Wr + 1):
+        S = embed(ev[:, n - 1, :], w, pe)
+        state = rnn_core(w["kappa"] * (S + state), w, H)
+        if n > Wr - d:
+            logits[:, n - (Wr - d) - 1] = readout(state, types, w, d)
+    return logits, (logits > 0).astype(np.uint8)
+
+
 def decode_stream(R: np.ndarray, w: dict, d: int, W: int, H: int) -> int:
     """Decode a whole memory experiment: split, decode every window, XOR the bits."""
     meas, types = split_stream(R, d, W)

@@ -256,6 +256,28 @@ def test_forward_invariants():
     assert abs(la[0] - la[1]) > 1e-6
 
 
+def test_recurrent_readouts():
+    """Algorithm 1's recurrent branch: the last readout is the inference result, and by
+    causality the readout after round n of a bulk window (no masks) is the decode of the
+    window cut after round n, here from the independent torch model."""
+    import dataclasses
+    wl = tiny_workload(B=9, W=8, p=0.3)
+    w = synth.make_weights(wl, seed=6)
+    meas, types = synth.make_windows(wl, seed=8, realistic_boundaries=False)
+    rl, rb = O.forward_windows_recurrent(meas, types, w, wl.d, wl.H)
+    fl, _ = O.forward_windows(meas, types, w, wl.d, wl.H)
+    assert rl.shape == (wl.B, wl.d) and np.array_equal(rb, (rl > 0).astype(np.uint8))
+    assert np.array_equal(rl[:, -1], fl)
+    bulk = types == O.BULK
+    assert bulk.sum() >= 2
+    for tau in range(wl.d):
+        n = wl.W - wl.d + 1 + tau
+        ref = torch_model_logits(meas[bulk, :n + 1], types[bulk], w, dataclasses.replace(wl, W=n))
+        assert np.allclose(rl[bulk, tau], ref, atol=1e-10)
+    # the readouts move with the rounds they have seen
+    assert np.ptp(rl, axis=1).min() > 1e-9
+
+
 def test_stream_decode_is_xor_of_windows():
     wl = tiny_workload(B=1, W=6)
     w = synth.make_weights(wl, seed=4)
