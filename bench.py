@@ -112,6 +112,26 @@ def stream_measurement(dec, wl, torch, pwdec, synth):
     }
 
 
+def recurrent_measurement(dec, wl, torch, dev_meas, dev_types):
+    """One decode_windows_recurrent of the batch: the same pass with a readout after each of
+    the last d rounds (Algorithm 1, recurrent branch)."""
+    logits = torch.empty((wl.B, wl.d), dtype=torch.float32, device="cuda")
+    bits = torch.empty((wl.B, wl.d), dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    dec.decode_recurrent(dev_meas, dev_types, logits, bits, stream)   # warm-up
+    torch.cuda.synchronize()
+    dec.profile(True)
+    t0 = time.perf_counter()
+    dec.decode_recurrent(dev_meas, dev_types, logits, bits, stream)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    stages = dec.profile_read()
+    dec.profile(False)
+    ro_ms, ro_n = stages["readout"]
+    return {"readouts_per_window": wl.d, "ms": round(dt * 1e3, 2), "us_per_round": dt / (wl.B * wl.d) * 1e6,
+            "readout_launches": ro_n, "readout_ms_total": round(ro_ms, 2)}
+
+
 def cpu_baseline(wl, weights, sample):
     """The fp64 oracle on `sample` windows (one per window type) on the host cores."""
     from oracle import decoder as O
@@ -146,6 +166,7 @@ def main():
     ap.add_argument("--workload", default="d25")
     ap.add_argument("--cpu-sample", type=int, default=3, help="oracle windows for the CPU baseline (0: skip)")
     ap.add_argument("--no-stream", action="store_true", help="skip the decode_stream measurement")
+    ap.add_argument("--no-recurrent", action="store_true", help="skip the recurrent-readout measurement")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first copy 1 GiB device-to-device 3 times (the known-size reference that "
                          "scales rocprofv3 FETCH_SIZE / WRITE_SIZE counters)")
@@ -257,6 +278,8 @@ def main():
     }
     if not args.no_stream:
         out["stream"] = stream_measurement(dec, wl, torch, pwdec, synth)
+    if not args.no_recurrent:
+        out["recurrent"] = recurrent_measurement(dec, wl, torch, dev_meas, dev_types)
     dec.close()
     if args.cpu_sample > 0:
         out["cpu_baseline"] = cpu_baseline(wl, weights, args.cpu_sample)

@@ -128,6 +128,16 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims,
 int decode_windows(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_types,
                    int64_t n_windows, float* d_logits, uint8_t* d_bits, void* hip_stream);
 
+/* The recurrent branch of Algorithm 1 (Sec. recurrent training): the same pass over each
+ * window, with a readout of the decoder state after every round n > W - distance (the rounds
+ * that complete a window of left buffer, tau core and right buffer rounds, tau = 1..distance).
+ *   d_logits: float [n_windows][distance] out, column tau-1 after round W - distance + tau;
+ *   d_bits:   uint8 [n_windows][distance] out, 1 iff logit > 0.
+ * The last column is what decode_windows returns. Arguments, errors and the type check as
+ * for decode_windows. */
+int decode_windows_recurrent(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_types,
+                             int64_t n_windows, float* d_logits, uint8_t* d_bits, void* hip_stream);
+
 /* Writes the detection events the decoder feeds to its network:
  * d_events uint32 [n_windows][window_rounds][words], packed as the input. Same masks and
  * type check as decode_windows (an invalid type yields all-zero events). */

@@ -1,6 +1,6 @@
 // fp32 decoder for small windows: one workgroup runs one window through every round,
-// layer and the readout with its whole state in LDS (Algorithm 1, inference branch;
-// App. A model). Used for the fp32 configurations (d_model <= 64, about d <= 5), where a
+// layer and the readout with its whole state in LDS (Algorithm 1, inference branch, or the
+// recurrent branch's readout after each of the last rounds; App. A model). Used for the fp32 configurations (d_model <= 64, about d <= 5), where a
 // window is a few kilobytes and the batch is small, so one launch per decode is the point.
 //
 // All matrix products are fp32 FMA loops with the model width as a compile-time constant,
@@ -98,6 +98,53 @@ __global__ __launch_bounds__(THREADS) void f32_window_kernel(F32Params p) {
     const float* we = p.w;
     const float scale = rsqrtf((float)dh);
 
+    // readout (App. A.3) of the current state into output slot k: 2x2 valid convolution +
+    // ReLU, mean over columns, linear; one fixed-order reduction over the workgroup
+    auto readout = [&](int k) {
+        LayerPtrs L;
+        const float* Wc = layer_ptrs(p.w, D, F, p.L - 1, L);
+        const float* bc = Wc + 4 * (size_t)D * D;
+        const float* wo = bc + D;
+        const float bo = wo[(size_t)d * D];
+        const float* beta = wo + (size_t)d * D + 1;
+        const int gw = d + 1;
+        float part = 0.f;
+        for (int idx = threadIdx.x; idx < d * D; idx += THREADS) {
+            const int i = idx / D, o = idx % D;
+            float pool = 0.f;
+            for (int j = 0; j < d; ++j) {
+                float acc = bc[o];
+                for (int a = 0; a < 2; ++a)
+                    for (int b = 0; b < 2; ++b) {
+                        const int tok = p.cell_token[(i + a) * gw + (j + b)];
+                        if (tok < 0) continue;
+                        acc += dot_col<D>(X + tok * D, Wc + (size_t)(a * 2 + b) * D * D, D, o);
+                    }
+                pool += fmaxf(acc, 0.f);
+            }
+            part = fmaf(wo[idx], pool / (float)d, part);
+        }
+        red[threadIdx.x] = part;
+        __syncthreads();
+        for (int n = THREADS / 2; n > 0; n >>= 1) {
+            if ((int)threadIdx.x < n) red[threadIdx.x] += red[threadIdx.x + n];
+            __syncthreads();
+        }
+        if (threadIdx.x == 0) {
+            const int64_t o = (int64_t)win * p.readouts + k;
+            if (type > WIN_FINAL) {
+                p.logits[o] = __builtin_nanf("");
+                p.bits[o] = 0;
+                atomicOr(p.err, 1);
+            } else {
+                const float logit = red[0] + bo + beta[type];
+                p.logits[o] = logit;
+                p.bits[o] = logit > 0.f ? 1 : 0;
+            }
+        }
+        __syncthreads();   // red is reused by the next readout
+    };
+
     for (int t = 0; t < p.in.W; ++t) {
         for (int wd = threadIdx.x; wd < p.in.words; wd += THREADS)
             ev[wd] = type > WIN_FINAL ? 0u : event_word(meas, p.in.words, t, wd, type, p.in.b_left, d);
@@ -155,48 +202,7 @@ __global__ __launch_bounds__(THREADS) void f32_window_kernel(F32Params p) {
             layer_norm_rows<D>(X, N, L.g2, L.be2, p.eps);
             __syncthreads();
         }
-    }
-
-    // readout (App. A.3): 2x2 valid convolution + ReLU, mean over columns, linear
-    LayerPtrs L;
-    const float* Wc = layer_ptrs(p.w, D, F, p.L - 1, L);
-    const float* bc = Wc + 4 * (size_t)D * D;
-    const float* wo = bc + D;
-    const float bo = wo[(size_t)d * D];
-    const float* beta = wo + (size_t)d * D + 1;
-    const int gw = d + 1;
-    float part = 0.f;
-    for (int idx = threadIdx.x; idx < d * D; idx += THREADS) {
-        const int i = idx / D, o = idx % D;
-        float pool = 0.f;
-        for (int j = 0; j < d; ++j) {
-            float acc = bc[o];
-            for (int a = 0; a < 2; ++a)
-                for (int b = 0; b < 2; ++b) {
-                    const int tok = p.cell_token[(i + a) * gw + (j + b)];
-                    if (tok < 0) continue;
-                    acc += dot_col<D>(X + tok * D, Wc + (size_t)(a * 2 + b) * D * D, D, o);
-                }
-            pool += fmaxf(acc, 0.f);
-        }
-        part = fmaf(wo[idx], pool / (float)d, part);
-    }
-    red[threadIdx.x] = part;
-    __syncthreads();
-    for (int n = THREADS / 2; n > 0; n >>= 1) {
-        if ((int)threadIdx.x < n) red[threadIdx.x] += red[threadIdx.x + n];
-        __syncthreads();
-    }
-    if (threadIdx.x == 0) {
-        if (type > WIN_FINAL) {
-            p.logits[win] = __builtin_nanf("");
-            p.bits[win] = 0;
-            atomicOr(p.err, 1);
-        } else {
-            const float logit = red[0] + bo + beta[type];
-            p.logits[win] = logit;
-            p.bits[win] = logit > 0.f ? 1 : 0;
-        }
+        if (t >= p.in.W - p.readouts) readout(t - (p.in.W - p.readouts));
     }
 }
 

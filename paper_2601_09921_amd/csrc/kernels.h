@@ -30,6 +30,7 @@ struct TokParams {
     const uint16_t* qkv_stream;    // Q/K/V projection of the layer that follows
     const float* post_vecs;   // POST layer vectors [b_o g1 be1 b2 g2 be2 | b1], 10 D floats
     const float* bqkv;                                  // [3D] bias of the Q/K/V projection
+    uint16_t* state_out;    // POST|EMBED: if not null, D_t (before the fold) as bf16 C fragments
 };
 
 struct AttnParams {
@@ -39,10 +40,12 @@ struct AttnParams {
 };
 
 struct ReadoutParams {
-    const float* X;         // final state, C fragments
+    const float* X;         // decoder state, fp32 C fragments [tb][D/16][64][4] ...
+    const uint16_t* Xb;     // ... or, when not null, the same layout in bf16
     const uint8_t* types;
-    float* logits;
-    uint8_t* bits;
+    float* logits;          // logits[win * stride]
+    uint8_t* bits;          // bits[win * stride]
+    int stride;
     int* err;               // device error word
     const uint16_t* Wc;     // bf16 A fragments of Wc^T: [D/16][4D/32][64][8], k = tap*D + in
     const float* bc;        // [D]
@@ -64,10 +67,11 @@ struct F32Params {
     const float* w;         // blob tensors in blob order (fp32)
     const float* S0;        // b_e + PE per token [N][D]
     const int* cell_token;  // [(d+1)*(d+1)]
-    float* logits;
+    float* logits;          // logits[win * readouts + k] after round W - readouts + k
     uint8_t* bits;
     int* err;
     int D, L, H, F;
+    int readouts;           // readouts after the last `readouts` rounds (1: final state only)
     float kappa, eps;
 };
 

@@ -463,8 +463,10 @@ static SyndromeIn syndrome_in(const pwd_decoder* dec, const uint32_t* meas, cons
     return in;
 }
 
-int decode_windows(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_types, int64_t n,
-                   float* d_logits, uint8_t* d_bits, void* hip_stream) {
+// decode_windows with `readouts` readouts after the last `readouts` rounds (1: the inference
+// branch; distance: the recurrent branch), written to d_logits[win * readouts + k].
+static int decode_impl(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_types, int64_t n,
+                       float* d_logits, uint8_t* d_bits, void* hip_stream, int readouts) {
     if (!dec) return fail(PWD_EINVAL, "null decoder");
     if (n < 0) return fail(PWD_EINVAL, "negative n_windows");
     if (n > dec->max_windows) return fail(PWD_EBATCH, "n_windows %lld > max_windows %d", (long long)n, dec->max_windows);
@@ -485,6 +487,7 @@ int decode_windows(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_ty
         p.bits = d_bits;
         p.err = dec->err;
         p.D = dec->D; p.L = dec->L; p.H = dec->H; p.F = dec->F;
+        p.readouts = readouts;
         p.kappa = dec->kappa; p.eps = dec->eps;
         HIP_OK(timed(dec, PWD_STAGE_FP32_WINDOW, s, [&] { return launch_f32_window(p, s); }));
         return PWD_OK;
@@ -521,31 +524,10 @@ int decode_windows(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_ty
     ap.nbw = dec->nbw;
     ap.H = dec->H;
 
-    // round 0: embed (state D_0 = 0) and project layer 0
-    tp.t = 0;
-    set_qkv(0);
-    HIP_OK(timed(dec, PWD_STAGE_EMBED_QKV, s, [&] { return launch_tok(dec->D, TOK_EMBED | TOK_QKV, tp, n_tb, s); }));
-    for (int t = 0; t < dec->W; ++t) {
-        for (int l = 0; l < dec->L; ++l) {
-            HIP_OK(timed(dec, PWD_STAGE_ATTENTION, s, [&] { return launch_attn(dec->dh, ap, (int)n, s); }));
-            set_post(l);
-            if (l + 1 < dec->L) {
-                set_qkv(l + 1);
-                HIP_OK(timed(dec, PWD_STAGE_POST_QKV, s, [&] { return launch_tok(dec->D, TOK_POST | TOK_QKV, tp, n_tb, s); }));
-            } else if (t + 1 < dec->W) {
-                tp.t = t + 1;          // fold the next round's embedding into D_t
-                set_qkv(0);
-                HIP_OK(timed(dec, PWD_STAGE_POST_EMBED_QKV, s, [&] { return launch_tok(dec->D, TOK_POST | TOK_EMBED | TOK_QKV, tp, n_tb, s); }));
-            } else {
-                HIP_OK(timed(dec, PWD_STAGE_POST, s, [&] { return launch_tok(dec->D, TOK_POST, tp, n_tb, s); }));
-            }
-        }
-    }
     ReadoutParams rp;
     rp.X = dec->X;
+    rp.Xb = nullptr;
     rp.types = d_types;
-    rp.logits = d_logits;
-    rp.bits = d_bits;
     rp.err = dec->err;
     rp.Wc = dec->Wc;
     rp.bc = dec->bc;
@@ -557,8 +539,54 @@ int decode_windows(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_ty
     rp.d = dec->d;
     rp.D = dec->D;
     rp.nbw = dec->nbw;
-    HIP_OK(timed(dec, PWD_STAGE_READOUT, s, [&] { return launch_readout(rp, s); }));
+    rp.stride = readouts;
+    // readout of D_t into output slot k; `state` is null for the fp32 final state in X, else
+    // the bf16 copy of D_t
+    auto readout = [&](int k, const uint16_t* state) {
+        rp.Xb = state;
+        rp.logits = d_logits + k;
+        rp.bits = d_bits + k;
+        return timed(dec, PWD_STAGE_READOUT, s, [&] { return launch_readout(rp, s); });
+    };
+
+    // round 0: embed (state D_0 = 0) and project layer 0
+    tp.t = 0;
+    set_qkv(0);
+    HIP_OK(timed(dec, PWD_STAGE_EMBED_QKV, s, [&] { return launch_tok(dec->D, TOK_EMBED | TOK_QKV, tp, n_tb, s); }));
+    for (int t = 0; t < dec->W; ++t) {
+        const bool read_t = t >= dec->W - readouts;
+        for (int l = 0; l < dec->L; ++l) {
+            HIP_OK(timed(dec, PWD_STAGE_ATTENTION, s, [&] { return launch_attn(dec->dh, ap, (int)n, s); }));
+            set_post(l);
+            if (l + 1 < dec->L) {
+                set_qkv(l + 1);
+                HIP_OK(timed(dec, PWD_STAGE_POST_QKV, s, [&] { return launch_tok(dec->D, TOK_POST | TOK_QKV, tp, n_tb, s); }));
+            } else if (t + 1 < dec->W) {
+                tp.t = t + 1;          // fold the next round's embedding into D_t
+                set_qkv(0);
+                // D_t for a readout goes to the Y buffer: each workgroup has read its own Y
+                // tiles by then, and the next writer of Y is the next round's attention
+                tp.state_out = read_t ? dec->Y : nullptr;
+                HIP_OK(timed(dec, PWD_STAGE_POST_EMBED_QKV, s, [&] { return launch_tok(dec->D, TOK_POST | TOK_EMBED | TOK_QKV, tp, n_tb, s); }));
+                tp.state_out = nullptr;
+                if (read_t) HIP_OK(readout(t - (dec->W - readouts), dec->Y));
+            } else {
+                HIP_OK(timed(dec, PWD_STAGE_POST, s, [&] { return launch_tok(dec->D, TOK_POST, tp, n_tb, s); }));
+            }
+        }
+    }
+    HIP_OK(readout(readouts - 1, nullptr));
     return PWD_OK;
+}
+
+int decode_windows(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_types, int64_t n,
+                   float* d_logits, uint8_t* d_bits, void* hip_stream) {
+    return decode_impl(dec, d_meas, d_types, n, d_logits, d_bits, hip_stream, 1);
+}
+
+int decode_windows_recurrent(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_types, int64_t n,
+                             float* d_logits, uint8_t* d_bits, void* hip_stream) {
+    return decode_impl(dec, d_meas, d_types, n, d_logits, d_bits, hip_stream, dec ? dec->d : 1);
 }
 
 int decoder_detection_events(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_types,

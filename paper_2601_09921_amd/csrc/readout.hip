@@ -58,12 +58,27 @@ __global__ __launch_bounds__(RWAVES * 64) void readout_kernel(ReadoutParams p) {
             for (int b = 0; b < RB; ++b) {
                 const int T = tok[b][t];
                 f32x4 lo = {0.f, 0.f, 0.f, 0.f}, hi = lo;
-                if (T >= 0) {
-                    const float* src = p.X + ((tb_base + (T >> 4)) * RT + 2 * s) * 256 + (g * 16 + (T & 15)) * 4;
-                    lo = ld4g(src);
-                    hi = ld4g(src + 256);
+                if (p.Xb) {   // bf16 state: the rounded values the fp32 branch computes
+                    u16x8 v = {0, 0, 0, 0, 0, 0, 0, 0};
+                    if (T >= 0) {
+                        const uint16_t* src = p.Xb + ((tb_base + (T >> 4)) * RT + 2 * s) * 256 + (g * 16 + (T & 15)) * 4;
+                        const u16x4 l4 = *reinterpret_cast<const u16x4*>(src);
+                        const u16x4 h4 = *reinterpret_cast<const u16x4*>(src + 256);
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            v[i] = l4[i];
+                            v[4 + i] = h4[i];
+                        }
+                    }
+                    gb[b] = __builtin_bit_cast(bf16x8, v);
+                } else {
+                    if (T >= 0) {
+                        const float* src = p.X + ((tb_base + (T >> 4)) * RT + 2 * s) * 256 + (g * 16 + (T & 15)) * 4;
+                        lo = ld4g(src);
+                        hi = ld4g(src + 256);
+                    }
+                    gb[b] = pack_b(lo, hi);
                 }
-                gb[b] = pack_b(lo, hi);
             }
 #pragma unroll
             for (int rt = 0; rt < RT; ++rt) {
@@ -98,14 +113,15 @@ __global__ __launch_bounds__(RWAVES * 64) void readout_kernel(ReadoutParams p) {
 #pragma unroll
         for (int w = 0; w < RWAVES; ++w) tot += red[w];
         const int type = p.types[win];
+        const int64_t o = (int64_t)win * p.stride;
         if (type > WIN_FINAL) {
-            p.logits[win] = __builtin_nanf("");
-            p.bits[win] = 0;
+            p.logits[o] = __builtin_nanf("");
+            p.bits[o] = 0;
             atomicOr(p.err, 1);
         } else {
             const float logit = tot + p.bo + p.beta[type];
-            p.logits[win] = logit;
-            p.bits[win] = logit > 0.f ? 1 : 0;
+            p.logits[o] = logit;
+            p.bits[o] = logit > 0.f ? 1 : 0;
         }
     }
 }

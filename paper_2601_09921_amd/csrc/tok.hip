@@ -477,6 +477,17 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 1) void tok_kernel(To
         layer_norm<RT, TB>(x, vec + V::G2, vec + V::BE2, p.eps, g);
     }
 
+    if constexpr (POST && (FLAGS & TOK_EMBED) != 0) {
+        // the state D_t itself, for a readout of this round (bf16, the readout's operand type)
+        if (p.state_out) {
+#pragma unroll
+            for (int b = 0; b < TB; ++b)
+#pragma unroll
+                for (int rt = 0; rt < RT; ++rt)
+                    st_stream(reinterpret_cast<u16x4*>(p.state_out + (((tb0 + b) * RT + rt) * 64 + lane) * 4),
+                              to_bf16x4(x[rt][b]));
+        }
+    }
     if constexpr ((FLAGS & TOK_EMBED) != 0) {
         // ---- embedding of round t folded into the state: X = kappa (S_t + X)
 #pragma unroll

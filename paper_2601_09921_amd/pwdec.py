@@ -65,6 +65,7 @@ def load_library() -> ctypes.CDLL:
         "decoder_validate_config": (ctypes.c_int, [P(Geometry), P(ModelDims)]),
         "decoder_create": (ctypes.c_int, [P(Geometry), P(ModelDims), ctypes.c_void_p, ctypes.c_size_t, P(VP)]),
         "decode_windows": (ctypes.c_int, [VP, VP, VP, I64, VP, VP, VP]),
+        "decode_windows_recurrent": (ctypes.c_int, [VP, VP, VP, I64, VP, VP, VP]),
         "decoder_detection_events": (ctypes.c_int, [VP, VP, VP, I64, VP, VP]),
         "decode_stream": (ctypes.c_int, [VP, VP, I64, VP, VP, VP, VP, VP]),
         "decoder_sync_status": (ctypes.c_int, [VP, VP]),
@@ -151,6 +152,15 @@ class Decoder:
                                         ctypes.c_void_p(types.data_ptr()), n,
                                         ctypes.c_void_p(logits.data_ptr()), ctypes.c_void_p(bits.data_ptr()),
                                         _stream_ptr(stream)))
+
+    def decode_recurrent(self, meas, types, logits, bits, stream=None):
+        """As decode, with outputs float32 / uint8 [n][distance]: a readout after each of the
+        last `distance` rounds (the recurrent branch of Algorithm 1)."""
+        n = types.shape[0]
+        _check(self._lib.decode_windows_recurrent(self._h, ctypes.c_void_p(meas.data_ptr()),
+                                                  ctypes.c_void_p(types.data_ptr()), n,
+                                                  ctypes.c_void_p(logits.data_ptr()),
+                                                  ctypes.c_void_p(bits.data_ptr()), _stream_ptr(stream)))
 
     def decode_stream(self, rounds, bit, prob=None, window_logits=None, window_bits=None, stream=None):
         """rounds: int32/uint32 [T][words] cuda tensor of packed measurement rounds; bit: uint8 [1]

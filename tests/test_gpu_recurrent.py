@@ -1,0 +1,54 @@
+"""GPU parity of decode_windows_recurrent, the recurrent branch of Algorithm 1 (a readout after
+each of the last `distance` rounds), against the oracle's forward_windows_recurrent: fp32
+(d3), bf16 with d_model 128 (d7) and 256 (d11), small seeded batches of all window types."""
+import numpy as np
+import pytest
+
+from gpu_helpers import BF16_ATOL, FP32_ATOL, FP32_RTOL, gpu_decode, say, to_device, weights
+from oracle import decoder as O
+from paper_2601_09921_amd import pwdec, synth
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def gpu_recurrent(dec, meas, types, d):
+    meas_t, types_t = to_device(meas, types)
+    n = types.shape[0]
+    logits = torch.full((n, d), float("nan"), dtype=torch.float32, device="cuda")
+    bits = torch.full((n, d), 7, dtype=torch.uint8, device="cuda")
+    dec.decode_recurrent(meas_t, types_t, logits, bits)
+    torch.cuda.synchronize()
+    return logits.cpu().numpy(), bits.cpu().numpy(), dec.sync_status()
+
+
+@pytest.mark.parametrize("name,B", [("d3", 9), ("d7", 6), ("d11", 3)])
+def test_recurrent_parity(name, B):
+    wl = synth.WORKLOADS[name]
+    w = weights(name)
+    meas, types = synth.make_windows(wl, B=B, seed=4242)
+    say(f"recurrent {name} B={B}")
+    dec = pwdec.Decoder.from_workload(wl, w, max_windows=B)
+    gl, gb, rc = gpu_recurrent(dec, meas, types, wl.d)
+    assert rc == pwdec.PWD_OK
+    ol, _ = O.forward_windows_recurrent(meas, types, w, wl.d, wl.H)
+    assert gl.shape == ol.shape and np.isfinite(gl).all()
+    bound = FP32_RTOL * np.abs(ol) + FP32_ATOL if wl.dtype == synth.DTYPE_F32 else np.full_like(ol, BF16_ATOL)
+    err = np.abs(gl - ol)
+    say(f"  max |gpu - oracle| = {err.max():.3e}")
+    assert (err <= bound).all(), (gl, ol)
+    assert np.array_equal(gb, (gl > 0).astype(np.uint8))
+    # the last readout is the inference branch, computed by the same kernels
+    fl, _, rc = gpu_decode(dec, meas, types)
+    assert rc == pwdec.PWD_OK
+    assert np.array_equal(gl[:, -1].view(np.uint32), fl.view(np.uint32))
+    # a sub-batch gives the same rows, bit for bit
+    sl, _, _ = gpu_recurrent(dec, meas[1:], types[1:], wl.d)
+    assert np.array_equal(sl.view(np.uint32), gl[1:].view(np.uint32))
+    dec.close()
