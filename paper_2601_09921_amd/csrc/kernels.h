@@ -29,7 +29,7 @@ struct TokParams {
     const uint16_t* post_stream;   // out-projection + feed-forward of the POST layer
     const uint16_t* qkv_stream;    // Q/K/V projection of the layer that follows
     const float* post_vecs;   // POST layer vectors [b_o g1 be1 b2 g2 be2 | b1], 10 D floats
-    const float* bqkv;                                  // [3D] bias of the Q/K/V projection
+    const float* bqkv;      // [6D] bias of the Q/K/V projection: b_q, b_k, then b_v with each value x 4
     uint16_t* state_out;    // POST|EMBED: if not null, D_t (before the fold) as bf16 C fragments
 };
 

@@ -143,7 +143,7 @@ struct pwd_decoder {
     // views into `weights`
     struct Layer {
         const uint16_t *post, *qkv;
-        const float *post_vecs, *bqkv;   // [b_o g1 be1 b2 g2 be2 | b1] (10 D) and [b_q b_k b_v]
+        const float *post_vecs, *bqkv;   // [b_o g1 be1 b2 g2 be2 | b1] (10 D) and [b_q b_k | b_v x 4] (6 D)
     };
     std::vector<Layer> layers;
     const float* S0 = nullptr;
@@ -328,7 +328,7 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
             const float *Wq = p, *bq = Wq + D * D, *Wk = bq + D, *bk = Wk + D * D, *Wv = bk + D, *bv = Wv + D * D;
             const float *Wo = bv + D, *bo = Wo + D * D, *g1 = bo + D, *be1 = g1 + D, *W1 = be1 + D;
             const float *b1 = W1 + (size_t)D * F, *W2 = b1 + F, *b2 = W2 + (size_t)F * D, *g2 = b2 + D, *be2 = g2 + D;
-            std::vector<float> wqkv((size_t)D * 3 * D), bqkv(3 * D);
+            std::vector<float> wqkv((size_t)D * 3 * D), bqkv(6 * D);
             for (int k = 0; k < D; ++k)
                 for (int o = 0; o < D; ++o) {
                     wqkv[(size_t)k * 3 * D + o] = Wq[k * D + o];
@@ -338,7 +338,7 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
             for (int o = 0; o < D; ++o) {
                 bqkv[o] = bq[o];
                 bqkv[D + o] = bk[o];
-                bqkv[2 * D + o] = bv[o];
+                for (int r = 0; r < 4; ++r) bqkv[2 * D + 4 * o + r] = bv[o];
             }
             std::vector<uint16_t> fr;
             append_post_stream(fr, Wo, W1, W2, D, tok_mlp_chunk(D));
@@ -350,7 +350,7 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
             for (const float* v : {bo, g1, be1, b2, g2, be2}) pv.insert(pv.end(), v, v + D);
             pv.insert(pv.end(), b1, b1 + F);
             loff[l].post_vecs = put(pv.data(), pv.size() * 4);
-            loff[l].bqkv = put(bqkv.data(), 3 * D * 4);
+            loff[l].bqkv = put(bqkv.data(), 6 * D * 4);
         }
         {
             std::vector<uint16_t> fr;

@@ -289,7 +289,9 @@ PWD_DEV void layer_norm(f32x4 (&x)[RT][TB], const float* gamma, const float* bet
 template <int D>
 struct Vecs {
     static constexpr int BO = 0, G1 = D, BE1 = 2 * D, B2 = 3 * D, G2 = 4 * D, BE2 = 5 * D;
-    static constexpr int B1 = 6 * D, BQKV = 10 * D, SIZE = 13 * D;
+    // [b_q b_k] then b_v with each value four times (the bias of a V tile is one column value
+    // per lane, loaded as the f32x4 an accumulator starts from)
+    static constexpr int B1 = 6 * D, BQKV = 10 * D, BV4 = 12 * D, QKV_VECS = 6 * D, SIZE = 16 * D;
 };
 
 // Global stores a wavefront issues in one Q/K/V chunk after its last load of the next
@@ -362,8 +364,8 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 1) void tok_kernel(To
     // first chunk's sync awaits and publishes them.
     __shared__ __align__(16) float vec[V::SIZE];
     {
-        constexpr int NP_V = POST ? V::BQKV / 64 : 0, NQ_V = QKV ? 3 * D / 64 : 0;
-        static_assert(V::BQKV % 64 == 0 && (3 * D) % 64 == 0, "whole 256-byte pieces");
+        constexpr int NP_V = POST ? V::BQKV / 64 : 0, NQ_V = QKV ? V::QKV_VECS / 64 : 0;
+        static_assert(V::BQKV % 64 == 0 && V::QKV_VECS % 64 == 0, "whole 256-byte pieces");
         for (int k = pipe.wave; k < NP_V + NQ_V; k += WAVES) {
             const float* src = k < NP_V ? p.post_vecs + k * 64 : p.bqkv + (k - NP_V) * 64;
             const int dst = k < NP_V ? k * 64 : V::BQKV + (k - NP_V) * 64;
@@ -560,9 +562,10 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 1) void tok_kernel(To
             for (int o2 = 0; o2 < OPC; ++o2)
 #pragma unroll
                 for (int hh = 0; hh < 2; ++hh) {
-                    if constexpr (VOUT) {   // bias (along the tile's columns) added at the store
+                    if constexpr (VOUT) {   // bias along the tile's columns: lane col's value x 4
+                        const f32x4 bias = ld4(vec + V::BV4 + ((qc * OPC + o2 - 2 * KS) * 32 + hh * 16 + col) * 4);
 #pragma unroll
-                        for (int b = 0; b < TB; ++b) q[o2][hh][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+                        for (int b = 0; b < TB; ++b) q[o2][hh][b] = bias;
                     } else {
                         const f32x4 bias = ld4(vec + V::BQKV + (qc * OPC + o2) * 32 + hh * 16 + 4 * g);
 #pragma unroll
@@ -587,10 +590,8 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 1) void tok_kernel(To
                             if constexpr (VOUT) {
                                 uint16_t* t = p.QKV + ((tb0 + b) * (3 * KS) + og) * FRAG + lane * 4;
 #pragma unroll
-                                for (int h2 = 0; h2 < 2; ++h2) {
-                                    const float bias = vec[V::BQKV + og * 32 + h2 * 16 + col];
-                                    st_stream(reinterpret_cast<u16x4*>(t + h2 * (FRAG / 2)), to_bf16x4(q[o2][h2][b] + bias));
-                                }
+                                for (int h2 = 0; h2 < 2; ++h2)
+                                    st_stream(reinterpret_cast<u16x4*>(t + h2 * (FRAG / 2)), to_bf16x4(q[o2][h2][b]));
                             } else {
                                 const float sc = og < KS ? p.qscale : 1.0f;   // Q: log2(e)/sqrt(dh)
                                 stfrag(p.QKV, (tb0 + b) * (3 * KS) + og, lane,
