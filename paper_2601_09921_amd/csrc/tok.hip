@@ -31,11 +31,11 @@ namespace {
 constexpr int MAX_CHUNK = 64;   // weight fragments (1 KB each) per LDS chunk, at most
 constexpr int FRAG = 512;       // bf16 values per fragment
 
-// Two 16-token blocks per wavefront, and per workgroup 8 wavefronts (two per SIMD, so one
-// hides the other's latencies; 16 blocks share each streamed weight chunk) where the
-// registers fit 256 per wavefront, else 4 (the variant that also embeds at D = 256).
+// Two 16-token blocks per wavefront; at D = 256 8 wavefronts per workgroup (two per SIMD, so
+// one hides the other's latencies, and 16 blocks share each streamed weight chunk), at
+// D = 128 (half the registers) 4 and two workgroups per CU.
 template <int D, int FLAGS>
-constexpr int tok_waves() { return (D == 256 && (FLAGS & TOK_EMBED) == 0) ? 8 : 4; }
+constexpr int tok_waves() { return D == 256 ? 8 : 4; }
 constexpr int TB = 2;
 
 template <int D, int NW>
@@ -359,6 +359,25 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 1) void tok_kernel(To
     }
     pipe.template issue<0>(0);
 
+    // detection events of round t for this lane's token of each block (EMBED), computed while
+    // few registers are live
+    float ev[TB];
+    if constexpr ((FLAGS & TOK_EMBED) != 0) {
+#pragma unroll
+        for (int b = 0; b < TB; ++b) {
+            const int64_t tb = tb0 + b;
+            const int64_t w = tb / p.nbw;
+            const int s = (int)(tb - w * p.nbw) * 16 + col;
+            ev[b] = 0.f;
+            if (w < p.in.nwin && s < p.in.N) {
+                const uint32_t* m = p.in.meas + w * (int64_t)(p.in.W + 1) * p.in.words;
+                const uint32_t word = event_word(m, p.in.words, p.t, s >> 5, p.in.types[w],
+                                                 p.in.b_left, p.in.d);
+                ev[b] = (float)((word >> (s & 31)) & 1u);
+            }
+        }
+    }
+
     // Per-launch vectors, staged in LDS by direct loads of 256 bytes (64 lanes x 4 bytes):
     // vec[0, 10 D) from the POST layer's vector table, vec[10 D, 13 D) the Q/K/V biases. The
     // first chunk's sync awaits and publishes them.
@@ -495,17 +514,9 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 1) void tok_kernel(To
 #pragma unroll
         for (int b = 0; b < TB; ++b) {
             const int64_t tb = tb0 + b;
-            const int64_t w = tb / p.nbw;
-            const int blk = (int)(tb - w * p.nbw);
-            const int s = blk * 16 + col;
-            float e = 0.f;
-            if (w < p.in.nwin && s < p.in.N) {
-                const uint32_t* m = p.in.meas + w * (int64_t)(p.in.W + 1) * p.in.words;
-                const uint32_t word = event_word(m, p.in.words, p.t, s >> 5, p.in.types[w],
-                                                 p.in.b_left, p.in.d);
-                e = (float)((word >> (s & 31)) & 1u);
-            }
-            const bool real = s < p.in.N;
+            const int blk = (int)(tb % p.nbw);
+            const bool real = blk * 16 + col < p.in.N;
+            const float e = ev[b];
 #pragma unroll
             for (int rt = 0; rt < RT; ++rt) {
                 const f32x4 s0 = ld4(p.S0 + (((int64_t)blk * RT + rt) * 64 + lane) * 4);
