@@ -31,16 +31,17 @@ namespace {
 constexpr int MAX_CHUNK = 64;   // weight fragments (1 KB each) per LDS chunk, at most
 constexpr int FRAG = 512;       // bf16 values per fragment
 
-// Two 16-token blocks per wavefront; at D = 256 8 wavefronts per workgroup (two per SIMD, so
-// one hides the other's latencies, and 16 blocks share each streamed weight chunk), at
-// D = 128 (half the registers) 4 and two workgroups per CU.
+// Two 16-token blocks per wavefront and 4 wavefronts per workgroup, within 256 registers and
+// 80 KB of LDS so that two workgroups share a CU: each SIMD runs two wavefronts, and one
+// workgroup's activation loads, chunk barriers and stores overlap the other's MFMAs. (One
+// 8-wavefront workgroup per CU, sharing one weight stream, measured 3-6 % slower.)
 template <int D, int FLAGS>
-constexpr int tok_waves() { return D == 256 ? 8 : 4; }
+constexpr int tok_waves() { return 4; }
 constexpr int TB = 2;
 
 template <int D, int NW>
 struct Shape {
-    static constexpr int CHUNK = (D == 256 && NW == 4) ? 64 : 32;  // weight fragments per LDS chunk
+    static constexpr int CHUNK = 32;                  // weight fragments per LDS chunk
     static constexpr int RT = D / 16;                 // 16-row C tiles of a D-vector
     static constexpr int KS = D / 32;                 // 32-deep k-steps of a D-vector
     static constexpr int F = 4 * D;
@@ -126,15 +127,16 @@ PWD_DEV void sched_pairs(std::integer_sequence<int, K...>) {
     (pair(std::integral_constant<int, K>{}), ...);
 }
 
-// Look-ahead of the fragment reads (fragments in flight ahead of the MFMAs that use them).
+// Look-ahead of the fragment reads (fragments in flight ahead of the MFMAs that use them);
+// with two wavefronts per SIMD a short ring suffices and keeps within 256 registers.
 #ifndef TOK_LA_WO
-#define TOK_LA_WO 6
+#define TOK_LA_WO 4
 #endif
 #ifndef TOK_LA_MLP
-#define TOK_LA_MLP 6
+#define TOK_LA_MLP 4
 #endif
 #ifndef TOK_LA_QKV
-#define TOK_LA_QKV 6
+#define TOK_LA_QKV 4
 #endif
 // Spacing, in fragment reads, of the next chunk's loads (0: spread over the whole chunk).
 #ifndef TOK_DMA_SP
@@ -315,14 +317,10 @@ template <int N, typename F>
 PWD_DEV void static_for(const F& f) { static_for_impl(f, std::make_integer_sequence<int, N>{}); }
 
 template <int D, int FLAGS>
-__global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 1) void tok_kernel(TokParams p) {
+__global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(TokParams p) {
     constexpr int WAVES = tok_waves<D, FLAGS>();
     using S = Shape<D, WAVES>;
-    // fragment-read look-ahead per phase: with two wavefronts per SIMD a shorter ring suffices
-    // and keeps the kernel within 256 registers
-    constexpr int LA_WO = WAVES == 8 ? 4 : TOK_LA_WO;
-    constexpr int LA_MLP = WAVES == 8 ? 4 : TOK_LA_MLP;
-    constexpr int LA_QKV = WAVES == 8 ? 4 : TOK_LA_QKV;
+    constexpr int LA_WO = TOK_LA_WO, LA_MLP = TOK_LA_MLP, LA_QKV = TOK_LA_QKV;
     using V = Vecs<D>;
     constexpr int RT = S::RT, KS = S::KS, CH = S::CH;
     constexpr bool POST = (FLAGS & TOK_POST) != 0, QKV = (FLAGS & TOK_QKV) != 0;
