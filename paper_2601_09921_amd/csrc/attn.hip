@@ -162,6 +162,19 @@ PWD_DEV float kmax2_blocks(const AttnShape& sh, const uint16_t* ks, int slot0, i
     return kmax2;
 }
 
+// Scheduling request for one iteration of the key loop (two superblocks, 20 QB MFMAs): each
+// MFMA followed by three VALU or transcendental instructions, so the exponentials and packs
+// issue while the matrix core runs instead of in separate bursts (measured: 3 per MFMA beats
+// 2 and 4).
+template <int NMFMA>
+PWD_DEV void interleave_mfma_valu() {
+#pragma unroll
+    for (int i = 0; i < NMFMA; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x402, 3, 0);   // VALU or TRANS
+    }
+}
+
 // One pass of a wavefront: query blocks qb0 .. qb0 + QB - 1 (those >= qend are computed
 // from a repeated block and not stored) against every key of the item.
 template <int DH, int QB>
@@ -258,6 +271,7 @@ PWD_DEV void attn_pass(const AttnShape& sh, const AttnItem& it, int qb0, int qen
         load_k(min(sb + 3, lastsb), kB);
         load_v(min(sb + 2, lastsb), vA);
         accumulate(sB, vB);                          // sb + 1
+        interleave_mfma_valu<10 * QB>();
     }
     if (sb < nfull) accumulate(sA, vA);
     {   // last superblock: missing key block and padding keys are -inf
