@@ -3,6 +3,9 @@
 Small batches (several token tiles and a ragged tail) compare every window; at the full
 batch sizes of each workload, windows the oracle can afford are compared one by one and
 the rest are checked through batch invariance and output consistency."""
+import copy
+import math
+
 import numpy as np
 import pytest
 
@@ -143,3 +146,58 @@ def test_full_batch_sampled(name):
     for w in (B // 3 + 1, B - 1):
         one, _, _ = gpu_decode(dec, meas[w:w + 1], types[w:w + 1])
         assert one.view(np.uint32)[0] == logits.view(np.uint32)[w], f"window {w}"
+
+
+def orthogonal_qk_weights(name, scale=12.0):
+    """Weights whose Q and K of every head live in disjoint halves of the head's features (Q
+    in the first, K in the second, biases included), scaled up: every attention score is
+    exactly 0 while |q'| max|k| is hundreds of log2 units."""
+    wl = synth.WORKLOADS[name]
+    w = copy.deepcopy(weights(name))
+    dh = wl.D // wl.H
+    for lw in w["layers"]:
+        Wq, Wk, bq, bk = lw["Wq"] * scale, lw["Wk"] * scale, lw["bq"].copy(), lw["bk"].copy()
+        for h in range(wl.H):
+            first, second = slice(h * dh, h * dh + dh // 2), slice(h * dh + dh // 2, (h + 1) * dh)
+            Wq[:, second], bq[second] = 0.0, 0.0
+            Wk[:, first], bk[first] = 0.0, 0.0
+        lw["Wq"], lw["Wk"] = synth.round_bf16(Wq), synth.round_bf16(Wk)
+        lw["bq"], lw["bk"] = synth.round_bf16(bq), synth.round_bf16(bk)
+    return w
+
+
+@pytest.mark.parametrize("name", ["d7", "d11"])
+def test_attention_shift_underflow(name):
+    """The attention kernel shifts each query's scores by the Cauchy-Schwarz bound
+    |q'| max_k |k| and recomputes a query block with a running maximum when a row sum
+    underflows. With Q and K in orthogonal feature halves every score is 0, so softmax is
+    uniform, while the bound is far above 100 log2 units: every row sum underflows in fp32
+    (checked below for round 0, layer 0) and the results can only match the oracle through
+    the running-maximum path (dh = 16 for d7, 32 for d11)."""
+    wl = synth.WORKLOADS[name]
+    B = 5
+    w = orthogonal_qk_weights(name)
+    meas, types = inputs(name, B)
+    # the bound on round 0, layer 0: X = kappa * Embed(E_0)
+    ev = O.detection_events(meas, types, wl.d)
+    pe = O.positional_encoding((wl.d + 1) ** 2, wl.D)[O.grid_positions(wl.d)]
+    X = w["kappa"] * O.embed(ev[:, 0, :], w, pe)
+    lw = w["layers"][0]
+    dh = wl.D // wl.H
+    Q, K = X @ lw["Wq"] + lw["bq"], X @ lw["Wk"] + lw["bk"]
+    for h in range(wl.H):
+        sl = slice(h * dh, (h + 1) * dh)
+        qn = np.linalg.norm(Q[:, :, sl], axis=-1) * math.log2(math.e) / math.sqrt(dh)
+        kmax = np.linalg.norm(K[:, :, sl], axis=-1).max(axis=1, keepdims=True)
+        assert np.abs(np.einsum("bnd,bmd->bnm", Q[:, :, sl], K[:, :, sl])).max() == 0.0
+        # every row: N * 2^(-bound) < 1e-30, the kernel's underflow test
+        assert (qn * kmax).min() > 100 + math.log2(wl.N), (h, (qn * kmax).min())
+    say(f"shift underflow {name} B={B}")
+    dec = pwdec.Decoder.from_workload(wl, w, max_windows=B)
+    logits, bits, rc = gpu_decode(dec, meas, types)
+    dec.close()
+    assert rc == pwdec.PWD_OK
+    assert np.isfinite(logits).all()
+    o_logits, _ = O.forward_windows(meas, types, w, wl.d, wl.H)
+    check_logits(name, logits, o_logits)
+    check_bits(bits, o_logits)
