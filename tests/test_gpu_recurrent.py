@@ -52,3 +52,28 @@ def test_recurrent_parity(name, B):
     sl, _, _ = gpu_recurrent(dec, meas[1:], types[1:], wl.d)
     assert np.array_equal(sl.view(np.uint32), gl[1:].view(np.uint32))
     dec.close()
+
+
+def test_recurrent_full_size_sampled():
+    """The benchmark's d=25 configuration (8192 windows, the launch shapes bench.py times):
+    all d readouts of one window of each type against the oracle, and two windows decoded
+    alone against their rows of the batch, bit for bit."""
+    wl = synth.WORKLOADS["d25"]
+    w = weights("d25")
+    meas, types = synth.make_windows(wl)
+    B = wl.B
+    say(f"recurrent d25 B={B}")
+    dec = pwdec.Decoder.from_workload(wl, w, max_windows=B)
+    gl, gb, rc = gpu_recurrent(dec, meas, types, wl.d)
+    assert rc == pwdec.PWD_OK
+    assert np.isfinite(gl).all() and np.array_equal(gb, (gl > 0).astype(np.uint8))
+    sample = np.array([int(np.flatnonzero(types == t)[0]) for t in (0, 1, 2)])
+    for w_ in (B // 3 + 1, B - 1):
+        one, _, _ = gpu_recurrent(dec, meas[w_:w_ + 1], types[w_:w_ + 1], wl.d)
+        assert np.array_equal(one.view(np.uint32)[0], gl.view(np.uint32)[w_]), f"window {w_}"
+    dec.close()
+    say(f"  oracle on windows {sample.tolist()}")
+    ol, _ = O.forward_windows_recurrent(meas[sample], types[sample], w, wl.d, wl.H)
+    err = np.abs(gl[sample] - ol)
+    say(f"  max |gpu - oracle| = {err.max():.3e}")
+    assert (err <= BF16_ATOL).all(), (gl[sample], ol)
