@@ -15,10 +15,10 @@
 //
 // Weights reach the MFMAs through LDS: the host lays every weight fragment out in the exact
 // order the kernel consumes them (a "weight stream"), and the workgroup pulls the stream
-// through a double-buffered LDS ring in 32 or 64 KB chunks with direct global->LDS loads.
+// through a double-buffered LDS ring in 32 KB chunks with direct global->LDS loads.
 // The loads of chunk i+1 are interleaved with the fragment reads of chunk i, and the reads
 // are software-pipelined in program order (a ring of fragments in flight ahead of the MFMAs).
-// Every fragment read from LDS feeds 2-3 MFMAs of each wavefront (one per 16-token block the
+// Every fragment read from LDS feeds 2 MFMAs of each wavefront (one per 16-token block the
 // wavefront owns). Activations (X, Y, Q/K/V) are streamed with non-temporal accesses.
 #include "common.h"
 #include "kernels.h"
@@ -28,8 +28,7 @@
 
 namespace {
 
-constexpr int MAX_CHUNK = 64;   // weight fragments (1 KB each) per LDS chunk, at most
-constexpr int FRAG = 512;       // bf16 values per fragment
+constexpr int FRAG = 512;       // bf16 values per fragment (1 KB)
 
 // Two 16-token blocks per wavefront and 4 wavefronts per workgroup, within 256 registers and
 // 80 KB of LDS so that two workgroups share a CU: each SIMD runs two wavefronts, and one
@@ -54,7 +53,7 @@ struct Shape {
     static constexpr int OG_PER_CHUNK = CHUNK / (2 * KS);
     static constexpr int POST_CHUNKS = WO_CHUNKS + MLP_CHUNKS;
     static_assert((CH / 16) * KS + RT * (CH / 32) == 32, "32 fragments per feed-forward sub-chunk");
-    static_assert(NMLP % MLP_PER == 0 && CHUNK <= MAX_CHUNK, "whole feed-forward chunks");
+    static_assert(NMLP % MLP_PER == 0, "whole feed-forward chunks");
     static_assert(RT * KS % CHUNK == 0 && (3 * D / 16) * KS % CHUNK == 0, "whole chunks");
 };
 
@@ -101,30 +100,6 @@ PWD_DEV f32x4 relu4(f32x4 v) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) r[i] = v[i] > 0.f ? v[i] : 0.f;
     return r;
-}
-
-// Spacing, in fragment reads, of the NDMA direct-to-LDS loads spread over a chunk of NREAD
-// reads whose first LA reads are issued up front.
-template <int NREAD, int LA, int NDMA>
-constexpr int dma_spacing() { return NDMA > 1 ? (NREAD - 1 - LA) / (NDMA - 1) : 1; }
-
-// Load j of the next chunk follows fragment read LA + j * SP in program order and in the
-// schedule below.
-template <int NREAD, int LA, int NDMA>
-constexpr int dma_after_read(int r) {
-    constexpr int SP = dma_spacing<NREAD, LA, NDMA>();
-    return (r >= LA && (r - LA) % SP == 0 && (r - LA) / SP < NDMA) ? (r - LA) / SP : -1;
-}
-
-template <int MPR, int LA, int SP, int NDMA, int... K>
-PWD_DEV void sched_pairs(std::integer_sequence<int, K...>) {
-    auto pair = [](auto k) {
-        constexpr int kk = decltype(k)::value;
-        __builtin_amdgcn_sched_group_barrier(0x008, MPR, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-        if constexpr (kk % SP == 0 && kk / SP < NDMA) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-    };
-    (pair(std::integral_constant<int, K>{}), ...);
 }
 
 // Look-ahead of the fragment reads (fragments in flight ahead of the MFMAs that use them);
@@ -184,7 +159,6 @@ PWD_DEV void sched_pipeline() {
 // tell that the direct-to-LDS prefetch into one never aliases reads of the other.
 template <int PAR, int CHUNK>
 PWD_DEV uint16_t* wbuf() {
-    static_assert(CHUNK <= MAX_CHUNK, "chunk size");
     __shared__ __align__(16) uint16_t buf[CHUNK * FRAG];   // one object per (buffer, size)
     return buf;
 }
