@@ -13,94 +13,109 @@
 
 namespace {
 
-constexpr int RB = 2;          // 16-position blocks per wavefront pass
 constexpr int RWAVES = 4;
+constexpr int PB = 8;          // 16-position blocks per workgroup pass (128 positions)
 
 PWD_DEV f32x4 ld4g(const float* __restrict__ p) { return *reinterpret_cast<const f32x4*>(p); }
 
 // One workgroup per window. The d x d output positions (data qubits) form 16-wide MFMA
-// column blocks; for each, Y^T = Wc^T G^T over k = 4 taps x D input features, where the B
-// fragment of (tap (a,b), features 32s..32s+31) holds the state of the stabilizer at cell
-// (i+a, j+b) rounded to bf16 (zero where the cell is empty). The A fragments of Wc^T come
-// from L2. Each lane then adds sum_o w_o[i][o] ReLU(Y[o] + b_c[o]) / d over its outputs.
+// column blocks; Y^T = Wc^T G^T over k = 4 taps x D input features, where the B fragment of
+// (tap (a,b), features 32s..32s+31) holds the state of the stabilizer at cell (i+a, j+b)
+// rounded to bf16 (zero where the cell is empty). A pass covers PB position blocks: for each
+// tap the workgroup gathers their B fragments into LDS once, and each wavefront multiplies
+// them by the A fragments (from L2) of its quarter of the output features, so every weight
+// fragment feeds PB MFMAs and every gathered fragment feeds D / 64 of each wavefront. Each
+// lane then adds sum_o w_o[i][o] ReLU(Y[o] + b_c[o]) / d over its outputs; one fixed-order
+// reduction over lanes and wavefronts gives the window's sum.
 template <int D>
-__global__ __launch_bounds__(RWAVES * 64) void readout_kernel(ReadoutParams p) {
+__global__ __launch_bounds__(RWAVES * 64, 2) void readout_kernel(ReadoutParams p) {
     constexpr int RT = D / 16, KSD = D / 32, KS = 4 * KSD;
+    constexpr int RTW = RT / RWAVES;                  // output row tiles per wavefront
+    constexpr int GPB = PB / RWAVES;                  // position blocks gathered per wavefront
+    static_assert(RT % RWAVES == 0 && PB % RWAVES == 0, "whole tiles per wavefront");
     const int win = blockIdx.x;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int g = lane >> 4, col = lane & 15;
     const int d = p.d, gw = d + 1, npos = d * d, npb = (npos + 15) / 16;
     const int64_t tb_base = (int64_t)win * p.nbw;
     const float inv_d = 1.0f / (float)d;
+    __shared__ __align__(16) uint16_t bsm[PB * KSD * 512];   // [PB][KSD] gathered B fragments
     __shared__ float red[RWAVES];
 
-    float part = 0.f;
-    for (int pb0 = wave * RB; pb0 < npb; pb0 += RWAVES * RB) {
-        f32x4 acc[RT][RB];
-        int pos_i[RB], tok[RB][4];
+    // gathered B fragment of token T (-1: empty cell), features 32 s .. 32 s + 31
+    auto gather = [&](int T, int s) -> u16x8 {
+        u16x8 v = {0, 0, 0, 0, 0, 0, 0, 0};
+        if (T < 0) return v;
+        if (p.Xb) {   // bf16 state: the rounded values the fp32 branch computes
+            const uint16_t* src = p.Xb + ((tb_base + (T >> 4)) * RT + 2 * s) * 256 + (g * 16 + (T & 15)) * 4;
+            const u16x4 l4 = *reinterpret_cast<const u16x4*>(src);
+            const u16x4 h4 = *reinterpret_cast<const u16x4*>(src + 256);
 #pragma unroll
-        for (int b = 0; b < RB; ++b) {
-            const int pos = (pb0 + b) * 16 + col;
-            const bool ok = pos < npos && pb0 + b < npb;
-            const int i = ok ? pos / d : 0, j = ok ? pos % d : 0;
-            pos_i[b] = ok ? i : -1;
-#pragma unroll
-            for (int t = 0; t < 4; ++t)
-                tok[b][t] = ok ? p.cell_token[(i + (t >> 1)) * gw + j + (t & 1)] : -1;
-#pragma unroll
-            for (int rt = 0; rt < RT; ++rt) acc[rt][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int i = 0; i < 4; ++i) {
+                v[i] = l4[i];
+                v[4 + i] = h4[i];
+            }
+            return v;
         }
+        const float* src = p.X + ((tb_base + (T >> 4)) * RT + 2 * s) * 256 + (g * 16 + (T & 15)) * 4;
+        return __builtin_bit_cast(u16x8, pack_b(ld4g(src), ld4g(src + 256)));
+    };
+
+    float part = 0.f;
+    for (int pb0 = 0; pb0 < npb; pb0 += PB) {
+        f32x4 acc[RTW][PB];
+#pragma unroll
+        for (int rr = 0; rr < RTW; ++rr)
+#pragma unroll
+            for (int b = 0; b < PB; ++b) acc[rr][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int t = 0; t < 4; ++t) {
+            // this wavefront's GPB position blocks of the pass, every k-step of tap t
+#pragma unroll
+            for (int q = 0; q < GPB; ++q) {
+                const int pbl = wave * GPB + q;
+                const int pos = (pb0 + pbl) * 16 + col;
+                int T = -1;
+                if (pos < npos) {
+                    const int i = pos / d, j = pos % d;
+                    T = p.cell_token[(i + (t >> 1)) * gw + j + (t & 1)];
+                }
+#pragma unroll
+                for (int s = 0; s < KSD; ++s)
+                    *reinterpret_cast<u16x8*>(bsm + ((pbl * KSD + s) * 64 + lane) * 8) = gather(T, s);
+            }
+            __syncthreads();
 #pragma unroll 2
-        for (int ks = 0; ks < KS; ++ks) {
-            const int t = ks / KSD, s = ks % KSD;
-            bf16x8 gb[RB];
+            for (int s = 0; s < KSD; ++s) {
+                bf16x8 a[RTW];
 #pragma unroll
-            for (int b = 0; b < RB; ++b) {
-                const int T = tok[b][t];
-                f32x4 lo = {0.f, 0.f, 0.f, 0.f}, hi = lo;
-                if (p.Xb) {   // bf16 state: the rounded values the fp32 branch computes
-                    u16x8 v = {0, 0, 0, 0, 0, 0, 0, 0};
-                    if (T >= 0) {
-                        const uint16_t* src = p.Xb + ((tb_base + (T >> 4)) * RT + 2 * s) * 256 + (g * 16 + (T & 15)) * 4;
-                        const u16x4 l4 = *reinterpret_cast<const u16x4*>(src);
-                        const u16x4 h4 = *reinterpret_cast<const u16x4*>(src + 256);
+                for (int rr = 0; rr < RTW; ++rr)
+                    a[rr] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(
+                        p.Wc + (((size_t)(wave * RTW + rr) * KS + t * KSD + s) * 64 + lane) * 8));
 #pragma unroll
-                        for (int i = 0; i < 4; ++i) {
-                            v[i] = l4[i];
-                            v[4 + i] = h4[i];
-                        }
-                    }
-                    gb[b] = __builtin_bit_cast(bf16x8, v);
-                } else {
-                    if (T >= 0) {
-                        const float* src = p.X + ((tb_base + (T >> 4)) * RT + 2 * s) * 256 + (g * 16 + (T & 15)) * 4;
-                        lo = ld4g(src);
-                        hi = ld4g(src + 256);
-                    }
-                    gb[b] = pack_b(lo, hi);
+                for (int b = 0; b < PB; ++b) {
+                    const bf16x8 bb = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(
+                        bsm + ((b * KSD + s) * 64 + lane) * 8));
+#pragma unroll
+                    for (int rr = 0; rr < RTW; ++rr) acc[rr][b] = mfma16x16x32(a[rr], bb, acc[rr][b]);
                 }
             }
-#pragma unroll
-            for (int rt = 0; rt < RT; ++rt) {
-                const bf16x8 a = __builtin_bit_cast(bf16x8,
-                    *reinterpret_cast<const u16x8*>(p.Wc + (((size_t)rt * KS + ks) * 64 + lane) * 8));
-#pragma unroll
-                for (int b = 0; b < RB; ++b) acc[rt][b] = mfma16x16x32(a, gb[b], acc[rt][b]);
-            }
+            __syncthreads();   // the next tap's gather overwrites the fragments
         }
 #pragma unroll
-        for (int b = 0; b < RB; ++b) {
-            if (pos_i[b] < 0) continue;
-            const float* wrow = p.wo + pos_i[b] * D;
-            float s = 0.f;
+        for (int b = 0; b < PB; ++b) {
+            const int pos = (pb0 + b) * 16 + col;
+            if (pos >= npos) continue;
+            const float* wrow = p.wo + (pos / d) * D;
+            float sum = 0.f;
 #pragma unroll
-            for (int rt = 0; rt < RT; ++rt) {
-                const f32x4 bias = ld4g(p.bc + rt * 16 + 4 * g);
-                const f32x4 w = ld4g(wrow + rt * 16 + 4 * g);
+            for (int rr = 0; rr < RTW; ++rr) {
+                const int o = (wave * RTW + rr) * 16 + 4 * g;
+                const f32x4 bias = ld4g(p.bc + o);
+                const f32x4 w = ld4g(wrow + o);
 #pragma unroll
-                for (int i = 0; i < 4; ++i) s = fmaf(w[i], fmaxf(acc[rt][b][i] + bias[i], 0.f), s);
+                for (int i = 0; i < 4; ++i) sum = fmaf(w[i], fmaxf(acc[rr][b][i] + bias[i], 0.f), sum);
             }
-            part += s * inv_d;
+            part += sum * inv_d;
         }
     }
     // fixed-order reduction: lanes, then wavefronts
