@@ -128,7 +128,7 @@ PWD_DEV void stage_kv(const AttnShape& sh, const uint16_t* k0, uint16_t* ks, uin
 
 // max |k|^2 over the real keys of blocks kb0, kb0 + stride, ..., reduced over the wavefront;
 // KMAX_UNROLL blocks at a time so their LDS reads and cross-lane sums are in flight together.
-// An index past the last block repeats block kb0, so only the listed blocks are read.
+// Blocks past the last are skipped (the tests are wavefront-uniform).
 template <int DH>
 PWD_DEV float kmax2_blocks(const AttnShape& sh, const uint16_t* ks, int slot0, int kb0, int stride, int lane) {
     constexpr int NV = DH == 32 ? 8 : 4;
@@ -138,23 +138,27 @@ PWD_DEV float kmax2_blocks(const AttnShape& sh, const uint16_t* ks, int slot0, i
         float n2[KMAX_UNROLL];
 #pragma unroll
         for (int u = 0; u < KMAX_UNROLL; ++u) {
-            const int kb = kbs + u * stride < sh.nbw ? kbs + u * stride : kb0;
-            const u16x8 kv = *reinterpret_cast<const u16x8*>(ks + (kb * 64 + lane) * 8);
+            const int kb = kbs + u * stride;
             n2[u] = 0.f;
+            if (kb < sh.nbw) {
+                const u16x8 kv = *reinterpret_cast<const u16x8*>(ks + (kb * 64 + lane) * 8);
 #pragma unroll
-            for (int i = 0; i < NV; ++i) {
-                const float f = (float)__builtin_bit_cast(__bf16, (uint16_t)kv[slot0 + i]);
-                n2[u] = fmaf(f, f, n2[u]);
+                for (int i = 0; i < NV; ++i) {
+                    const float f = (float)__builtin_bit_cast(__bf16, (uint16_t)kv[slot0 + i]);
+                    n2[u] = fmaf(f, f, n2[u]);
+                }
             }
         }
 #pragma unroll
-        for (int u = 0; u < KMAX_UNROLL; ++u) n2[u] += __shfl_xor(n2[u], 16);
+        for (int u = 0; u < KMAX_UNROLL; ++u)
+            if (kbs + u * stride < sh.nbw) n2[u] += __shfl_xor(n2[u], 16);
 #pragma unroll
-        for (int u = 0; u < KMAX_UNROLL; ++u) n2[u] += __shfl_xor(n2[u], 32);
+        for (int u = 0; u < KMAX_UNROLL; ++u)
+            if (kbs + u * stride < sh.nbw) n2[u] += __shfl_xor(n2[u], 32);
 #pragma unroll
         for (int u = 0; u < KMAX_UNROLL; ++u) {
-            const int kb = kbs + u * stride < sh.nbw ? kbs + u * stride : kb0;
-            if (kb * 16 + col < sh.N) kmax2 = fmaxf(kmax2, n2[u]);
+            const int kb = kbs + u * stride;
+            if (kb < sh.nbw && kb * 16 + col < sh.N) kmax2 = fmaxf(kmax2, n2[u]);
         }
     }
 #pragma unroll
@@ -288,11 +292,12 @@ PWD_DEV void attn_pass(const AttnShape& sh, const AttnItem& it, int qb0, int qen
 #pragma unroll
                 for (int j = 0; j < QB; ++j) s[j][kk] = f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
             }
+            if (kb < nbw && (kb + 1) * 16 > N)   // a real block with padding keys (uniform test)
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                if (kb * 16 + 4 * g + i >= N)
+                for (int i = 0; i < 4; ++i)
+                    if (kb * 16 + 4 * g + i >= N)
 #pragma unroll
-                    for (int j = 0; j < QB; ++j) s[j][kk][i] = -INFINITY;
+                        for (int j = 0; j < QB; ++j) s[j][kk][i] = -INFINITY;
         }
         bf16x8 vl[RT];
         load_v(last, vl);
