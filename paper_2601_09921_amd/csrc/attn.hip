@@ -26,41 +26,52 @@
 
 namespace {
 
-constexpr int QMAX = 4;               // query blocks per wavefront pass, at most
 constexpr int KMAX_UNROLL = 8;        // key blocks per step of the max |k| scan
 
 PWD_DEV float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Head sizes: a Q/K/V fragment holds 32 features of 16 tokens, so a head of 64 spans NF = 2
+// fragments per token block (its scores take two 32-deep k-steps), a head of 32 one, and a
+// head of 16 half of one (slot0 selects its four values in each lane).
 template <int DH>
 struct Frag;
 template <>
+struct Frag<64> {
+    using T = bf16x8;
+    static constexpr int NF = 2, NV = 8, QMAX = 2;
+    static __device__ __forceinline__ f32x4 mma(T a, T b, f32x4 c) { return mfma16x16x32(a, b, c); }
+};
+template <>
 struct Frag<32> {
     using T = bf16x8;
+    static constexpr int NF = 1, NV = 8, QMAX = 4;
     static __device__ __forceinline__ f32x4 mma(T a, T b, f32x4 c) { return mfma16x16x32(a, b, c); }
 };
 template <>
 struct Frag<16> {
     using T = bf16x4;
+    static constexpr int NF = 1, NV = 4, QMAX = 4;
     static __device__ __forceinline__ f32x4 mma(T a, T b, f32x4 c) { return mfma16x16x16(a, b, c); }
 };
 
-// K fragment of key block kb (LDS holds whole 1 KB fragments; with dh = 16 one fragment
-// carries two heads and slot0 selects this head's four values).
+// K fragment f of key block kb (LDS holds whole 1 KB fragments, NF per key block).
 template <int DH>
-PWD_DEV typename Frag<DH>::T ld_kfrag(const uint16_t* ks, int kb, int lane, int slot0) {
-    if constexpr (DH == 32)
-        return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(ks + (kb * 64 + lane) * 8));
+PWD_DEV typename Frag<DH>::T ld_kfrag(const uint16_t* ks, int kb, int f, int lane, int slot0) {
+    const uint16_t* src = ks + ((kb * Frag<DH>::NF + f) * 64 + lane) * 8;
+    if constexpr (DH == 16)
+        return __builtin_bit_cast(bf16x4, *reinterpret_cast<const u16x4*>(src + slot0));
     else
-        return __builtin_bit_cast(bf16x4, *reinterpret_cast<const u16x4*>(ks + (kb * 64 + lane) * 8 + slot0));
+        return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(src));
 }
 
-// V^T A fragment of the 32 keys of superblock sb for dh columns 16 half .. 16 half + 15: this
-// lane's four keys of key block 2 sb (k slots 0-3) and of key block 2 sb + 1 (k slots 4-7),
-// i.e. the lane's 8 bytes of tile half `half` of both V fragments.
-PWD_DEV bf16x8 ld_vfrag(const uint16_t* vs, int half, int sb, int lane) {
-    const uint16_t* t = vs + (2 * sb) * 512 + half * 256 + lane * 4;
+// V^T A fragment of the 32 keys of superblock sb for head features 16 t .. 16 t + 15 (tile t
+// = half `half` of V fragment f): this lane's four keys of key block 2 sb (k slots 0-3) and of
+// key block 2 sb + 1 (k slots 4-7), i.e. the lane's 8 bytes of that tile in both blocks.
+template <int NF>
+PWD_DEV bf16x8 ld_vfrag(const uint16_t* vs, int f, int half, int sb, int lane) {
+    const uint16_t* t = vs + ((2 * sb) * NF + f) * 512 + half * 256 + lane * 4;
     const u16x4 lo = *reinterpret_cast<const u16x4*>(t);
-    const u16x4 hi = *reinterpret_cast<const u16x4*>(t + 512);
+    const u16x4 hi = *reinterpret_cast<const u16x4*>(t + NF * 512);
     u16x8 v;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -82,11 +93,11 @@ struct AttnShape {
 
 // One (window, head) item: its K/V in LDS, its Q, K and Y in HBM, and max |k|.
 struct AttnItem {
-    const uint16_t* ks;   // LDS [nbw][512] K fragments
-    const uint16_t* vs;   // LDS [nbw + 1][512] V tiles (+ a zero block when nbw is odd)
-    const uint16_t* q0;   // Q fragment of token block 0; block stride 3 KSD fragments
-    const uint16_t* k0;   // K fragment of token block 0 (V follows at + KSD fragments)
-    uint16_t* y0;         // Y fragment of token block 0; block stride KSD fragments
+    const uint16_t* ks;   // LDS [nbw][NF][512] K fragments
+    const uint16_t* vs;   // LDS [nbw + 1][NF][512] V tiles (+ a zero block when nbw is odd)
+    const uint16_t* q0;   // first Q fragment of token block 0; block stride 3 KSD fragments
+    const uint16_t* k0;   // first K fragment of token block 0 (V follows at + KSD fragments)
+    uint16_t* y0;         // first Y fragment of token block 0; block stride KSD fragments
     int slot0, vhalf;     // this head's slots inside a fragment (dh = 16 packs two heads)
     float kmax;
 };
@@ -94,36 +105,42 @@ struct AttnItem {
 template <int DH>
 PWD_DEV AttnItem make_item(const AttnParams& p, const AttnShape& sh, int item) {
     const int win = item / p.H, h = item % p.H;
-    const int frag = DH == 32 ? h : h / 2;
+    const int frag = DH == 64 ? 2 * h : DH == 32 ? h : h / 2;
     const int64_t tb_base = (int64_t)win * sh.nbw;
     AttnItem it;
     it.ks = it.vs = nullptr;
     it.q0 = p.QKV + (tb_base * 3 * sh.KSD + frag) * 512;
     it.k0 = it.q0 + (size_t)sh.KSD * 512;
     it.y0 = p.Y + (tb_base * sh.KSD + frag) * 512;
-    it.slot0 = DH == 32 ? 0 : (h % 2) * 4;
-    it.vhalf = DH == 32 ? 0 : h % 2;
+    it.slot0 = DH == 16 ? (h % 2) * 4 : 0;
+    it.vhalf = DH == 16 ? h % 2 : 0;
     it.kmax = 0.f;
     return it;
 }
 
-// Q of the QMAX blocks from qb0 (indices past qend - 1 repeat the last block).
-PWD_DEV void load_q(const AttnShape& sh, const uint16_t* q0, int qb0, int qend, int lane, u16x8 (&qv)[QMAX]) {
+// Q of the QM blocks from qb0 (indices past qend - 1 repeat the last block), NF fragments each.
+template <int NF, int QM>
+PWD_DEV void load_q(const AttnShape& sh, const uint16_t* q0, int qb0, int qend, int lane, u16x8 (&qv)[QM][NF]) {
 #pragma unroll
-    for (int j = 0; j < QMAX; ++j) {
+    for (int j = 0; j < QM; ++j) {
         const int qb = min(qb0 + j, qend - 1);
-        qv[j] = *reinterpret_cast<const u16x8*>(q0 + (size_t)qb * 3 * sh.KSD * 512 + lane * 8);
+#pragma unroll
+        for (int f = 0; f < NF; ++f)
+            qv[j][f] = *reinterpret_cast<const u16x8*>(q0 + ((size_t)qb * 3 * sh.KSD + f) * 512 + lane * 8);
     }
 }
 
 // Direct copies of the K and V fragments of key blocks kb0, kb0 + stride, ... into LDS.
+template <int NF>
 PWD_DEV void stage_kv(const AttnShape& sh, const uint16_t* k0, uint16_t* ks, uint16_t* vs, int kb0, int stride,
                       int lane) {
-    for (int kb = kb0; kb < sh.nbw; kb += stride) {
-        const uint16_t* src = k0 + (size_t)kb * 3 * sh.KSD * 512;
-        lds_load_1k(uniform_ptr(src), lds_addr(ks + kb * 512), lane);
-        lds_load_1k(uniform_ptr(src + (size_t)sh.KSD * 512), lds_addr(vs + kb * 512), lane);
-    }
+    for (int kb = kb0; kb < sh.nbw; kb += stride)
+#pragma unroll
+        for (int f = 0; f < NF; ++f) {
+            const uint16_t* src = k0 + ((size_t)kb * 3 * sh.KSD + f) * 512;
+            lds_load_1k(uniform_ptr(src), lds_addr(ks + (kb * NF + f) * 512), lane);
+            lds_load_1k(uniform_ptr(src + (size_t)sh.KSD * 512), lds_addr(vs + (kb * NF + f) * 512), lane);
+        }
 }
 
 // max |k|^2 over the real keys of blocks kb0, kb0 + stride, ..., reduced over the wavefront;
@@ -131,7 +148,7 @@ PWD_DEV void stage_kv(const AttnShape& sh, const uint16_t* k0, uint16_t* ks, uin
 // Blocks past the last are skipped (the tests are wavefront-uniform).
 template <int DH>
 PWD_DEV float kmax2_blocks(const AttnShape& sh, const uint16_t* ks, int slot0, int kb0, int stride, int lane) {
-    constexpr int NV = DH == 32 ? 8 : 4;
+    constexpr int NV = Frag<DH>::NV, NF = Frag<DH>::NF;
     const int col = lane & 15;
     float kmax2 = 0.f;
     for (int kbs = kb0; kbs < sh.nbw; kbs += KMAX_UNROLL * stride) {
@@ -141,11 +158,14 @@ PWD_DEV float kmax2_blocks(const AttnShape& sh, const uint16_t* ks, int slot0, i
             const int kb = kbs + u * stride;
             n2[u] = 0.f;
             if (kb < sh.nbw) {
-                const u16x8 kv = *reinterpret_cast<const u16x8*>(ks + (kb * 64 + lane) * 8);
 #pragma unroll
-                for (int i = 0; i < NV; ++i) {
-                    const float f = (float)__builtin_bit_cast(__bf16, (uint16_t)kv[slot0 + i]);
-                    n2[u] = fmaf(f, f, n2[u]);
+                for (int fr = 0; fr < NF; ++fr) {
+                    const u16x8 kv = *reinterpret_cast<const u16x8*>(ks + ((kb * NF + fr) * 64 + lane) * 8);
+#pragma unroll
+                    for (int i = 0; i < NV; ++i) {
+                        const float f = (float)__builtin_bit_cast(__bf16, (uint16_t)kv[slot0 + i]);
+                        n2[u] = fmaf(f, f, n2[u]);
+                    }
                 }
             }
         }
@@ -166,7 +186,7 @@ PWD_DEV float kmax2_blocks(const AttnShape& sh, const uint16_t* ks, int slot0, i
     return kmax2;
 }
 
-// Scheduling request for one iteration of the key loop (two superblocks, 20 QB MFMAs): each
+// Scheduling request for one iteration of the key loop (two superblocks, NMFMA MFMAs): each
 // MFMA followed by three VALU or transcendental instructions, so the exponentials and packs
 // issue while the matrix core runs instead of in separate bursts (measured: 3 per MFMA beats
 // 2 and 4).
@@ -182,28 +202,30 @@ PWD_DEV void interleave_mfma_valu() {
 // One pass of a wavefront: query blocks qb0 .. qb0 + QB - 1 (those >= qend are computed
 // from a repeated block and not stored) against every key of the item.
 template <int DH, int QB>
-PWD_DEV void attn_pass(const AttnShape& sh, const AttnItem& it, int qb0, int qend, const u16x8 (&qv)[QMAX],
-                       const bf16x8& ones, int lane) {
+PWD_DEV void attn_pass(const AttnShape& sh, const AttnItem& it, int qb0, int qend,
+                       const u16x8 (&qv)[Frag<DH>::QMAX][Frag<DH>::NF], const bf16x8& ones, int lane) {
     using FT = typename Frag<DH>::T;
+    constexpr int NF = Frag<DH>::NF, NV = Frag<DH>::NV;
     constexpr int RT = DH / 16;                 // 16-row tiles of O^T
-    constexpr int NV = DH == 32 ? 8 : 4;        // Q/K values per lane
     const int g = lane >> 4, col = lane & 15;
     const int nbw = sh.nbw, N = sh.N, slot0 = it.slot0;
     const int nsb = (nbw + 1) / 2;
     const uint16_t* ks = it.ks;
     const uint16_t* vs = it.vs;
 
-    FT q[QB];
+    FT q[QB][NF];
     f32x4 shift[QB];
 #pragma unroll
     for (int j = 0; j < QB; ++j) {
         float n2 = 0.f;
 #pragma unroll
-        for (int i = 0; i < NV; ++i) {
-            const float f = (float)__builtin_bit_cast(__bf16, (uint16_t)qv[j][slot0 + i]);
-            n2 = fmaf(f, f, n2);
-            q[j][i] = __builtin_bit_cast(__bf16, (uint16_t)qv[j][slot0 + i]);
-        }
+        for (int f = 0; f < NF; ++f)
+#pragma unroll
+            for (int i = 0; i < NV; ++i) {
+                const float x = (float)__builtin_bit_cast(__bf16, (uint16_t)qv[j][f][slot0 + i]);
+                n2 = fmaf(x, x, n2);
+                q[j][f][i] = __builtin_bit_cast(__bf16, (uint16_t)qv[j][f][slot0 + i]);
+            }
         const float m = sqrtf(sum4(n2)) * it.kmax;
         shift[j] = f32x4{-m, -m, -m, -m};
     }
@@ -217,23 +239,34 @@ PWD_DEV void attn_pass(const AttnShape& sh, const AttnItem& it, int qb0, int qen
         for (int rt = 0; rt < RT; ++rt) o[j][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
 
+    // V^T tile rt: half rt % 2 of fragment rt / 2 (dh = 16: this head's half of fragment 0)
+    auto vtile = [&](int rt, int sb) { return ld_vfrag<NF>(vs, DH == 16 ? 0 : rt / 2, DH == 16 ? it.vhalf : rt % 2, sb, lane); };
+    // S^T - m of key block kb for query block j: NF k-steps over the head's features
+    auto score = [&](const FT (&kf)[NF], int j, f32x4 init) {
+        f32x4 acc = Frag<DH>::mma(kf[0], q[j][0], init);
+#pragma unroll
+        for (int f = 1; f < NF; ++f) acc = Frag<DH>::mma(kf[f], q[j][f], acc);
+        return acc;
+    };
     // K and V^T fragments of superblock sb (two 16-key blocks). Indices up to nsb - 1 stay
     // inside the LDS image (a missing last key block reads the start of V^T), so the
     // prefetches below never need a bounds branch; such values are never used.
-    auto load_k = [&](int sb, FT (&kf)[2]) {
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk) kf[kk] = ld_kfrag<DH>(ks, 2 * sb + kk, lane, slot0);
-    };
-    auto load_v = [&](int sb, bf16x8 (&vf)[RT]) {
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt) vf[rt] = ld_vfrag(vs, DH == 32 ? rt : it.vhalf, sb, lane);
-    };
-    // S^T - m of one superblock for every query block
-    auto scores = [&](const FT (&kf)[2], f32x4 (&s)[QB][2]) {
+    auto load_k = [&](int sb, FT (&kf)[2][NF]) {
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-            for (int j = 0; j < QB; ++j) s[j][kk] = Frag<DH>::mma(kf[kk], q[j], shift[j]);
+            for (int f = 0; f < NF; ++f) kf[kk][f] = ld_kfrag<DH>(ks, 2 * sb + kk, f, lane, slot0);
+    };
+    auto load_v = [&](int sb, bf16x8 (&vf)[RT]) {
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) vf[rt] = vtile(rt, sb);
+    };
+    // S^T - m of one superblock for every query block
+    auto scores = [&](const FT (&kf)[2][NF], f32x4 (&s)[QB][2]) {
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+            for (int j = 0; j < QB; ++j) s[j][kk] = score(kf[kk], j, shift[j]);
     };
     // P = exp2(S), row sums, and O^T += V^T P^T for one superblock
     auto accumulate = [&](const f32x4 (&s)[QB][2], const bf16x8 (&vf)[RT]) {
@@ -258,7 +291,7 @@ PWD_DEV void attn_pass(const AttnShape& sh, const AttnItem& it, int qb0, int qen
     // sb+2 and V of sb+1 are in flight from LDS.
     const int nfull = nsb - 1;
     const int lastsb = nsb - 1;
-    FT kA[2], kB[2];
+    FT kA[2][NF], kB[2][NF];
     bf16x8 vA[RT], vB[RT];
     f32x4 sA[QB][2], sB[QB][2];
     load_k(0, kA);
@@ -275,7 +308,7 @@ PWD_DEV void attn_pass(const AttnShape& sh, const AttnItem& it, int qb0, int qen
         load_k(min(sb + 3, lastsb), kB);
         load_v(min(sb + 2, lastsb), vA);
         accumulate(sB, vB);                          // sb + 1
-        interleave_mfma_valu<10 * QB>();
+        interleave_mfma_valu<2 * QB * (2 * NF + 1 + RT)>();
     }
     if (sb < nfull) accumulate(sA, vA);
     {   // last superblock: missing key block and padding keys are -inf
@@ -285,9 +318,11 @@ PWD_DEV void attn_pass(const AttnShape& sh, const AttnItem& it, int qb0, int qen
         for (int kk = 0; kk < 2; ++kk) {
             const int kb = 2 * last + kk;
             if (kb < nbw) {
-                const FT a = ld_kfrag<DH>(ks, kb, lane, slot0);
+                FT a[NF];
 #pragma unroll
-                for (int j = 0; j < QB; ++j) s[j][kk] = Frag<DH>::mma(a, q[j], shift[j]);
+                for (int f = 0; f < NF; ++f) a[f] = ld_kfrag<DH>(ks, kb, f, lane, slot0);
+#pragma unroll
+                for (int j = 0; j < QB; ++j) s[j][kk] = score(a, j, shift[j]);
             } else {
 #pragma unroll
                 for (int j = 0; j < QB; ++j) s[j][kk] = f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
@@ -318,8 +353,13 @@ PWD_DEV void attn_pass(const AttnShape& sh, const AttnItem& it, int qb0, int qen
                 f32x4 s2[2];
                 for (int kk = 0; kk < 2; ++kk) {
                     const int kb = 2 * sb + kk;
-                    if (kb < nbw) s2[kk] = Frag<DH>::mma(ld_kfrag<DH>(ks, kb, lane, slot0), q[j], zero);
-                    else s2[kk] = f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+                    if (kb < nbw) {
+                        FT a[NF];
+                        for (int f = 0; f < NF; ++f) a[f] = ld_kfrag<DH>(ks, kb, f, lane, slot0);
+                        s2[kk] = score(a, j, zero);
+                    } else {
+                        s2[kk] = f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+                    }
                     for (int i = 0; i < 4; ++i)
                         if (kb * 16 + 4 * g + i >= N) s2[kk][i] = -INFINITY;
                 }
@@ -339,22 +379,24 @@ PWD_DEV void attn_pass(const AttnShape& sh, const AttnItem& it, int qb0, int qen
                 ll = ll * alpha + lsum;
                 mm = mnew;
                 const bf16x8 pb2 = pack_b(pr[0], pr[1]);
-                for (int rt = 0; rt < RT; ++rt)
-                    o[j][rt] = mfma16x16x32(ld_vfrag(vs, DH == 32 ? rt : it.vhalf, sb, lane), pb2, o[j][rt] * alpha);
+                for (int rt = 0; rt < RT; ++rt) o[j][rt] = mfma16x16x32(vtile(rt, sb), pb2, o[j][rt] * alpha);
             }
             lt = sum4(ll);
         }
         if (qb >= qend) continue;
         const float inv = 1.0f / lt;
         uint16_t* dst = it.y0 + (size_t)qb * sh.KSD * 512 + lane * 8;
-        if constexpr (DH == 32) {
-            const bf16x8 out = pack_b(o[j][0] * inv, o[j][RT - 1] * inv);
-            *reinterpret_cast<u16x8*>(dst) = __builtin_bit_cast(u16x8, out);
-        } else {
+        if constexpr (DH == 16) {
             u16x4 out;
 #pragma unroll
             for (int i = 0; i < 4; ++i) out[i] = __builtin_bit_cast(uint16_t, (__bf16)(o[j][0][i] * inv));
             *reinterpret_cast<u16x4*>(dst + it.slot0) = out;
+        } else {
+#pragma unroll
+            for (int f = 0; f < NF; ++f) {   // fragment f: O^T tiles 2f and 2f + 1
+                const bf16x8 out = pack_b(o[j][2 * f] * inv, o[j][2 * f + 1] * inv);
+                *reinterpret_cast<u16x8*>(dst + f * 512) = __builtin_bit_cast(u16x8, out);
+            }
         }
     }
 }
@@ -370,46 +412,43 @@ PWD_DEV bf16x8 ones_row(int lane) {
 // Passes of QMAX, 2 and 1 blocks over this wavefront's query blocks [qbeg, qend). qnext
 // holds Q of the first pass on entry; each pass first starts the Q load of the pass after it.
 template <int DH>
-PWD_DEV void attn_passes(const AttnShape& sh, const AttnItem& it, int qbeg, int qend, u16x8 (&qnext)[QMAX],
-                         const bf16x8& ones, int lane) {
+PWD_DEV void attn_passes(const AttnShape& sh, const AttnItem& it, int qbeg, int qend,
+                         u16x8 (&qnext)[Frag<DH>::QMAX][Frag<DH>::NF], const bf16x8& ones, int lane) {
+    constexpr int QM = Frag<DH>::QMAX, NF = Frag<DH>::NF;
     auto prefetch = [&](int qb_after) {
-        if (qb_after < qend) load_q(sh, it.q0, qb_after, qend, lane, qnext);
+        if (qb_after < qend) load_q<NF, QM>(sh, it.q0, qb_after, qend, lane, qnext);
+    };
+    auto run = [&](auto qbc, int qb) {
+        constexpr int QB = decltype(qbc)::value;
+        u16x8 qv[QM][NF];
+#pragma unroll
+        for (int j = 0; j < QM; ++j)
+#pragma unroll
+            for (int f = 0; f < NF; ++f) qv[j][f] = qnext[j][f];
+        prefetch(qb + QB);
+        attn_pass<DH, QB>(sh, it, qb, qend, qv, ones, lane);
     };
     int qb = qbeg;
-    while (qend - qb >= QMAX) {
-        u16x8 qv[QMAX];
-#pragma unroll
-        for (int j = 0; j < QMAX; ++j) qv[j] = qnext[j];
-        prefetch(qb + QMAX);
-        attn_pass<DH, QMAX>(sh, it, qb, qend, qv, ones, lane);
-        qb += QMAX;
+    for (; qend - qb >= QM; qb += QM) run(std::integral_constant<int, QM>{}, qb);
+    if constexpr (QM > 2) {
+        if (qend - qb >= 2) {
+            run(std::integral_constant<int, 2>{}, qb);
+            qb += 2;
+        }
     }
-    if (qend - qb >= 2) {
-        u16x8 qv[QMAX];
-#pragma unroll
-        for (int j = 0; j < QMAX; ++j) qv[j] = qnext[j];
-        prefetch(qb + 2);
-        attn_pass<DH, 2>(sh, it, qb, qend, qv, ones, lane);
-        qb += 2;
-    }
-    if (qend - qb == 1) {
-        u16x8 qv[QMAX];
-#pragma unroll
-        for (int j = 0; j < QMAX; ++j) qv[j] = qnext[j];
-        prefetch(qb + 1);
-        attn_pass<DH, 1>(sh, it, qb, qend, qv, ones, lane);
-    }
+    if (qend - qb == 1) run(std::integral_constant<int, 1>{}, qb);
 }
 
 // One workgroup per (window, head); K/V stay in LDS for the whole item.
 template <int DH, int WAVES>
 __global__ __launch_bounds__(WAVES * 64, 2) void attn_kernel(AttnParams p) {
+    constexpr int NF = Frag<DH>::NF, QM = Frag<DH>::QMAX;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const AttnShape sh{p.N, p.nbw, p.H * DH / 32};
     const int nbw = sh.nbw;
     extern __shared__ __align__(16) unsigned char smem[];
-    uint16_t* ks = reinterpret_cast<uint16_t*>(smem);   // [nbw][512]: K fragments
-    uint16_t* vs = ks + (size_t)nbw * 512;               // [nbw + 1][512]: V tiles, + a zero block
+    uint16_t* ks = reinterpret_cast<uint16_t*>(smem);   // [nbw][NF][512]: K fragments
+    uint16_t* vs = ks + (size_t)nbw * NF * 512;          // [nbw + 1][NF][512]: V tiles, + a zero block
     __shared__ float kmax_w[WAVES];
     AttnItem it = make_item<DH>(p, sh, blockIdx.x);
     it.ks = ks;
@@ -418,14 +457,15 @@ __global__ __launch_bounds__(WAVES * 64, 2) void attn_kernel(AttnParams p) {
     // Each wavefront owns a contiguous share of the query blocks; Q of its first pass is
     // loaded before the K/V staging, so its latency overlaps the staging.
     const int qbeg = wave * nbw / WAVES, qend = (wave + 1) * nbw / WAVES;
-    u16x8 qnext[QMAX];
-    if (qbeg < qend) load_q(sh, it.q0, qbeg, qend, lane, qnext);
+    u16x8 qnext[QM][NF];
+    if (qbeg < qend) load_q<NF, QM>(sh, it.q0, qbeg, qend, lane, qnext);
 
     // stage K and V; an odd key-block count gets a zero V block so the last superblock's
     // missing keys meet P = 0 and V = 0
-    stage_kv(sh, it.k0, ks, vs, wave, WAVES, lane);
+    stage_kv<NF>(sh, it.k0, ks, vs, wave, WAVES, lane);
     if (nbw & 1)
-        for (int i = threadIdx.x; i < 256; i += blockDim.x) reinterpret_cast<uint32_t*>(vs + nbw * 512)[i] = 0u;
+        for (int i = threadIdx.x; i < 256 * NF; i += blockDim.x)
+            reinterpret_cast<uint32_t*>(vs + (size_t)nbw * NF * 512)[i] = 0u;
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     const float kw = kmax2_blocks<DH>(sh, ks, it.slot0, wave, WAVES, lane);
@@ -452,21 +492,23 @@ template <int DH>
 hipError_t launch_dh(const AttnParams& p, int nwin, hipStream_t s) {
     // wavefronts per (window, head): enough for a pass of QMAX query blocks each, at most
     // four, so small windows run as many small workgroups rather than idle wavefronts
-    if (p.nbw <= QMAX) return launch_shape<DH, 1>(p, nwin, s);
-    if (p.nbw <= 2 * QMAX) return launch_shape<DH, 2>(p, nwin, s);
+    constexpr int QM = Frag<DH>::QMAX;
+    if (p.nbw <= QM) return launch_shape<DH, 1>(p, nwin, s);
+    if (p.nbw <= 2 * QM) return launch_shape<DH, 2>(p, nwin, s);
     return launch_shape<DH, 4>(p, nwin, s);
 }
 
 }  // namespace
 
 size_t attn_smem_bytes(int dh, int Npad, int nbw) {
-    (void)dh;
     (void)Npad;
-    return (size_t)(2 * nbw + 1) * 1024;   // K [nbw] and V [nbw + 1] fragments of 1 KB
+    // K [nbw] and V [nbw + 1] blocks of 1 KB fragments, two per block for a head of 64
+    return (size_t)(2 * nbw + 1) * (dh == 64 ? 2 : 1) * 1024;
 }
 
 hipError_t launch_attn(int dh, const AttnParams& p, int nwin, hipStream_t s) {
     if (nwin <= 0) return hipSuccess;
+    if (dh == 64) return launch_dh<64>(p, nwin, s);
     if (dh == 32) return launch_dh<32>(p, nwin, s);
     if (dh == 16) return launch_dh<16>(p, nwin, s);
     return hipErrorInvalidValue;

@@ -218,14 +218,15 @@ int decoder_validate_config(const pwd_geometry* g, const pwd_model_dims* m) {
     if (m->dtype == PWD_DTYPE_BF16) {
         if (m->d_model != 128 && m->d_model != 256)
             return fail(PWD_EUNSUPPORTED, "bf16 d_model %d: need 128 or 256", m->d_model);
-        if (dh != 16 && dh != 32) return fail(PWD_EUNSUPPORTED, "bf16 head size %d: need 16 or 32", dh);
+        if (dh != 16 && dh != 32 && dh != 64)
+            return fail(PWD_EUNSUPPORTED, "bf16 head size %d: need 16, 32 or 64", dh);
         const size_t smem = attn_smem_bytes(dh, (N + 15) / 16 * 16, (N + 15) / 16);
         if (smem > 160 * 1024) return fail(PWD_EUNSUPPORTED, "attention tile needs %zu bytes of LDS", smem);
     } else if (m->dtype == PWD_DTYPE_F32) {
         if (m->d_model != 16 && m->d_model != 32 && m->d_model != 64)
             return fail(PWD_EUNSUPPORTED, "fp32 d_model %d: need 16, 32 or 64", m->d_model);
-        if (dh != 4 && dh != 8 && dh != 16 && dh != 32)
-            return fail(PWD_EUNSUPPORTED, "fp32 head size %d: need 4, 8, 16 or 32", dh);
+        if (dh != 4 && dh != 8 && dh != 16 && dh != 32 && dh != 64)
+            return fail(PWD_EUNSUPPORTED, "fp32 head size %d: need 4, 8, 16, 32 or 64", dh);
         const size_t smem = f32_window_smem_bytes(N, m->d_model, m->n_heads, 4 * m->d_model);
         if (smem > 64 * 1024)
             return fail(PWD_EUNSUPPORTED, "fp32 window of %d tokens needs %zu bytes of LDS (max 65536)", N, smem);
