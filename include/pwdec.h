@@ -99,11 +99,12 @@ typedef enum {
 size_t decoder_blob_floats(const pwd_geometry* geom, const pwd_model_dims* dims);
 
 /* Checks geometry and dimensions on the host only; touches no device.
- * Supported: distance odd in 3..25; distance <= window_rounds <= 3*distance;
+ * Supported: distance odd in 3..63 with the on-chip limits below (bf16: up to 35 at head
+ * sizes 16 and 32, up to 25 at 64); distance <= window_rounds <= 3*distance;
  * 1 <= max_windows <= 2^24; mlp_ratio = 4; n_layers 1..8;
  * PWD_DTYPE_BF16: d_model in {128, 256}, head size d_model/n_heads in {16, 32, 64}, and the
  * attention tile (K and V of one head: (2 ceil((d*d-1)/16) + 1) KB, twice that for head size
- * 64) within 160 KB of LDS (every distance up to 25 fits);
+ * 64) within 160 KB of LDS;
  * PWD_DTYPE_F32: d_model in {16, 32, 64}, head size in {4, 8, 16, 32, 64} and
  * (d*d-1) * (3*d_model + 4*d_model) * 4 bytes within the on-chip budget (about d <= 5 at
  * d_model 64). Returns PWD_OK, PWD_EINVAL (null) or PWD_EUNSUPPORTED. */

@@ -204,7 +204,8 @@ size_t decoder_blob_floats(const pwd_geometry* geom, const pwd_model_dims* dims)
 int decoder_validate_config(const pwd_geometry* g, const pwd_model_dims* m) {
     if (!g || !m) return fail(PWD_EINVAL, "null geometry or dimensions");
     const int d = g->distance;
-    if (d < 3 || d > 25 || d % 2 == 0) return fail(PWD_EUNSUPPORTED, "distance %d: need odd 3..25", d);
+    // any odd distance whose attention tile (bf16) or window (fp32) fits on chip, checked below
+    if (d < 3 || d > 63 || d % 2 == 0) return fail(PWD_EUNSUPPORTED, "distance %d: need odd 3..63", d);
     if (g->window_rounds < d || g->window_rounds > 3 * d)
         return fail(PWD_EUNSUPPORTED, "window_rounds %d: need %d..%d", g->window_rounds, d, 3 * d);
     if (g->max_windows < 1 || g->max_windows > (1 << 24))

@@ -32,7 +32,8 @@ def test_workloads_are_supported(lib, wl):
 
 
 @pytest.mark.parametrize("kw", [
-    dict(d=4), dict(d=1), dict(d=27), dict(W=6), dict(W=22), dict(B=0), dict(r=5), dict(L=0),
+    dict(d=4), dict(d=1), dict(d=65), dict(d=37, W=37), dict(d=27, W=27, D=256, H=4),
+    dict(W=6), dict(W=22), dict(B=0), dict(r=5), dict(L=0),
     dict(H=3), dict(D=96, H=6), dict(D=128, H=1), dict(D=256, H=2), dict(dt=2), dict(dt=0, D=256, H=8),
     dict(dt=0, d=11, W=22, D=64, H=4),
 ])
@@ -44,10 +45,12 @@ def test_rejects_unsupported(lib, kw):
 @pytest.mark.parametrize("kw", [
     dict(D=128, H=2), dict(D=256, H=4), dict(d=25, W=50, D=256, H=4), dict(d=25, W=75, D=128, H=2),
     dict(D=256, H=16), dict(dt=0, d=3, W=6, D=64, H=1),
+    dict(d=27, W=54, D=256, H=8), dict(d=35, W=35, D=128, H=8), dict(d=35, W=105, D=256, H=8),
 ])
 def test_supported_head_sizes(lib, kw):
-    """Head sizes 16, 32 and 64 on the bf16 path up to d = 25 (LDS for K and V of one head
-    of 64 at d = 25: 2 x 79 KB), and 64 on the fp32 path."""
+    """Head sizes 16, 32 and 64 on the bf16 path (LDS for K and V of one head of 64 at
+    d = 25: 2 x 79 KB), 64 on the fp32 path, and distances past 25 while the attention tile
+    fits (d = 35, heads of 16 or 32: 155 KB; d = 37 and d = 27 with heads of 64 do not)."""
     assert validate(lib, **kw) == pwdec.PWD_OK
 
 

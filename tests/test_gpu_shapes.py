@@ -29,6 +29,8 @@ SHAPES = [
     (7, 14, 4, 128, 1, 2),      # dh 64, odd key-block count (zero V block of two fragments)
     (11, 22, 3, 128, 2, 2),     # dh 64, four wavefronts
     (25, 25, 2, 256, 1, 4),     # dh 64 at d25: K and V of one head fill 158 KB of LDS
+    (27, 27, 2, 256, 1, 8),     # past the benchmark distances: N = 728
+    (35, 35, 1, 128, 1, 8),     # N = 1224, 77 key blocks: 155 KB of K/V in LDS
 ]
 
 
