@@ -132,6 +132,33 @@ def recurrent_measurement(dec, wl, torch, dev_meas, dev_types):
             "readout_launches": ro_n, "readout_ms_total": round(ro_ms, 2)}
 
 
+def input_stage_measurement(dec, wl, torch, dev_meas, dev_types, reps=5):
+    """The input stage on its own: decoder_detection_events over the batch (packed measurement
+    rounds in, packed detection events out; the same event_word the token kernel fuses),
+    timed with HIP events on the stream it runs on."""
+    B, W, words = wl.B, wl.W, wl.words
+    events = torch.empty((B, W, words), dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+    dec.detection_events(dev_meas, dev_types, events, stream)     # warm-up
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        dec.detection_events(dev_meas, dev_types, events, stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    nbytes = B * (W + 1) * words * 4 + B + B * W * words * 4
+    return {"kernel": "events_kernel", "avg_ms": round(ms, 4), "bytes": nbytes,
+            "GBps": round(nbytes / (ms * 1e-3) / 1e9, 1), "frac_of_hbm_peak": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 3)}
+
+
+def environment(torch):
+    props = torch.cuda.get_device_properties(0)
+    return {"device": props.name, "arch": getattr(props, "gcnArchName", ""),
+            "compute_units": props.multi_processor_count, "torch": torch.__version__,
+            "hip": getattr(torch.version, "hip", None)}
+
+
 def cpu_baseline(wl, weights, sample):
     """The fp64 oracle on `sample` windows (one per window type) on the host cores."""
     from oracle import decoder as O
@@ -276,6 +303,8 @@ def main():
             "traffic": load_traffic(dom),
         },
     }
+    out["input_stage"] = input_stage_measurement(dec, wl, torch, dev_meas, dev_types)
+    out["env"] = environment(torch)
     if not args.no_stream:
         out["stream"] = stream_measurement(dec, wl, torch, pwdec, synth)
     if not args.no_recurrent:
