@@ -141,19 +141,21 @@ __global__ __launch_bounds__(RWAVES * 64, 2) void readout_kernel(ReadoutParams p
     }
 }
 
+// One thread per output word; 32-bit index arithmetic (IDX = uint32_t) below 2^31 words.
+template <typename IDX>
 __global__ void events_kernel(EventsParams p) {
-    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const int64_t per_win = (int64_t)p.in.W * p.in.words;
-    if (idx >= per_win * p.in.nwin) return;
-    const int64_t win = idx / per_win;
+    const IDX idx = (IDX)blockIdx.x * blockDim.x + threadIdx.x;
+    const IDX per_win = (IDX)p.in.W * (IDX)p.in.words;
+    if (idx >= per_win * (IDX)p.in.nwin) return;
+    const IDX win = idx / per_win;
     const int rem = (int)(idx - win * per_win);
-    const int t = rem / p.in.words, wd = rem % p.in.words;
+    const int t = rem / p.in.words, wd = rem - t * p.in.words;
     const int type = p.in.types[win];
     uint32_t e = 0u;
     if (type > WIN_FINAL) {
         atomicOr(p.err, 1);
     } else {
-        e = event_word(p.in.meas + win * (int64_t)(p.in.W + 1) * p.in.words, p.in.words, t, wd,
+        e = event_word(p.in.meas + (int64_t)win * (p.in.W + 1) * p.in.words, p.in.words, t, wd,
                        type, p.in.b_left, p.in.d);
         const int valid = p.in.N - wd * 32;
         if (valid < 32) e &= (1u << valid) - 1u;
@@ -175,6 +177,8 @@ hipError_t launch_readout(const ReadoutParams& p, hipStream_t s) {
 hipError_t launch_events(const EventsParams& p, hipStream_t s) {
     const int64_t total = (int64_t)p.in.nwin * p.in.W * p.in.words;
     if (total <= 0) return hipSuccess;
-    events_kernel<<<dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s>>>(p);
+    const dim3 grid((unsigned)((total + 255) / 256)), block(256);
+    if (total < ((int64_t)1 << 31)) events_kernel<uint32_t><<<grid, block, 0, s>>>(p);
+    else events_kernel<uint64_t><<<grid, block, 0, s>>>(p);
     return hipGetLastError();
 }

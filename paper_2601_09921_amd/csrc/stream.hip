@@ -10,19 +10,21 @@ constexpr int SPLIT_THREADS = 256;
 constexpr int COMBINE_THREADS = 256;
 
 // One thread per (window, row, word): meas[i][k][w] = R[i d - b_left - 1 + k][w], zero
-// before the stream and R[T-1] after it. Consecutive threads copy consecutive words.
+// before the stream and R[T-1] after it. Consecutive threads copy consecutive words. The
+// index arithmetic is 32-bit (IDX = uint32_t) whenever the output has fewer than 2^31 words.
+template <typename IDX>
 __global__ __launch_bounds__(SPLIT_THREADS) void stream_split_kernel(StreamSplitParams p) {
-    const int64_t idx = (int64_t)blockIdx.x * SPLIT_THREADS + threadIdx.x;
-    const int64_t total = (int64_t)p.m * (p.W + 1) * p.words;
+    const IDX idx = (IDX)blockIdx.x * SPLIT_THREADS + threadIdx.x;
+    const IDX total = (IDX)p.m * (IDX)(p.W + 1) * (IDX)p.words;
     if (idx < total) {
-        const int w = (int)(idx % p.words);
-        const int64_t r = idx / p.words;
-        const int k = (int)(r % (p.W + 1));
-        const int64_t i = r / (p.W + 1);
-        const int64_t src = i * p.d - p.b_left - 1 + k;
+        const IDX r = idx / (IDX)p.words;
+        const int w = (int)(idx - r * (IDX)p.words);
+        const IDX i = r / (IDX)(p.W + 1);
+        const int k = (int)(r - i * (IDX)(p.W + 1));
+        const int64_t src = (int64_t)i * p.d - p.b_left - 1 + k;
         p.meas[idx] = src < 0 ? 0u : p.stream[(src < p.T ? src : p.T - 1) * p.words + w];
     }
-    if (idx < p.m) p.types[idx] = idx == 0 ? WIN_INITIAL : (idx == p.m - 1 ? WIN_FINAL : WIN_BULK);
+    if (idx < (IDX)p.m) p.types[idx] = idx == 0 ? WIN_INITIAL : (idx == (IDX)p.m - 1 ? WIN_FINAL : WIN_BULK);
 }
 
 // One workgroup: XOR of the window bits and prod_k (1 - 2 sigmoid(logit_k)) in double. Each
@@ -59,7 +61,9 @@ __global__ __launch_bounds__(COMBINE_THREADS) void stream_combine_kernel(StreamC
 hipError_t launch_stream_split(const StreamSplitParams& p, hipStream_t s) {
     const int64_t total = (int64_t)p.m * (p.W + 1) * p.words;
     const int64_t n = total > p.m ? total : p.m;
-    stream_split_kernel<<<dim3((unsigned)((n + SPLIT_THREADS - 1) / SPLIT_THREADS)), dim3(SPLIT_THREADS), 0, s>>>(p);
+    const dim3 grid((unsigned)((n + SPLIT_THREADS - 1) / SPLIT_THREADS)), block(SPLIT_THREADS);
+    if (n < ((int64_t)1 << 31)) stream_split_kernel<uint32_t><<<grid, block, 0, s>>>(p);
+    else stream_split_kernel<uint64_t><<<grid, block, 0, s>>>(p);
     return hipGetLastError();
 }
 
