@@ -15,7 +15,8 @@ It follows the paper's statement of the method step by step:
   * the XOR combination of per-window bits (eq. global_xor).
 
 Readings taken where the paper is silent or ambiguous (each listed in the design notes):
-the token set is the d*d-1 real stabilizers; LayerNorm (post-norm, eps from the weights)
+the token set is the d*d-1 real stabilizers by default, with the paper's (d+1)^2 grid as an
+option (grid=True); LayerNorm (post-norm, eps from the weights)
 replaces BatchNorm; ReLU feed-forward; attention has Q/K/V/O biases and scale 1/sqrt(dh);
 the readout convolution is followed by a bias and ReLU, pooling averages over columns;
 the window type adds a learned bias to the logit on top of the boundary padding masks.
@@ -65,6 +66,27 @@ def stabilizer_kind(cell) -> str:
 def grid_positions(d: int) -> np.ndarray:
     """Flattened grid index r*(d+1)+c of each token (the PE position, App. A.1.2/A.1.4)."""
     return np.array([r * (d + 1) + c for r, c in stabilizer_cells(d)], dtype=np.int64)
+
+
+def token_cells(d: int, grid: bool = False):
+    """Cells that carry a token, row-major. By default the d*d-1 stabilizer cells; with
+    grid=True every cell of the (d+1)x(d+1) array, the token set of App. A.1.2 and of
+    Algorithm 1's (d+1)^2 x d_model state: a cell without a stabilizer then carries state
+    but never receives a detection event."""
+    if not grid:
+        return stabilizer_cells(d)
+    return [(r, c) for r in range(d + 1) for c in range(d + 1)]
+
+
+def token_events(ev: np.ndarray, d: int, grid: bool = False) -> np.ndarray:
+    """Detection events per token: the stabilizer events [..][N] themselves, or (grid) placed
+    at their cells of the (d+1)^2 grid with zeros at the other cells."""
+    if not grid:
+        return ev
+    out = np.zeros(ev.shape[:-1] + ((d + 1) ** 2,), dtype=ev.dtype)
+    for s, (r, c) in enumerate(stabilizer_cells(d)):
+        out[..., r * (d + 1) + c] = ev[..., s]
+    return out
 
 
 # ----------------------------------------------------------------------------- bits
@@ -240,18 +262,18 @@ def rnn_core(X: np.ndarray, w: dict, H: int) -> np.ndarray:
     return X
 
 
-def readout(state: np.ndarray, types: np.ndarray, w: dict, d: int) -> np.ndarray:
+def readout(state: np.ndarray, types: np.ndarray, w: dict, d: int, grid: bool = False) -> np.ndarray:
     """Readout of App. A.3 on the final decoder state.
 
     state: [B][N][D]. The tokens are scattered back onto the (d+1)x(d+1) grid (zeros at
-    cells without a stabilizer); a 2x2 convolution without padding shrinks it to d x d:
+    cells without a token); a 2x2 convolution without padding shrinks it to d x d:
     Y[i, j] = ReLU(b_c + sum_{a,b in {0,1}} G[i+a, j+b] @ Wc[a][b]); logical pooling
     averages over j; a linear map of the d x D features gives the logit, plus the output
     bias and the bias of the window type.
     """
     B, N, D = state.shape
     G = np.zeros((B, d + 1, d + 1, D), dtype=np.float64)
-    for s, (r, c) in enumerate(stabilizer_cells(d)):
+    for s, (r, c) in enumerate(token_cells(d, grid)):
         G[:, r, c, :] = state[:, s, :]
     Y = np.zeros((B, d, d, D), dtype=np.float64)
     for a in (0, 1):
@@ -264,30 +286,35 @@ def readout(state: np.ndarray, types: np.ndarray, w: dict, d: int) -> np.ndarray
 
 
 def forward_windows(meas: np.ndarray, types: np.ndarray, w: dict, d: int, H: int,
-                    return_events: bool = False):
+                    return_events: bool = False, grid: bool = False):
     """Algorithm 1, inference branch, on a batch of windows.
 
-    meas: 0/1 [B][W+1][N] measurement rounds; types: [B] window types.
-    D_0 = 0; for each round n: S_n = Embed(E_n); D_n = RNNCore(kappa * (S_n + D_{n-1}));
-    after the last round the readout gives one logit per window; bit = [logit > 0].
+    meas: 0/1 [B][W+1][N] measurement rounds of the N = d*d-1 stabilizers; types: [B]
+    window types. D_0 = 0; for each round n: S_n = Embed(E_n); D_n = RNNCore(kappa * (S_n +
+    D_{n-1})); after the last round the readout gives one logit per window; bit = [logit >
+    0]. grid=True runs the network over all (d+1)^2 cells (token_cells).
     """
     meas = np.asarray(meas, dtype=np.uint8)
-    B, W1, N = meas.shape
+    B = meas.shape[0]
+    W1 = meas.shape[1]
     D = w["w_e"].shape[0]
     ev = detection_events(meas, types, d)
-    pe = positional_encoding((d + 1) ** 2, D)[grid_positions(d)]
-    state = np.zeros((B, N, D), dtype=np.float64)
+    tev = token_events(ev, d, grid)
+    pos = np.array([r * (d + 1) + c for r, c in token_cells(d, grid)], dtype=np.int64)
+    pe = positional_encoding((d + 1) ** 2, D)[pos]
+    state = np.zeros((B, len(pos), D), dtype=np.float64)
     for n in range(W1 - 1):
-        S = embed(ev[:, n, :], w, pe)
+        S = embed(tev[:, n, :], w, pe)
         state = rnn_core(w["kappa"] * (S + state), w, H)
-    logits = readout(state, types, w, d)
+    logits = readout(state, types, w, d, grid)
     bits = (logits > 0).astype(np.uint8)
     if return_events:
         return logits, bits, ev
     return logits, bits
 
 
-def forward_windows_recurrent(meas: np.ndarray, types: np.ndarray, w: dict, d: int, H: int):
+def forward_windows_recurrent(meas: np.ndarray, types: np.ndarray, w: dict, d: int, H: int,
+                              grid: bool = False):
     """Algorithm 1, recurrent branch: the same pass over the window's rounds, with a readout
     of the decoder state after every round n > 2b (Sec. recurrent training), i.e. after the
     rounds that complete a window of b left buffer, tau core and b right buffer rounds,
@@ -296,23 +323,24 @@ def forward_windows_recurrent(meas: np.ndarray, types: np.ndarray, w: dict, d: i
     inference-branch result.
     """
     meas = np.asarray(meas, dtype=np.uint8)
-    B, W1, N = meas.shape
+    B, W1 = meas.shape[0], meas.shape[1]
     Wr = W1 - 1
     D = w["w_e"].shape[0]
-    ev = detection_events(meas, types, d)
-    pe = positional_encoding((d + 1) ** 2, D)[grid_positions(d)]
-    state = np.zeros((B, N, D), dtype=np.float64)
+    tev = token_events(detection_events(meas, types, d), d, grid)
+    pos = np.array([r * (d + 1) + c for r, c in token_cells(d, grid)], dtype=np.int64)
+    pe = positional_encoding((d + 1) ** 2, D)[pos]
+    state = np.zeros((B, len(pos), D), dtype=np.float64)
     logits = np.zeros((B, d), dtype=np.float64)
     for n in range(1, Wr + 1):
-        S = embed(ev[:, n - 1, :], w, pe)
+        S = embed(tev[:, n - 1, :], w, pe)
         state = rnn_core(w["kappa"] * (S + state), w, H)
         if n > Wr - d:
-            logits[:, n - (Wr - d) - 1] = readout(state, types, w, d)
+            logits[:, n - (Wr - d) - 1] = readout(state, types, w, d, grid)
     return logits, (logits > 0).astype(np.uint8)
 
 
-def decode_stream(R: np.ndarray, w: dict, d: int, W: int, H: int) -> int:
+def decode_stream(R: np.ndarray, w: dict, d: int, W: int, H: int, grid: bool = False) -> int:
     """Decode a whole memory experiment: split, decode every window, XOR the bits."""
     meas, types = split_stream(R, d, W)
-    _, bits = forward_windows(meas, types, w, d, H)
+    _, bits = forward_windows(meas, types, w, d, H, grid=grid)
     return combine_bits(bits)

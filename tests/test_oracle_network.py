@@ -170,8 +170,9 @@ def test_fold_closed_form_without_layers():
     assert np.allclose(logits, O.readout(state, types, w, wl.d))
 
 
-def torch_model_logits(meas, types, w, wl):
-    """An independent float64 forward built from torch modules."""
+def torch_model_logits(meas, types, w, wl, grid=False):
+    """An independent float64 forward built from torch modules (grid: every cell of the
+    (d+1)x(d+1) array is a token, events only at stabilizer cells)."""
     d, D, H, F = wl.d, wl.D, wl.H, wl.F
     layers = []
     for lw in w["layers"]:
@@ -198,6 +199,12 @@ def torch_model_logits(meas, types, w, wl):
             ev[b, bl] = m_t[b, bl + 1]
         if types[b] == 2:
             ev[b, bl + d:] = 0
+    if grid:   # scatter the stabilizer events onto the grid; tokens = all cells
+        evg = torch.zeros(B, wl.W, (d + 1) ** 2, dtype=torch.float64)
+        for s, (r, c) in enumerate(cells):
+            evg[:, :, r * (d + 1) + c] = ev[:, :, s]
+        ev = evg
+        cells = [(r, c) for r in range(d + 1) for c in range(d + 1)]
     pos = torch.tensor([r * (d + 1) + c for r, c in cells], dtype=torch.float64)
     freq = 10000.0 ** (-torch.arange(0, D, 2, dtype=torch.float64) / D)
     ang = pos[:, None] * freq[None, :]
@@ -220,13 +227,14 @@ def torch_model_logits(meas, types, w, wl):
         return (feat @ lin.T)[:, 0].numpy() + w["b_o"][0] + w["beta"][types]
 
 
+@pytest.mark.parametrize("grid", [False, True], ids=["stabilizers", "grid"])
 @pytest.mark.parametrize("d,W,D,L,H", [(3, 6, 16, 2, 4), (3, 9, 32, 1, 2), (5, 10, 16, 2, 2)])
-def test_forward_matches_torch_model(d, W, D, L, H):
+def test_forward_matches_torch_model(d, W, D, L, H, grid):
     wl = synth.Workload("t", d, W, 6, 0.15, 0.0, D, L, H, 4, synth.DTYPE_F32)
     w = synth.make_weights(wl, seed=d + W)
     meas, types = synth.make_windows(wl, seed=11, realistic_boundaries=False)
-    logits, bits = O.forward_windows(meas, types, w, d, H)
-    ref = torch_model_logits(meas, types, w, wl)
+    logits, bits = O.forward_windows(meas, types, w, d, H, grid=grid)
+    ref = torch_model_logits(meas, types, w, wl, grid=grid)
     assert np.allclose(logits, ref, atol=1e-10)
     assert np.array_equal(bits, (logits > 0).astype(np.uint8))
 
@@ -285,3 +293,25 @@ def test_stream_decode_is_xor_of_windows():
     meas, types = O.split_stream(R, wl.d, wl.W)
     _, bits = O.forward_windows(meas, types, w, wl.d, wl.H)
     assert O.decode_stream(R, w, wl.d, wl.W, wl.H) == int(np.bitwise_xor.reduce(bits))
+
+
+def test_grid_tokens_fold_and_empty_cells():
+    """The (d+1)^2 token set with no transformer layers: the final state of every cell is
+    sum_k kappa^(W-k+1) S_k, where a cell without a stabilizer sees only b_e + PE; those cells
+    feed the readout, so the logits differ from the stabilizer-only token set."""
+    wl = tiny_workload(L=0, B=5, W=6)
+    w = synth.make_weights(wl, seed=3)
+    meas, types = synth.make_windows(wl, seed=7, realistic_boundaries=False)
+    d = wl.d
+    ev = O.token_events(O.detection_events(meas, types, d), d, grid=True)
+    assert ev.shape[-1] == (d + 1) ** 2 and ev.sum() == O.detection_events(meas, types, d).sum()
+    empty = [r * (d + 1) + c for r in range(d + 1) for c in range(d + 1)
+             if (r, c) not in set(O.stabilizer_cells(d))]
+    assert len(empty) == 2 * d + 2 and not ev[..., empty].any()   # (d+1)^2 - (d^2 - 1) cells
+    pe = O.positional_encoding((d + 1) ** 2, wl.D)
+    kappa = w["kappa"]
+    state = sum(kappa ** (wl.W - n) * O.embed(ev[:, n], w, pe) for n in range(wl.W))
+    logits, _ = O.forward_windows(meas, types, w, d, wl.H, grid=True)
+    assert np.allclose(logits, O.readout(state, types, w, d, grid=True))
+    stab, _ = O.forward_windows(meas, types, w, d, wl.H)
+    assert np.abs(logits - stab).max() > 1e-3
