@@ -47,18 +47,24 @@ typedef struct {
     int32_t max_windows;
 } pwd_geometry;
 
-/* Network dimensions (App. A model table): d_model, layers, heads, MLP expansion and the
- * arithmetic type. PWD_DTYPE_BF16: bf16 weights and matrix operands, fp32 accumulation,
- * softmax, LayerNorm, residual stream and recurrent state. PWD_DTYPE_F32: fp32 throughout. */
+/* Network dimensions (App. A model table): d_model, layers, heads, MLP expansion, the
+ * arithmetic type and the token set. PWD_DTYPE_BF16: bf16 weights and matrix operands, fp32
+ * accumulation, softmax, LayerNorm, residual stream and recurrent state. PWD_DTYPE_F32: fp32
+ * throughout. PWD_TOKENS_STABILIZERS: one token per stabilizer (d*d-1); PWD_TOKENS_GRID: one
+ * token per cell of the (d+1)x(d+1) stabilizer array (App. A.1.2 and the (d+1)^2 x d_model
+ * state of Algorithm 1), the cells without a stabilizer carrying state but no detection
+ * events. Syndrome inputs and detection events stay one bit per stabilizer either way. */
 typedef struct {
     int32_t d_model;
     int32_t n_layers;
     int32_t n_heads;
     int32_t mlp_ratio;
     int32_t dtype;
+    int32_t token_set;
 } pwd_model_dims;
 
 enum { PWD_DTYPE_F32 = 0, PWD_DTYPE_BF16 = 1 };
+enum { PWD_TOKENS_STABILIZERS = 0, PWD_TOKENS_GRID = 1 };
 
 /* Window types (App. A.1.1): the initial window has zero padding in place of its left
  * buffer, the final window in place of its right buffer. */
@@ -81,7 +87,7 @@ typedef enum {
  *     [2] distance  [3] window_rounds  [4] d_model  [5] n_layers  [6] n_heads
  *     [7] mlp hidden size F = mlp_ratio * d_model  [8] dtype
  *     [9] fold constant kappa (float32 bits; App. A.2 uses 0.707)
- *     [10] LayerNorm epsilon (float32 bits)  [11..15] zero
+ *     [10] LayerNorm epsilon (float32 bits)  [11] token set  [12..15] zero
  *   then float32 tensors, row-major, matrices stored [in][out] (y = x W + b):
  *     w_e[D], b_e[D]                                    StabilizerEmbedder Linear(1 -> D)
  *     per layer: Wq[D][D] bq[D] Wk[D][D] bk[D] Wv[D][D] bv[D] Wo[D][D] bo[D]
@@ -102,8 +108,9 @@ size_t decoder_blob_floats(const pwd_geometry* geom, const pwd_model_dims* dims)
  * Supported: distance odd in 3..63 with the on-chip limits below (bf16: up to 35 at head
  * sizes 16 and 32, up to 25 at 64); distance <= window_rounds <= 3*distance;
  * 1 <= max_windows <= 2^24; mlp_ratio = 4; n_layers 1..8;
+ * token_set PWD_TOKENS_STABILIZERS or PWD_TOKENS_GRID (n_tokens = d*d-1 or (d+1)^2);
  * PWD_DTYPE_BF16: d_model in {128, 256}, head size d_model/n_heads in {16, 32, 64}, and the
- * attention tile (K and V of one head: (2 ceil((d*d-1)/16) + 1) KB, twice that for head size
+ * attention tile (K and V of one head: (2 ceil(n_tokens/16) + 1) KB, twice that for head size
  * 64) within 160 KB of LDS;
  * PWD_DTYPE_F32: d_model in {16, 32, 64}, head size in {4, 8, 16, 32, 64} and
  * (d*d-1) * (3*d_model + 4*d_model) * 4 bytes within the on-chip budget (about d <= 5 at

@@ -80,7 +80,7 @@ template <int D>
 __global__ __launch_bounds__(THREADS) void f32_window_kernel(F32Params p) {
     constexpr int F = 4 * D;
     const int win = blockIdx.x;
-    const int N = p.in.N, H = p.H, dh = D / H, d = p.in.d;
+    const int N = p.ntok, H = p.H, dh = D / H, d = p.in.d;
     extern __shared__ __align__(16) float sm[];
     float* X = sm;                 // [N][D] state / residual stream
     float* Z = X + N * D;          // [N][D] scratch
@@ -90,7 +90,7 @@ __global__ __launch_bounds__(THREADS) void f32_window_kernel(F32Params p) {
     float* A = V + N * D;          // [N][D] attention output (heads concatenated)
     float* Hd = A + N * D;         // [N][F] feed-forward hidden
     float* S = Hd + N * F;         // [H][N][N] scores / probabilities
-    __shared__ uint32_t ev[32];    // event words of one round (N <= 1024)
+    __shared__ uint32_t ev[32];    // event words of one round (at most 1024 stabilizers)
     __shared__ float red[THREADS];
 
     const int type = p.in.types[win];
@@ -152,7 +152,8 @@ __global__ __launch_bounds__(THREADS) void f32_window_kernel(F32Params p) {
         // embedding + fold: X = kappa (E w_e + b_e + PE + X), X = 0 before round 0
         for (int idx = threadIdx.x; idx < N * D; idx += THREADS) {
             const int n = idx / D, k = idx % D;
-            const float e = (float)((ev[n >> 5] >> (n & 31)) & 1u);
+            const int st = p.tok_stab ? p.tok_stab[n] : n;   // the token's stabilizer, or -1
+            const float e = st >= 0 ? (float)((ev[st >> 5] >> (st & 31)) & 1u) : 0.f;
             const float s = fmaf(e, we[k], p.S0[idx]);
             X[idx] = p.kappa * (s + (t > 0 ? X[idx] : 0.f));
         }
@@ -208,7 +209,7 @@ __global__ __launch_bounds__(THREADS) void f32_window_kernel(F32Params p) {
 
 template <int D>
 hipError_t launch_d(const F32Params& p, hipStream_t s) {
-    const size_t smem = f32_window_smem_bytes(p.in.N, p.D, p.H, p.F);
+    const size_t smem = f32_window_smem_bytes(p.ntok, p.D, p.H, p.F);
     hipError_t e = hipFuncSetAttribute((const void*)f32_window_kernel<D>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     if (e != hipSuccess) return e;

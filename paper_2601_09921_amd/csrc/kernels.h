@@ -15,7 +15,9 @@ struct SyndromeIn {
 enum { TOK_POST = 1, TOK_EMBED = 2, TOK_QKV = 4 };
 
 struct TokParams {
-    SyndromeIn in;
+    SyndromeIn in;          // in.N: stabilizers (bits per measurement round)
+    int ntok;               // tokens per window (in.N, or (d+1)^2 for the grid token set)
+    const int* tok_stab;    // [ntok] stabilizer of each token or -1; null: token s = stabilizer s
     int Npad, nbw;          // padded tokens and 16-token blocks per window
     int t;                  // round whose embedding TOK_EMBED adds
     float kappa, eps;
@@ -63,9 +65,11 @@ struct EventsParams {
 };
 
 struct F32Params {
-    SyndromeIn in;
+    SyndromeIn in;          // in.N: stabilizers (bits per measurement round)
+    int ntok;               // tokens per window
+    const int* tok_stab;    // [ntok] stabilizer of each token or -1; null: token s = stabilizer s
     const float* w;         // blob tensors in blob order (fp32)
-    const float* S0;        // b_e + PE per token [N][D]
+    const float* S0;        // b_e + PE per token [ntok][D]
     const int* cell_token;  // [(d+1)*(d+1)]
     float* logits;          // logits[win * readouts + k] after round W - readouts + k
     uint8_t* bits;

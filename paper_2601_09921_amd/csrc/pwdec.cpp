@@ -126,6 +126,8 @@ size_t layer_floats(int D, int F) { return (size_t)4 * D * D + 2 * (size_t)D * F
 struct pwd_decoder {
     int device = 0;
     int d = 0, W = 0, max_windows = 0, N = 0, Npad = 0, nbw = 0, words = 0, b_left = 0;
+    int ntok = 0;                  // tokens per window (N stabilizers, or (d+1)^2 grid cells)
+    const int* tok_stab = nullptr; // grid token set: stabilizer of each token or -1
     int D = 0, L = 0, H = 0, F = 0, dh = 0, dtype = 0;
     float kappa = 0.f, eps = 0.f;
     int64_t n_tb_alloc = 0;
@@ -215,7 +217,9 @@ int decoder_validate_config(const pwd_geometry* g, const pwd_model_dims* m) {
     if (m->n_heads < 1 || m->d_model % m->n_heads != 0)
         return fail(PWD_EUNSUPPORTED, "d_model %d not divisible by n_heads %d", m->d_model, m->n_heads);
     const int dh = m->d_model / m->n_heads;
-    const int N = d * d - 1;
+    if (m->token_set != PWD_TOKENS_STABILIZERS && m->token_set != PWD_TOKENS_GRID)
+        return fail(PWD_EUNSUPPORTED, "token_set %d: need 0 (stabilizers) or 1 (grid)", m->token_set);
+    const int N = m->token_set == PWD_TOKENS_GRID ? (d + 1) * (d + 1) : d * d - 1;   // tokens
     if (m->dtype == PWD_DTYPE_BF16) {
         if (m->d_model != 128 && m->d_model != 256)
             return fail(PWD_EUNSUPPORTED, "bf16 d_model %d: need 128 or 256", m->d_model);
@@ -255,6 +259,8 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
     for (int i = 0; i < 7; ++i)
         if ((int)hdr[2 + i] != expect[i])
             return fail(PWD_EBLOB, "blob header word %d is %d, expected %d", 2 + i, (int)hdr[2 + i], expect[i]);
+    if ((int)hdr[11] != dims->token_set)
+        return fail(PWD_EBLOB, "blob header word 11 (token set) is %d, expected %d", (int)hdr[11], dims->token_set);
     float kappa, eps;
     std::memcpy(&kappa, &hdr[9], 4);
     std::memcpy(&eps, &hdr[10], 4);
@@ -270,16 +276,29 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
     dec->d = d;
     dec->W = geom->window_rounds;
     dec->max_windows = geom->max_windows;
+    const bool grid = dims->token_set == PWD_TOKENS_GRID;
     dec->N = d * d - 1;
-    dec->Npad = (dec->N + 15) / 16 * 16;
+    dec->ntok = grid ? (d + 1) * (d + 1) : dec->N;
+    dec->Npad = (dec->ntok + 15) / 16 * 16;
     dec->nbw = dec->Npad / 16;
     dec->words = (dec->N + 31) / 32;
     dec->b_left = (dec->W - d) / 2;
     dec->D = D; dec->L = L; dec->H = H; dec->F = F; dec->dh = D / H; dec->dtype = dims->dtype;
     dec->kappa = kappa; dec->eps = eps;
 
-    // geometry tables
-    const auto cells = stabilizer_cells(d);
+    // geometry tables: the cell of each token (grid: every cell, row-major), each cell's
+    // token (-1: none), and for the grid token set each token's stabilizer (-1: none)
+    const auto stab_cells = stabilizer_cells(d);
+    std::vector<std::pair<int, int>> cells = stab_cells;
+    std::vector<int> tok_stab;
+    if (grid) {
+        cells.clear();
+        tok_stab.assign((size_t)(d + 1) * (d + 1), -1);
+        for (int r = 0; r <= d; ++r)
+            for (int c = 0; c <= d; ++c) cells.push_back({r, c});
+        for (size_t s = 0; s < stab_cells.size(); ++s)
+            tok_stab[stab_cells[s].first * (d + 1) + stab_cells[s].second] = (int)s;
+    }
     std::vector<int> cell_token((size_t)(d + 1) * (d + 1), -1);
     for (size_t s = 0; s < cells.size(); ++s) cell_token[cells[s].first * (d + 1) + cells[s].second] = (int)s;
 
@@ -306,6 +325,7 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
         }
     };
     const size_t off_cell = put(cell_token.data(), cell_token.size() * sizeof(int));
+    const size_t off_tok_stab = grid ? put(tok_stab.data(), tok_stab.size() * sizeof(int)) : 0;
 
     struct LayerOff { size_t post, qkv, post_vecs, bqkv; };
     std::vector<LayerOff> loff(L);
@@ -315,7 +335,7 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
     if (dims->dtype == PWD_DTYPE_BF16) {
         const int RT = D / 16;
         std::vector<float> s0((size_t)dec->nbw * RT * 64 * 4, 0.f);
-        for (int s = 0; s < dec->N; ++s) {
+        for (int s = 0; s < dec->ntok; ++s) {
             pe_of(cells[s].first * (d + 1) + cells[s].second);
             const int blk = s / 16, cl = s % 16;
             for (int f = 0; f < D; ++f) {
@@ -362,8 +382,8 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
         off_bc = put(tail + 4 * (size_t)D * D, D * 4);
         off_wo = put(tail + 4 * (size_t)D * D + D, (size_t)d * D * 4);
     } else {
-        std::vector<float> s0((size_t)dec->N * D);
-        for (int s = 0; s < dec->N; ++s) {
+        std::vector<float> s0((size_t)dec->ntok * D);
+        for (int s = 0; s < dec->ntok; ++s) {
             pe_of(cells[s].first * (d + 1) + cells[s].second);
             for (int f = 0; f < D; ++f) s0[(size_t)s * D + f] = (float)((double)b_e[f] + pe_row[f]);
         }
@@ -390,6 +410,7 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
     auto fptr = [&](size_t off) { return reinterpret_cast<const float*>(base + off); };
     auto hptr = [&](size_t off) { return reinterpret_cast<const uint16_t*>(base + off); };
     dec->cell_token = reinterpret_cast<const int*>(base + off_cell);
+    if (grid) dec->tok_stab = reinterpret_cast<const int*>(base + off_tok_stab);
     dec->S0 = fptr(off_S0);
     if (dims->dtype == PWD_DTYPE_BF16) {
         dec->we = fptr(off_we);
@@ -484,6 +505,8 @@ static int decode_impl(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* 
         p.in = in;
         p.w = dec->f32w;
         p.S0 = dec->S0;
+        p.ntok = dec->ntok;
+        p.tok_stab = dec->tok_stab;
         p.cell_token = dec->cell_token;
         p.logits = d_logits;
         p.bits = d_bits;
@@ -508,6 +531,8 @@ static int decode_impl(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* 
     tp.QKV = dec->QKV;
     tp.Y = dec->Y;
     tp.S0 = dec->S0;
+    tp.ntok = dec->ntok;
+    tp.tok_stab = dec->tok_stab;
     tp.we = dec->we;
     auto set_post = [&](int l) {
         const auto& ly = dec->layers[l];
@@ -521,7 +546,7 @@ static int decode_impl(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* 
     AttnParams ap;
     ap.QKV = dec->QKV;
     ap.Y = dec->Y;
-    ap.N = dec->N;
+    ap.N = dec->ntok;
     ap.Npad = dec->Npad;
     ap.nbw = dec->nbw;
     ap.H = dec->H;

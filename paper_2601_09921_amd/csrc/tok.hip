@@ -339,13 +339,14 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(To
         for (int b = 0; b < TB; ++b) {
             const int64_t tb = tb0 + b;
             const int64_t w = tb / p.nbw;
-            const int s = (int)(tb - w * p.nbw) * 16 + col;
+            const int s = (int)(tb - w * p.nbw) * 16 + col;   // token
             ev[b] = 0.f;
-            if (w < p.in.nwin && s < p.in.N) {
+            const int st = s < p.ntok ? (p.tok_stab ? p.tok_stab[s] : s) : -1;   // its stabilizer
+            if (w < p.in.nwin && st >= 0) {
                 const uint32_t* m = p.in.meas + w * (int64_t)(p.in.W + 1) * p.in.words;
-                const uint32_t word = event_word(m, p.in.words, p.t, s >> 5, p.in.types[w],
+                const uint32_t word = event_word(m, p.in.words, p.t, st >> 5, p.in.types[w],
                                                  p.in.b_left, p.in.d);
-                ev[b] = (float)((word >> (s & 31)) & 1u);
+                ev[b] = (float)((word >> (st & 31)) & 1u);
             }
         }
     }
@@ -487,7 +488,7 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(To
         for (int b = 0; b < TB; ++b) {
             const int64_t tb = tb0 + b;
             const int blk = (int)(tb % p.nbw);
-            const bool real = blk * 16 + col < p.in.N;
+            const bool real = blk * 16 + col < p.ntok;
             const float e = ev[b];
 #pragma unroll
             for (int rt = 0; rt < RT; ++rt) {

@@ -36,7 +36,7 @@ class Geometry(ctypes.Structure):
 
 class ModelDims(ctypes.Structure):
     _fields_ = [("d_model", ctypes.c_int32), ("n_layers", ctypes.c_int32), ("n_heads", ctypes.c_int32),
-                ("mlp_ratio", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+                ("mlp_ratio", ctypes.c_int32), ("dtype", ctypes.c_int32), ("token_set", ctypes.c_int32)]
 
 
 NUM_STAGES = 9
@@ -97,17 +97,21 @@ def geometry(d: int, W: int, max_windows: int) -> Geometry:
     return Geometry(d, W, max_windows)
 
 
-def dims(D: int, L: int, H: int, mlp_ratio: int, dtype: int) -> ModelDims:
-    return ModelDims(D, L, H, mlp_ratio, dtype)
+TOKENS_STABILIZERS, TOKENS_GRID = 0, 1
 
 
-def make_blob(d: int, W: int, D: int, L: int, H: int, F: int, dtype: int, weights: dict) -> bytes:
+def dims(D: int, L: int, H: int, mlp_ratio: int, dtype: int, token_set: int = TOKENS_STABILIZERS) -> ModelDims:
+    return ModelDims(D, L, H, mlp_ratio, dtype, token_set)
+
+
+def make_blob(d: int, W: int, D: int, L: int, H: int, F: int, dtype: int, weights: dict,
+              token_set: int = TOKENS_STABILIZERS) -> bytes:
     """Serializes a weight dict into the library's blob format (header + fp32 tensors)."""
     kappa = np.float32(weights["kappa"])
     eps = np.float32(weights["eps"])
     hdr = [BLOB_MAGIC, BLOB_VERSION, d, W, D, L, H, F, dtype,
            struct.unpack("<I", struct.pack("<f", kappa))[0],
-           struct.unpack("<I", struct.pack("<f", eps))[0], 0, 0, 0, 0, 0]
+           struct.unpack("<I", struct.pack("<f", eps))[0], token_set, 0, 0, 0, 0]
     parts = [weights["w_e"], weights["b_e"]]
     for lw in weights["layers"]:
         parts += [lw[k] for k in ("Wq", "bq", "Wk", "bk", "Wv", "bv", "Wo", "bo", "g1", "be1",
@@ -128,13 +132,13 @@ class Decoder:
     """Owns one pwd_decoder handle."""
 
     def __init__(self, d: int, W: int, max_windows: int, D: int, L: int, H: int, mlp_ratio: int,
-                 dtype: int, blob: bytes):
+                 dtype: int, blob: bytes, token_set: int = TOKENS_STABILIZERS):
         lib = load_library()
         self._lib = lib
         self.d, self.W, self.max_windows = d, W, max_windows
         self.N = d * d - 1
         self.words = (self.N + 31) // 32
-        g, m = geometry(d, W, max_windows), dims(D, L, H, mlp_ratio, dtype)
+        g, m = geometry(d, W, max_windows), dims(D, L, H, mlp_ratio, dtype, token_set)
         h = ctypes.c_void_p()
         buf = ctypes.create_string_buffer(blob, len(blob))
         _check(lib.decoder_create(ctypes.byref(g), ctypes.byref(m), buf, len(blob), ctypes.byref(h)))
@@ -142,8 +146,9 @@ class Decoder:
 
     @classmethod
     def from_workload(cls, wl, weights: dict, max_windows: int | None = None) -> "Decoder":
-        blob = make_blob(wl.d, wl.W, wl.D, wl.L, wl.H, wl.F, wl.dtype, weights)
-        return cls(wl.d, wl.W, max_windows or wl.B, wl.D, wl.L, wl.H, wl.mlp_ratio, wl.dtype, blob)
+        ts = TOKENS_GRID if getattr(wl, "grid", False) else TOKENS_STABILIZERS
+        blob = make_blob(wl.d, wl.W, wl.D, wl.L, wl.H, wl.F, wl.dtype, weights, ts)
+        return cls(wl.d, wl.W, max_windows or wl.B, wl.D, wl.L, wl.H, wl.mlp_ratio, wl.dtype, blob, ts)
 
     def decode(self, meas, types, logits, bits, stream=None):
         """meas: int32/uint32 [n][W+1][words] cuda tensor; types: uint8 [n]; outputs float32/uint8 [n]."""

@@ -33,6 +33,8 @@ class Workload:
     pair_p: probability per round of one extra correlated flip of a diagonal stabilizer pair.
     D, L, H, mlp_ratio: model width, layers, heads and MLP expansion.
     dtype: DTYPE_F32 or DTYPE_BF16 (bf16 weights/activations, fp32 accumulation).
+    grid: run the network over all (d+1)^2 cells of the stabilizer array instead of the
+       d*d-1 stabilizers (inputs stay one bit per stabilizer).
     """
 
     name: str
@@ -46,6 +48,7 @@ class Workload:
     H: int
     mlp_ratio: int
     dtype: int
+    grid: bool = False
 
     @property
     def N(self) -> int:

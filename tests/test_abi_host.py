@@ -21,8 +21,8 @@ def test_exports_every_header_function(lib):
         assert hasattr(lib, n), n
 
 
-def validate(lib, d=7, W=14, B=16, D=128, L=3, H=8, r=4, dt=1):
-    g, m = pwdec.geometry(d, W, B), pwdec.dims(D, L, H, r, dt)
+def validate(lib, d=7, W=14, B=16, D=128, L=3, H=8, r=4, dt=1, ts=0):
+    g, m = pwdec.geometry(d, W, B), pwdec.dims(D, L, H, r, dt, ts)
     return lib.decoder_validate_config(ctypes.byref(g), ctypes.byref(m))
 
 
@@ -35,6 +35,7 @@ def test_workloads_are_supported(lib, wl):
     dict(d=4), dict(d=1), dict(d=65), dict(d=37, W=37), dict(d=27, W=27, D=256, H=4),
     dict(W=6), dict(W=22), dict(B=0), dict(r=5), dict(L=0),
     dict(H=3), dict(D=96, H=6), dict(D=128, H=1), dict(D=256, H=2), dict(dt=2), dict(dt=0, D=256, H=8),
+    dict(ts=2), dict(ts=-1), dict(ts=1, d=35, W=35),
     dict(dt=0, d=11, W=22, D=64, H=4),
 ])
 def test_rejects_unsupported(lib, kw):
@@ -46,11 +47,14 @@ def test_rejects_unsupported(lib, kw):
     dict(D=128, H=2), dict(D=256, H=4), dict(d=25, W=50, D=256, H=4), dict(d=25, W=75, D=128, H=2),
     dict(D=256, H=16), dict(dt=0, d=3, W=6, D=64, H=1),
     dict(d=27, W=54, D=256, H=8), dict(d=35, W=35, D=128, H=8), dict(d=35, W=105, D=256, H=8),
+    dict(ts=1), dict(ts=1, d=25, W=50, D=256, H=8), dict(ts=1, d=33, W=33), dict(ts=1, dt=0, d=3, W=6, D=64, H=4),
 ])
 def test_supported_head_sizes(lib, kw):
     """Head sizes 16, 32 and 64 on the bf16 path (LDS for K and V of one head of 64 at
     d = 25: 2 x 79 KB), 64 on the fp32 path, and distances past 25 while the attention tile
-    fits (d = 35, heads of 16 or 32: 155 KB; d = 37 and d = 27 with heads of 64 do not)."""
+    fits (d = 35, heads of 16 or 32: 155 KB; d = 37 and d = 27 with heads of 64 do not), and
+    the (d+1)^2 token set, whose tile is counted in grid tokens (d = 33: 1156 tokens fit,
+    d = 35: 1296 do not)."""
     assert validate(lib, **kw) == pwdec.PWD_OK
 
 
@@ -83,7 +87,7 @@ def corrupt(blob, word, value):
     return bytes(b)
 
 
-@pytest.mark.parametrize("how", ["magic", "version", "distance", "layers", "dtype", "short", "long"])
+@pytest.mark.parametrize("how", ["magic", "version", "distance", "layers", "dtype", "token_set", "short", "long"])
 def test_bad_blobs_rejected_before_device_use(lib, how):
     wl, blob = blob_for("d3")
     bad = {"magic": lambda b: corrupt(b, 0, 0x12345678),
@@ -91,6 +95,7 @@ def test_bad_blobs_rejected_before_device_use(lib, how):
            "distance": lambda b: corrupt(b, 2, 5),
            "layers": lambda b: corrupt(b, 5, 3),
            "dtype": lambda b: corrupt(b, 8, 1),
+           "token_set": lambda b: corrupt(b, 11, 1),
            "short": lambda b: b[:-4],
            "long": lambda b: b + b"\0\0\0\0"}[how](blob)
     g, m = pwdec.geometry(wl.d, wl.W, 4), pwdec.dims(wl.D, wl.L, wl.H, wl.mlp_ratio, wl.dtype)
