@@ -132,6 +132,25 @@ def recurrent_measurement(dec, wl, torch, dev_meas, dev_types):
             "readout_launches": ro_n, "readout_ms_total": round(ro_ms, 2)}
 
 
+def grid_measurement(wl, weights, torch, pwdec, dev_meas, dev_types):
+    """The same batch through the network with the (d+1)^2 token set (every cell of the
+    stabilizer array a token): one warm-up and one timed decode."""
+    import dataclasses
+    gwl = dataclasses.replace(wl, grid=True)
+    dec = pwdec.Decoder.from_workload(gwl, weights)
+    logits = torch.empty(wl.B, dtype=torch.float32, device="cuda")
+    bits = torch.empty(wl.B, dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    dec.decode(dev_meas, dev_types, logits, bits, stream)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    dec.decode(dev_meas, dev_types, logits, bits, stream)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    dec.close()
+    return {"tokens": (wl.d + 1) ** 2, "ms": round(dt * 1e3, 2), "us_per_round": dt / (wl.B * wl.d) * 1e6}
+
+
 def input_stage_measurement(dec, wl, torch, dev_meas, dev_types, reps=5):
     """The input stage on its own: decoder_detection_events over the batch (packed measurement
     rounds in, packed detection events out; the same event_word the token kernel fuses),
@@ -194,6 +213,7 @@ def main():
     ap.add_argument("--cpu-sample", type=int, default=3, help="oracle windows for the CPU baseline (0: skip)")
     ap.add_argument("--no-stream", action="store_true", help="skip the decode_stream measurement")
     ap.add_argument("--no-recurrent", action="store_true", help="skip the recurrent-readout measurement")
+    ap.add_argument("--no-grid", action="store_true", help="skip the (d+1)^2 token-set measurement")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first copy 1 GiB device-to-device 3 times (the known-size reference that "
                          "scales rocprofv3 FETCH_SIZE / WRITE_SIZE counters)")
@@ -310,6 +330,8 @@ def main():
     if not args.no_recurrent:
         out["recurrent"] = recurrent_measurement(dec, wl, torch, dev_meas, dev_types)
     dec.close()
+    if not args.no_grid and wl.dtype == synth.DTYPE_BF16:
+        out["grid_tokens"] = grid_measurement(wl, weights, torch, pwdec, dev_meas, dev_types)
     if args.cpu_sample > 0:
         out["cpu_baseline"] = cpu_baseline(wl, weights, args.cpu_sample)
     print(json.dumps(out), flush=True)

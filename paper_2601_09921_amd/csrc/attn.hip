@@ -26,6 +26,9 @@
 
 namespace {
 
+#ifndef ATTN_WIDE
+#define ATTN_WIDE 1
+#endif
 constexpr int KMAX_UNROLL = 8;        // key blocks per step of the max |k| scan
 
 PWD_DEV float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
@@ -439,9 +442,10 @@ PWD_DEV void attn_passes(const AttnShape& sh, const AttnItem& it, int qbeg, int 
     if (qend - qb == 1) run(std::integral_constant<int, 1>{}, qb);
 }
 
-// One workgroup per (window, head); K/V stay in LDS for the whole item.
+// One workgroup per (window, head); K/V stay in LDS for the whole item. Up to 4 wavefronts
+// two workgroups share a CU; 8 wavefronts (tiles above 80 KB) keep two per SIMD on their own.
 template <int DH, int WAVES>
-__global__ __launch_bounds__(WAVES * 64, 2) void attn_kernel(AttnParams p) {
+__global__ __launch_bounds__(WAVES * 64, WAVES == 8 ? 1 : 2) void attn_kernel(AttnParams p) {
     constexpr int NF = Frag<DH>::NF, QM = Frag<DH>::QMAX;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const AttnShape sh{p.N, p.nbw, p.H * DH / 32};
@@ -495,6 +499,8 @@ hipError_t launch_dh(const AttnParams& p, int nwin, hipStream_t s) {
     constexpr int QM = Frag<DH>::QMAX;
     if (p.nbw <= QM) return launch_shape<DH, 1>(p, nwin, s);
     if (p.nbw <= 2 * QM) return launch_shape<DH, 2>(p, nwin, s);
+    // a tile above 80 KB leaves room for one workgroup per CU: give it 8 wavefronts
+    if (ATTN_WIDE && attn_smem_bytes(DH, p.Npad, p.nbw) > 80 * 1024) return launch_shape<DH, 8>(p, nwin, s);
     return launch_shape<DH, 4>(p, nwin, s);
 }
 
