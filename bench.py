@@ -28,14 +28,14 @@ FP32_PEAK_TFLOPS = 157.3            # MI355X fp32 vector
 HBM_PEAK_GBS = 8000.0
 PAPER_US_PER_ROUND = {3: 0.781, 7: 0.789, 11: 0.812, 17: 0.841, 25: 0.979}   # one TPU v6e
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
-# Kernel names as rocprofv3 reports them for the d=25 workload (tok_kernel flags: POST=1,
-# EMBED=2, QKV=4).
+# Kernel names as rocprofv3 reports them for the d=25 workload (tok_kernel<d_model, MLP ratio,
+# flags>, flags POST=1, EMBED=2, QKV=4).
 STAGE_KERNELS = {
-    "embed_qkv": "tok_kernel<256, 6>",
+    "embed_qkv": "tok_kernel<256, 4, 6>",
     "attention": "attn_kernel<32, 4>",
-    "post_qkv": "tok_kernel<256, 5>",
-    "post_embed_qkv": "tok_kernel<256, 7>",
-    "post": "tok_kernel<256, 1>",
+    "post_qkv": "tok_kernel<256, 4, 5>",
+    "post_embed_qkv": "tok_kernel<256, 4, 7>",
+    "post": "tok_kernel<256, 4, 1>",
     "readout": "readout_kernel<256>",
     "fp32_window": "f32_window_kernel",
     "stream_split": "stream_split_kernel",

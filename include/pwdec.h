@@ -47,8 +47,9 @@ typedef struct {
     int32_t max_windows;
 } pwd_geometry;
 
-/* Network dimensions (App. A model table): d_model, layers, heads, MLP expansion, the
- * arithmetic type and the token set. PWD_DTYPE_BF16: bf16 weights and matrix operands, fp32
+/* Network dimensions (App. A model table): d_model, layers, heads, MLP expansion (the
+ * feed-forward width is mlp_ratio * d_model; the model table gives 5), the arithmetic type
+ * and the token set. PWD_DTYPE_BF16: bf16 weights and matrix operands, fp32
  * accumulation, softmax, LayerNorm, residual stream and recurrent state. PWD_DTYPE_F32: fp32
  * throughout. PWD_TOKENS_STABILIZERS: one token per stabilizer (d*d-1); PWD_TOKENS_GRID: one
  * token per cell of the (d+1)x(d+1) stabilizer array (App. A.1.2 and the (d+1)^2 x d_model
@@ -107,14 +108,14 @@ size_t decoder_blob_floats(const pwd_geometry* geom, const pwd_model_dims* dims)
 /* Checks geometry and dimensions on the host only; touches no device.
  * Supported: distance odd in 3..63 with the on-chip limits below (bf16: up to 35 at head
  * sizes 16 and 32, up to 25 at 64); distance <= window_rounds <= 3*distance;
- * 1 <= max_windows <= 2^24; mlp_ratio = 4; n_layers 1..8;
+ * 1 <= max_windows <= 2^24; mlp_ratio 4 or 5; n_layers 1..8;
  * token_set PWD_TOKENS_STABILIZERS or PWD_TOKENS_GRID (n_tokens = d*d-1 or (d+1)^2);
  * PWD_DTYPE_BF16: d_model in {128, 256}, head size d_model/n_heads in {16, 32, 64}, and the
  * attention tile (K and V of one head: (2 ceil(n_tokens/16) + 1) KB, twice that for head size
  * 64) within 160 KB of LDS;
- * PWD_DTYPE_F32: d_model in {16, 32, 64}, head size in {4, 8, 16, 32, 64} and
- * (d*d-1) * (3*d_model + 4*d_model) * 4 bytes within the on-chip budget (about d <= 5 at
- * d_model 64). Returns PWD_OK, PWD_EINVAL (null) or PWD_EUNSUPPORTED. */
+ * PWD_DTYPE_F32: d_model in {16, 32, 64}, head size in {4, 8, 16, 32, 64} and the window
+ * (n_tokens * (6 d_model + F) + n_heads * n_tokens^2) * 4 bytes within 64 KB of LDS (about
+ * d <= 5 at d_model 64). Returns PWD_OK, PWD_EINVAL (null) or PWD_EUNSUPPORTED. */
 int decoder_validate_config(const pwd_geometry* geom, const pwd_model_dims* dims);
 
 /* Creates a decoder on the current HIP device: validates, parses the blob (blob_bytes

@@ -76,9 +76,9 @@ PWD_DEV void layer_norm_rows(float* x, int N, const float* g, const float* b, fl
     }
 }
 
-template <int D>
+template <int D, int MR>
 __global__ __launch_bounds__(THREADS) void f32_window_kernel(F32Params p) {
-    constexpr int F = 4 * D;
+    constexpr int F = MR * D;   // feed-forward width
     const int win = blockIdx.x;
     const int N = p.ntok, H = p.H, dh = D / H, d = p.in.d;
     extern __shared__ __align__(16) float sm[];
@@ -207,14 +207,21 @@ __global__ __launch_bounds__(THREADS) void f32_window_kernel(F32Params p) {
     }
 }
 
-template <int D>
-hipError_t launch_d(const F32Params& p, hipStream_t s) {
+template <int D, int MR>
+hipError_t launch_dm(const F32Params& p, hipStream_t s) {
     const size_t smem = f32_window_smem_bytes(p.ntok, p.D, p.H, p.F);
-    hipError_t e = hipFuncSetAttribute((const void*)f32_window_kernel<D>,
+    hipError_t e = hipFuncSetAttribute((const void*)f32_window_kernel<D, MR>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     if (e != hipSuccess) return e;
-    f32_window_kernel<D><<<dim3((unsigned)p.in.nwin), dim3(THREADS), smem, s>>>(p);
+    f32_window_kernel<D, MR><<<dim3((unsigned)p.in.nwin), dim3(THREADS), smem, s>>>(p);
     return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_d(const F32Params& p, hipStream_t s) {
+    if (p.F == 4 * D) return launch_dm<D, 4>(p, s);
+    if (p.F == 5 * D) return launch_dm<D, 5>(p, s);
+    return hipErrorInvalidValue;
 }
 
 }  // namespace

@@ -82,7 +82,8 @@ struct F32Params {
 hipError_t launch_events(const EventsParams& p, hipStream_t s);
 int64_t tok_block_granule();
 int tok_mlp_chunk(int D);
-hipError_t launch_tok(int D, int flags, const TokParams& p, int64_t n_tb, hipStream_t s);
+int tok_bv_rep(int D, int F);
+hipError_t launch_tok(int D, int F, int flags, const TokParams& p, int64_t n_tb, hipStream_t s);
 hipError_t launch_attn(int dh, const AttnParams& p, int nwin, hipStream_t s);
 hipError_t launch_readout(const ReadoutParams& p, hipStream_t s);
 hipError_t launch_f32_window(const F32Params& p, hipStream_t s);

@@ -88,8 +88,9 @@ std::vector<std::pair<int, int>> stabilizer_cells(int d) {
 // fragments of its CH hidden units (row tile, k-step) followed by the W2 fragments of its
 // k-steps (row tile, k-step). qkv: per 32-feature output group og, per k-step, the two
 // row tiles 2og and 2og+1.
-void append_post_stream(std::vector<uint16_t>& out, const float* Wo, const float* W1, const float* W2, int D, int CH) {
-    const int F = 4 * D, RT = D / 16, KS = D / 32, FKS = F / 32;
+void append_post_stream(std::vector<uint16_t>& out, const float* Wo, const float* W1, const float* W2, int D, int F,
+                        int CH) {
+    const int RT = D / 16, KS = D / 32, FKS = F / 32;
     std::vector<uint16_t> fo, f1, f2;
     append_frags(fo, Wo, D, D);
     append_frags(f1, W1, D, F);
@@ -145,7 +146,7 @@ struct pwd_decoder {
     // views into `weights`
     struct Layer {
         const uint16_t *post, *qkv;
-        const float *post_vecs, *bqkv;   // [b_o g1 be1 b2 g2 be2 | b1] (10 D) and [b_q b_k | b_v x 4] (6 D)
+        const float *post_vecs, *bqkv;   // [b_o g1 be1 b2 g2 be2 | b1] (6 D + F) and [b_q b_k | b_v x rep]
     };
     std::vector<Layer> layers;
     const float* S0 = nullptr;
@@ -212,7 +213,8 @@ int decoder_validate_config(const pwd_geometry* g, const pwd_model_dims* m) {
         return fail(PWD_EUNSUPPORTED, "window_rounds %d: need %d..%d", g->window_rounds, d, 3 * d);
     if (g->max_windows < 1 || g->max_windows > (1 << 24))
         return fail(PWD_EUNSUPPORTED, "max_windows %d: need 1..2^24", g->max_windows);
-    if (m->mlp_ratio != 4) return fail(PWD_EUNSUPPORTED, "mlp_ratio %d: need 4", m->mlp_ratio);
+    if (m->mlp_ratio != 4 && m->mlp_ratio != 5)
+        return fail(PWD_EUNSUPPORTED, "mlp_ratio %d: need 4 or 5", m->mlp_ratio);
     if (m->n_layers < 1 || m->n_layers > 8) return fail(PWD_EUNSUPPORTED, "n_layers %d: need 1..8", m->n_layers);
     if (m->n_heads < 1 || m->d_model % m->n_heads != 0)
         return fail(PWD_EUNSUPPORTED, "d_model %d not divisible by n_heads %d", m->d_model, m->n_heads);
@@ -232,7 +234,7 @@ int decoder_validate_config(const pwd_geometry* g, const pwd_model_dims* m) {
             return fail(PWD_EUNSUPPORTED, "fp32 d_model %d: need 16, 32 or 64", m->d_model);
         if (dh != 4 && dh != 8 && dh != 16 && dh != 32 && dh != 64)
             return fail(PWD_EUNSUPPORTED, "fp32 head size %d: need 4, 8, 16, 32 or 64", dh);
-        const size_t smem = f32_window_smem_bytes(N, m->d_model, m->n_heads, 4 * m->d_model);
+        const size_t smem = f32_window_smem_bytes(N, m->d_model, m->n_heads, m->mlp_ratio * m->d_model);
         if (smem > 64 * 1024)
             return fail(PWD_EUNSUPPORTED, "fp32 window of %d tokens needs %zu bytes of LDS (max 65536)", N, smem);
     } else {
@@ -350,7 +352,8 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
             const float *Wq = p, *bq = Wq + D * D, *Wk = bq + D, *bk = Wk + D * D, *Wv = bk + D, *bv = Wv + D * D;
             const float *Wo = bv + D, *bo = Wo + D * D, *g1 = bo + D, *be1 = g1 + D, *W1 = be1 + D;
             const float *b1 = W1 + (size_t)D * F, *W2 = b1 + F, *b2 = W2 + (size_t)F * D, *g2 = b2 + D, *be2 = g2 + D;
-            std::vector<float> wqkv((size_t)D * 3 * D), bqkv(6 * D);
+            const int rep = tok_bv_rep(D, F);
+            std::vector<float> wqkv((size_t)D * 3 * D), bqkv((size_t)(2 + rep) * D);
             for (int k = 0; k < D; ++k)
                 for (int o = 0; o < D; ++o) {
                     wqkv[(size_t)k * 3 * D + o] = Wq[k * D + o];
@@ -360,10 +363,10 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
             for (int o = 0; o < D; ++o) {
                 bqkv[o] = bq[o];
                 bqkv[D + o] = bk[o];
-                for (int r = 0; r < 4; ++r) bqkv[2 * D + 4 * o + r] = bv[o];
+                for (int r = 0; r < rep; ++r) bqkv[2 * D + rep * o + r] = bv[o];
             }
             std::vector<uint16_t> fr;
-            append_post_stream(fr, Wo, W1, W2, D, tok_mlp_chunk(D));
+            append_post_stream(fr, Wo, W1, W2, D, F, tok_mlp_chunk(D));
             loff[l].post = put(fr.data(), fr.size() * 2);
             fr.clear();
             append_qkv_stream(fr, wqkv.data(), D);
@@ -372,7 +375,7 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
             for (const float* v : {bo, g1, be1, b2, g2, be2}) pv.insert(pv.end(), v, v + D);
             pv.insert(pv.end(), b1, b1 + F);
             loff[l].post_vecs = put(pv.data(), pv.size() * 4);
-            loff[l].bqkv = put(bqkv.data(), 6 * D * 4);
+            loff[l].bqkv = put(bqkv.data(), bqkv.size() * 4);
         }
         {
             std::vector<uint16_t> fr;
@@ -579,7 +582,7 @@ static int decode_impl(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* 
     // round 0: embed (state D_0 = 0) and project layer 0
     tp.t = 0;
     set_qkv(0);
-    HIP_OK(timed(dec, PWD_STAGE_EMBED_QKV, s, [&] { return launch_tok(dec->D, TOK_EMBED | TOK_QKV, tp, n_tb, s); }));
+    HIP_OK(timed(dec, PWD_STAGE_EMBED_QKV, s, [&] { return launch_tok(dec->D, dec->F, TOK_EMBED | TOK_QKV, tp, n_tb, s); }));
     for (int t = 0; t < dec->W; ++t) {
         const bool read_t = t >= dec->W - readouts;
         for (int l = 0; l < dec->L; ++l) {
@@ -587,18 +590,18 @@ static int decode_impl(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* 
             set_post(l);
             if (l + 1 < dec->L) {
                 set_qkv(l + 1);
-                HIP_OK(timed(dec, PWD_STAGE_POST_QKV, s, [&] { return launch_tok(dec->D, TOK_POST | TOK_QKV, tp, n_tb, s); }));
+                HIP_OK(timed(dec, PWD_STAGE_POST_QKV, s, [&] { return launch_tok(dec->D, dec->F, TOK_POST | TOK_QKV, tp, n_tb, s); }));
             } else if (t + 1 < dec->W) {
                 tp.t = t + 1;          // fold the next round's embedding into D_t
                 set_qkv(0);
                 // D_t for a readout goes to the Y buffer: each workgroup has read its own Y
                 // tiles by then, and the next writer of Y is the next round's attention
                 tp.state_out = read_t ? dec->Y : nullptr;
-                HIP_OK(timed(dec, PWD_STAGE_POST_EMBED_QKV, s, [&] { return launch_tok(dec->D, TOK_POST | TOK_EMBED | TOK_QKV, tp, n_tb, s); }));
+                HIP_OK(timed(dec, PWD_STAGE_POST_EMBED_QKV, s, [&] { return launch_tok(dec->D, dec->F, TOK_POST | TOK_EMBED | TOK_QKV, tp, n_tb, s); }));
                 tp.state_out = nullptr;
                 if (read_t) HIP_OK(readout(t - (dec->W - readouts), dec->Y));
             } else {
-                HIP_OK(timed(dec, PWD_STAGE_POST, s, [&] { return launch_tok(dec->D, TOK_POST, tp, n_tb, s); }));
+                HIP_OK(timed(dec, PWD_STAGE_POST, s, [&] { return launch_tok(dec->D, dec->F, TOK_POST, tp, n_tb, s); }));
             }
         }
     }

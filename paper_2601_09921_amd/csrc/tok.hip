@@ -38,12 +38,12 @@ template <int D, int FLAGS>
 constexpr int tok_waves() { return 4; }
 constexpr int TB = 2;
 
-template <int D, int NW>
+template <int D, int NW, int MR>
 struct Shape {
     static constexpr int CHUNK = 32;                  // weight fragments per LDS chunk
     static constexpr int RT = D / 16;                 // 16-row C tiles of a D-vector
     static constexpr int KS = D / 32;                 // 32-deep k-steps of a D-vector
-    static constexpr int F = 4 * D;
+    static constexpr int F = MR * D;                  // feed-forward width (MR = 4 or 5)
     static constexpr int CH = 8192 / D;               // hidden units per feed-forward chunk
     static constexpr int NMLP = F / CH;               // feed-forward sub-chunks (32 fragments each)
     static constexpr int MLP_PER = CHUNK / 32;        // feed-forward sub-chunks per LDS chunk
@@ -261,13 +261,21 @@ PWD_DEV void layer_norm(f32x4 (&x)[RT][TB], const float* gamma, const float* bet
     }
 }
 
-// Per-launch vectors staged in LDS once: [bo g1 be1 b2 g2 be2 | b1 (F) | bqkv (3D)].
-template <int D>
+// LDS of one workgroup (two per CU): the weight ring (two 32-fragment buffers) + vectors.
+constexpr int LDS_BUDGET = 80 * 1024, RING_BYTES = 2 * 32 * FRAG * 2;
+
+// b_v is stored with each value four times (the bias of a V tile is one column value per
+// lane, loaded as the f32x4 an accumulator starts from) where that fits in LDS, else once.
+constexpr int bv_rep(int D, int F) { return (12 * D + F) * 4 + RING_BYTES <= LDS_BUDGET ? 4 : 1; }
+
+// Per-launch vectors staged in LDS once: [bo g1 be1 b2 g2 be2 | b1 (F) | b_q b_k | b_v].
+template <int D, int F>
 struct Vecs {
     static constexpr int BO = 0, G1 = D, BE1 = 2 * D, B2 = 3 * D, G2 = 4 * D, BE2 = 5 * D;
-    // [b_q b_k] then b_v with each value four times (the bias of a V tile is one column value
-    // per lane, loaded as the f32x4 an accumulator starts from)
-    static constexpr int B1 = 6 * D, BQKV = 10 * D, BV4 = 12 * D, QKV_VECS = 6 * D, SIZE = 16 * D;
+    static constexpr int REP = bv_rep(D, F);
+    static constexpr int B1 = 6 * D, BQKV = 6 * D + F, BV = BQKV + 2 * D, QKV_VECS = (2 + REP) * D;
+    static constexpr int SIZE = BQKV + QKV_VECS;
+    static_assert(SIZE * 4 + RING_BYTES <= LDS_BUDGET, "vector table fits");
 };
 
 // Global stores a wavefront issues in one Q/K/V chunk after its last load of the next
@@ -290,12 +298,12 @@ PWD_DEV void static_for_impl(const F& f, std::integer_sequence<int, I...>) {
 template <int N, typename F>
 PWD_DEV void static_for(const F& f) { static_for_impl(f, std::make_integer_sequence<int, N>{}); }
 
-template <int D, int FLAGS>
+template <int D, int MR, int FLAGS>
 __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(TokParams p) {
     constexpr int WAVES = tok_waves<D, FLAGS>();
-    using S = Shape<D, WAVES>;
+    using S = Shape<D, WAVES, MR>;
     constexpr int LA_WO = TOK_LA_WO, LA_MLP = TOK_LA_MLP, LA_QKV = TOK_LA_QKV;
-    using V = Vecs<D>;
+    using V = Vecs<D, S::F>;
     constexpr int RT = S::RT, KS = S::KS, CH = S::CH;
     constexpr bool POST = (FLAGS & TOK_POST) != 0, QKV = (FLAGS & TOK_QKV) != 0;
     const int lane = threadIdx.x & 63;
@@ -352,8 +360,8 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(To
     }
 
     // Per-launch vectors, staged in LDS by direct loads of 256 bytes (64 lanes x 4 bytes):
-    // vec[0, 10 D) from the POST layer's vector table, vec[10 D, 13 D) the Q/K/V biases. The
-    // first chunk's sync awaits and publishes them.
+    // vec[0, 6 D + F) from the POST layer's vector table, then the Q/K/V biases. The first
+    // chunk's sync awaits and publishes them.
     __shared__ __align__(16) float vec[V::SIZE];
     {
         constexpr int NP_V = POST ? V::BQKV / 64 : 0, NQ_V = QKV ? V::QKV_VECS / 64 : 0;
@@ -547,7 +555,14 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(To
 #pragma unroll
                 for (int hh = 0; hh < 2; ++hh) {
                     if constexpr (VOUT) {   // bias along the tile's columns: lane col's value x 4
-                        const f32x4 bias = ld4(vec + V::BV4 + ((qc * OPC + o2 - 2 * KS) * 32 + hh * 16 + col) * 4);
+                        const int o = (qc * OPC + o2 - 2 * KS) * 32 + hh * 16 + col;
+                        f32x4 bias;
+                        if constexpr (V::REP == 4) {
+                            bias = ld4(vec + V::BV + o * 4);
+                        } else {
+                            const float bv = vec[V::BV + o];
+                            bias = f32x4{bv, bv, bv, bv};
+                        }
 #pragma unroll
                         for (int b = 0; b < TB; ++b) q[o2][hh][b] = bias;
                     } else {
@@ -595,21 +610,21 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(To
     asm volatile("s_waitcnt vmcnt(%0)" :: "n"(END_YOUNGER) : "memory");
 }
 
-template <int D, int FLAGS>
+template <int D, int MR, int FLAGS>
 void launch_variant(const TokParams& p, int64_t n_tb, hipStream_t s) {
     constexpr int WAVES = tok_waves<D, FLAGS>();
     const int64_t per_wg = (int64_t)WAVES * TB;
     const dim3 grid((unsigned)((n_tb + per_wg - 1) / per_wg)), block(WAVES * 64);
-    tok_kernel<D, FLAGS><<<grid, block, 0, s>>>(p);
+    tok_kernel<D, MR, FLAGS><<<grid, block, 0, s>>>(p);
 }
 
-template <int D>
+template <int D, int MR>
 hipError_t launch_tok_d(int flags, const TokParams& p, int64_t n_tb, hipStream_t s) {
     switch (flags) {
-        case TOK_EMBED | TOK_QKV: launch_variant<D, TOK_EMBED | TOK_QKV>(p, n_tb, s); break;
-        case TOK_POST | TOK_QKV: launch_variant<D, TOK_POST | TOK_QKV>(p, n_tb, s); break;
-        case TOK_POST | TOK_EMBED | TOK_QKV: launch_variant<D, TOK_POST | TOK_EMBED | TOK_QKV>(p, n_tb, s); break;
-        case TOK_POST: launch_variant<D, TOK_POST>(p, n_tb, s); break;
+        case TOK_EMBED | TOK_QKV: launch_variant<D, MR, TOK_EMBED | TOK_QKV>(p, n_tb, s); break;
+        case TOK_POST | TOK_QKV: launch_variant<D, MR, TOK_POST | TOK_QKV>(p, n_tb, s); break;
+        case TOK_POST | TOK_EMBED | TOK_QKV: launch_variant<D, MR, TOK_POST | TOK_EMBED | TOK_QKV>(p, n_tb, s); break;
+        case TOK_POST: launch_variant<D, MR, TOK_POST>(p, n_tb, s); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -624,9 +639,14 @@ int64_t tok_block_granule() { return 48; }
 // Fragments of the weight streams (see tok_kernel): hidden units per feed-forward chunk.
 int tok_mlp_chunk(int D) { return 8192 / D; }
 
-hipError_t launch_tok(int D, int flags, const TokParams& p, int64_t n_tb, hipStream_t s) {
+// Copies of each V bias value in the Q/K/V bias table: [b_q b_k] then b_v, each value rep times.
+int tok_bv_rep(int D, int F) { return bv_rep(D, F); }
+
+hipError_t launch_tok(int D, int F, int flags, const TokParams& p, int64_t n_tb, hipStream_t s) {
     if (n_tb <= 0) return hipSuccess;
-    if (D == 256) return launch_tok_d<256>(flags, p, n_tb, s);
-    if (D == 128) return launch_tok_d<128>(flags, p, n_tb, s);
+    if (D == 256 && F == 4 * D) return launch_tok_d<256, 4>(flags, p, n_tb, s);
+    if (D == 256 && F == 5 * D) return launch_tok_d<256, 5>(flags, p, n_tb, s);
+    if (D == 128 && F == 4 * D) return launch_tok_d<128, 4>(flags, p, n_tb, s);
+    if (D == 128 && F == 5 * D) return launch_tok_d<128, 5>(flags, p, n_tb, s);
     return hipErrorInvalidValue;
 }

@@ -33,7 +33,7 @@ def test_workloads_are_supported(lib, wl):
 
 @pytest.mark.parametrize("kw", [
     dict(d=4), dict(d=1), dict(d=65), dict(d=37, W=37), dict(d=27, W=27, D=256, H=4),
-    dict(W=6), dict(W=22), dict(B=0), dict(r=5), dict(L=0),
+    dict(W=6), dict(W=22), dict(B=0), dict(r=3), dict(r=6), dict(L=0),
     dict(H=3), dict(D=96, H=6), dict(D=128, H=1), dict(D=256, H=2), dict(dt=2), dict(dt=0, D=256, H=8),
     dict(ts=2), dict(ts=-1), dict(ts=1, d=35, W=35),
     dict(dt=0, d=11, W=22, D=64, H=4),
@@ -48,13 +48,15 @@ def test_rejects_unsupported(lib, kw):
     dict(D=256, H=16), dict(dt=0, d=3, W=6, D=64, H=1),
     dict(d=27, W=54, D=256, H=8), dict(d=35, W=35, D=128, H=8), dict(d=35, W=105, D=256, H=8),
     dict(ts=1), dict(ts=1, d=25, W=50, D=256, H=8), dict(ts=1, d=33, W=33), dict(ts=1, dt=0, d=3, W=6, D=64, H=4),
+    dict(r=5), dict(r=5, d=25, W=50, D=256, H=8), dict(r=5, dt=0, d=3, W=6, D=64, H=4),
 ])
 def test_supported_head_sizes(lib, kw):
     """Head sizes 16, 32 and 64 on the bf16 path (LDS for K and V of one head of 64 at
     d = 25: 2 x 79 KB), 64 on the fp32 path, and distances past 25 while the attention tile
-    fits (d = 35, heads of 16 or 32: 155 KB; d = 37 and d = 27 with heads of 64 do not), and
+    fits (d = 35, heads of 16 or 32: 155 KB; d = 37 and d = 27 with heads of 64 do not),
     the (d+1)^2 token set, whose tile is counted in grid tokens (d = 33: 1156 tokens fit,
-    d = 35: 1296 do not)."""
+    d = 35: 1296 do not), and feed-forward widths of 4 and 5 times d_model (3 and 6 are
+    rejected)."""
     assert validate(lib, **kw) == pwdec.PWD_OK
 
 

@@ -107,8 +107,9 @@ def test_attention_special_cases():
     assert np.allclose(O.attention(X[:, perm], lw, H), O.attention(X, lw, H)[:, perm])
 
 
-def test_transformer_layer_matches_torch():
-    D, H, N, F = 32, 4, 11, 128
+@pytest.mark.parametrize("F", [128, 160], ids=["ffn4", "ffn5"])
+def test_transformer_layer_matches_torch(F):
+    D, H, N = 32, 4, 11
     lw = layer_weights(D, F, seed=21)
     X = np.random.default_rng(5).standard_normal((3, N, D))
     m = torch.nn.TransformerEncoderLayer(D, H, F, dropout=0.0, activation="relu",
@@ -228,9 +229,10 @@ def torch_model_logits(meas, types, w, wl, grid=False):
 
 
 @pytest.mark.parametrize("grid", [False, True], ids=["stabilizers", "grid"])
-@pytest.mark.parametrize("d,W,D,L,H", [(3, 6, 16, 2, 4), (3, 9, 32, 1, 2), (5, 10, 16, 2, 2)])
-def test_forward_matches_torch_model(d, W, D, L, H, grid):
-    wl = synth.Workload("t", d, W, 6, 0.15, 0.0, D, L, H, 4, synth.DTYPE_F32)
+@pytest.mark.parametrize("d,W,D,L,H,r", [(3, 6, 16, 2, 4, 4), (3, 9, 32, 1, 2, 4), (5, 10, 16, 2, 2, 4),
+                                         (3, 6, 16, 2, 2, 5)])
+def test_forward_matches_torch_model(d, W, D, L, H, r, grid):
+    wl = synth.Workload("t", d, W, 6, 0.15, 0.0, D, L, H, r, synth.DTYPE_F32)
     w = synth.make_weights(wl, seed=d + W)
     meas, types = synth.make_windows(wl, seed=11, realistic_boundaries=False)
     logits, bits = O.forward_windows(meas, types, w, d, H, grid=grid)
