@@ -8,6 +8,8 @@ It follows the paper's statement of the method step by step:
   * the window decomposition of a syndrome stream (Sec. 3.1, eq. global_xor; App. A.1.1),
   * detection events from consecutive measurement rounds (Sec. 2.2, Sec. 3.2),
   * the stabilizer embedder and sinusoidal positional encoding (App. A.1, model table),
+    optionally with its residual block of two Conv1d layers over the flattened stabilizer
+    array ahead of the positional encoding (model table; syndrome-convolution section),
   * the recurrent fold D_n = RNNCore((S_n + D_{n-1}) * 0.707) with D_0 = 0
     (Algorithm 1 inference branch; App. A.2 fold equation),
   * Syndrome Transformer layers of multi-head self-attention and feed-forward (App. A.2),
@@ -19,6 +21,8 @@ the token set is the d*d-1 real stabilizers by default, with the paper's (d+1)^2
 option (grid=True); LayerNorm (post-norm, eps from the weights)
 replaces BatchNorm; ReLU feed-forward; attention has Q/K/V/O biases and scale 1/sqrt(dh);
 the readout convolution is followed by a bias and ReLU, pooling averages over columns;
+the embedder's Conv1d layers have kernel 3, zero padding 1, biases and a ReLU between them,
+and the block adds its input back (E + Conv2(ReLU(Conv1(E))));
 the window type adds a learned bias to the logit on top of the boundary padding masks.
 
 Everything is float64 numpy. Matrices are stored [in][out] so a projection is X @ W.
@@ -212,6 +216,40 @@ def embed(events_t: np.ndarray, w: dict, pe_tokens: np.ndarray) -> np.ndarray:
     return e * w["w_e"][None, None, :] + w["b_e"][None, None, :] + pe_tokens[None, :, :]
 
 
+def conv1d_same(x: np.ndarray, Wk: np.ndarray, b: np.ndarray) -> np.ndarray:
+    """Conv1d(D, D) with kernel 3 and zero padding 1 along the sequence axis:
+    y[p] = b + sum_{k=0..2} x[p+k-1] @ Wk[k], where x is zero outside the sequence.
+    x: [B][L][D]; Wk: [3][D][D] ([k][in][out])."""
+    L = x.shape[1]
+    y = np.broadcast_to(b, x.shape).astype(np.float64).copy()
+    for k in range(3):
+        off = k - 1
+        for p in range(L):
+            q = p + off
+            if 0 <= q < L:
+                y[:, p, :] += x[:, q, :] @ Wk[k]
+    return y
+
+
+def embed_round(events_t: np.ndarray, w: dict, d: int, grid: bool, pe_tokens: np.ndarray) -> np.ndarray:
+    """StabilizerEmbedder of one round with its residual Conv1d block (App. A model table:
+    Linear(1 -> D), then 2 x Conv1d(D, D); syndrome-convolution section: the ResNet runs on
+    the flattened (d+1)^2 array before PE is added).
+
+    events_t: [B][N] 0/1 stabilizer events. Every cell of the array gets E_lin = e * w_e +
+    b_e (e = 0 at a cell without a stabilizer); E_conv = E_lin + Conv2(ReLU(Conv1(E_lin)));
+    the tokens take E_conv at their cells plus PE. Without w["res"] this is embed().
+    """
+    if "res" not in w:
+        return embed(token_events(events_t, d, grid), w, pe_tokens)
+    e = token_events(events_t, d, True).astype(np.float64)[:, :, None]   # [B][(d+1)^2][1]
+    E = e * w["w_e"][None, None, :] + w["b_e"][None, None, :]
+    r = w["res"]
+    R = conv1d_same(np.maximum(conv1d_same(E, r["W1"], r["b1"]), 0.0), r["W2"], r["b2"])
+    cells = np.array([rr * (d + 1) + cc for rr, cc in token_cells(d, grid)], dtype=np.int64)
+    return (E + R)[:, cells, :] + pe_tokens[None, :, :]
+
+
 def layer_norm(y: np.ndarray, gamma: np.ndarray, beta: np.ndarray, eps: float) -> np.ndarray:
     """LayerNorm over the last axis with the biased variance."""
     mu = y.mean(axis=-1, keepdims=True)
@@ -299,12 +337,11 @@ def forward_windows(meas: np.ndarray, types: np.ndarray, w: dict, d: int, H: int
     W1 = meas.shape[1]
     D = w["w_e"].shape[0]
     ev = detection_events(meas, types, d)
-    tev = token_events(ev, d, grid)
     pos = np.array([r * (d + 1) + c for r, c in token_cells(d, grid)], dtype=np.int64)
     pe = positional_encoding((d + 1) ** 2, D)[pos]
     state = np.zeros((B, len(pos), D), dtype=np.float64)
     for n in range(W1 - 1):
-        S = embed(tev[:, n, :], w, pe)
+        S = embed_round(ev[:, n, :], w, d, grid, pe)
         state = rnn_core(w["kappa"] * (S + state), w, H)
     logits = readout(state, types, w, d, grid)
     bits = (logits > 0).astype(np.uint8)
@@ -326,13 +363,13 @@ def forward_windows_recurrent(meas: np.ndarray, types: np.ndarray, w: dict, d: i
     B, W1 = meas.shape[0], meas.shape[1]
     Wr = W1 - 1
     D = w["w_e"].shape[0]
-    tev = token_events(detection_events(meas, types, d), d, grid)
+    ev = detection_events(meas, types, d)
     pos = np.array([r * (d + 1) + c for r, c in token_cells(d, grid)], dtype=np.int64)
     pe = positional_encoding((d + 1) ** 2, D)[pos]
     state = np.zeros((B, len(pos), D), dtype=np.float64)
     logits = np.zeros((B, d), dtype=np.float64)
     for n in range(1, Wr + 1):
-        S = embed(tev[:, n - 1, :], w, pe)
+        S = embed_round(ev[:, n - 1, :], w, d, grid, pe)
         state = rnn_core(w["kappa"] * (S + state), w, H)
         if n > Wr - d:
             logits[:, n - (Wr - d) - 1] = readout(state, types, w, d, grid)

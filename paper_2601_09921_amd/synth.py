@@ -35,6 +35,8 @@ class Workload:
     dtype: DTYPE_F32 or DTYPE_BF16 (bf16 weights/activations, fp32 accumulation).
     grid: run the network over all (d+1)^2 cells of the stabilizer array instead of the
        d*d-1 stabilizers (inputs stay one bit per stabilizer).
+    resnet: add the embedder's residual block of two Conv1d(D, D, kernel 3) over the
+       flattened (d+1)^2 array (App. A model table and syndrome-convolution section).
     """
 
     name: str
@@ -49,6 +51,7 @@ class Workload:
     mlp_ratio: int
     dtype: int
     grid: bool = False
+    resnet: bool = False
 
     @property
     def N(self) -> int:
@@ -107,7 +110,8 @@ def make_weights(wl: Workload, seed: int = WEIGHT_SEED, gain: float = 1.0) -> di
     the GPU path and the oracle consume identical numbers.
 
     The draw order is fixed: embedding, then each layer (q, k, v, o, ln1, mlp1, mlp2, ln2),
-    then readout; each tensor is drawn in one call in row-major order.
+    then readout, then (resnet) the embedder's two Conv1d layers, weights [k][in][out]
+    N(0, 1/(3D)); each tensor is drawn in one call in row-major order.
     """
     rng = np.random.default_rng(seed)
     D, F, d = wl.D, wl.F, wl.d
@@ -137,6 +141,8 @@ def make_weights(wl: Workload, seed: int = WEIGHT_SEED, gain: float = 1.0) -> di
     w["w_o"] = rng.standard_normal((d, D)) / np.sqrt(d * D)
     w["b_o"] = np.array([0.01 * rng.standard_normal()])
     w["beta"] = 0.25 * rng.standard_normal(3)
+    if wl.resnet:   # drawn last, so the other tensors match the network without it
+        w["res"] = {"W1": mat(3 * D, (3, D, D)), "b1": bias(D), "W2": mat(3 * D, (3, D, D)), "b2": bias(D)}
     w["kappa"] = 0.707
     w["eps"] = 1e-5
     if wl.dtype == DTYPE_BF16:
@@ -151,6 +157,8 @@ def map_tensors(w: dict, fn) -> dict:
     for k, v in w.items():
         if k == "layers":
             out[k] = [{kk: fn(vv) for kk, vv in lw.items()} for lw in v]
+        elif k == "res":
+            out[k] = {kk: fn(vv) for kk, vv in v.items()}
         elif isinstance(v, np.ndarray):
             out[k] = fn(v)
         else:

@@ -200,12 +200,22 @@ def torch_model_logits(meas, types, w, wl, grid=False):
             ev[b, bl] = m_t[b, bl + 1]
         if types[b] == 2:
             ev[b, bl + d:] = 0
-    if grid:   # scatter the stabilizer events onto the grid; tokens = all cells
-        evg = torch.zeros(B, wl.W, (d + 1) ** 2, dtype=torch.float64)
-        for s, (r, c) in enumerate(cells):
-            evg[:, :, r * (d + 1) + c] = ev[:, :, s]
-        ev = evg
+    # the stabilizer events on the flattened grid (zeros at cells without a stabilizer)
+    evg = torch.zeros(B, wl.W, (d + 1) ** 2, dtype=torch.float64)
+    for s, (r, c) in enumerate(cells):
+        evg[:, :, r * (d + 1) + c] = ev[:, :, s]
+    if grid:   # tokens = all cells
         cells = [(r, c) for r in range(d + 1) for c in range(d + 1)]
+    cell_idx = [r * (d + 1) + c for r, c in cells]
+    convs = None
+    if "res" in w:   # the embedder's residual block as two torch Conv1d modules
+        convs = []
+        for k in ("1", "2"):
+            cv = torch.nn.Conv1d(D, D, 3, padding=1).double()
+            with torch.no_grad():
+                cv.weight.copy_(torch.tensor(np.transpose(w["res"]["W" + k], (2, 1, 0)).copy()))
+                cv.bias.copy_(torch.tensor(w["res"]["b" + k]))
+            convs.append(cv)
     pos = torch.tensor([r * (d + 1) + c for r, c in cells], dtype=torch.float64)
     freq = 10000.0 ** (-torch.arange(0, D, 2, dtype=torch.float64) / D)
     ang = pos[:, None] * freq[None, :]
@@ -213,7 +223,11 @@ def torch_model_logits(meas, types, w, wl, grid=False):
     state = torch.zeros(B, len(cells), D)
     with torch.no_grad():
         for n in range(wl.W):
-            S = ev[:, n, :, None] * torch.tensor(w["w_e"]) + torch.tensor(w["b_e"]) + pe
+            E = evg[:, n, :, None] * torch.tensor(w["w_e"]) + torch.tensor(w["b_e"])   # [B][cells][D]
+            if convs is not None:
+                Et = E.transpose(1, 2)
+                E = (Et + convs[1](torch.relu(convs[0](Et)))).transpose(1, 2)
+            S = E[:, cell_idx] + pe
             x = (S + state) * w["kappa"]
             for m in layers:
                 x = m(x)
@@ -229,10 +243,11 @@ def torch_model_logits(meas, types, w, wl, grid=False):
 
 
 @pytest.mark.parametrize("grid", [False, True], ids=["stabilizers", "grid"])
-@pytest.mark.parametrize("d,W,D,L,H,r", [(3, 6, 16, 2, 4, 4), (3, 9, 32, 1, 2, 4), (5, 10, 16, 2, 2, 4),
-                                         (3, 6, 16, 2, 2, 5)])
-def test_forward_matches_torch_model(d, W, D, L, H, r, grid):
-    wl = synth.Workload("t", d, W, 6, 0.15, 0.0, D, L, H, r, synth.DTYPE_F32)
+@pytest.mark.parametrize("d,W,D,L,H,r,res", [(3, 6, 16, 2, 4, 4, False), (3, 9, 32, 1, 2, 4, False),
+                                             (5, 10, 16, 2, 2, 4, False), (3, 6, 16, 2, 2, 5, False),
+                                             (3, 6, 16, 2, 4, 4, True), (5, 10, 16, 1, 2, 5, True)])
+def test_forward_matches_torch_model(d, W, D, L, H, r, res, grid):
+    wl = synth.Workload("t", d, W, 6, 0.15, 0.0, D, L, H, r, synth.DTYPE_F32, resnet=res)
     w = synth.make_weights(wl, seed=d + W)
     meas, types = synth.make_windows(wl, seed=11, realistic_boundaries=False)
     logits, bits = O.forward_windows(meas, types, w, d, H, grid=grid)
