@@ -62,10 +62,18 @@ typedef struct {
     int32_t mlp_ratio;
     int32_t dtype;
     int32_t token_set;
+    int32_t embedder;
 } pwd_model_dims;
 
 enum { PWD_DTYPE_F32 = 0, PWD_DTYPE_BF16 = 1 };
 enum { PWD_TOKENS_STABILIZERS = 0, PWD_TOKENS_GRID = 1 };
+/* PWD_EMBED_LINEAR: the embedding is Linear(1 -> d_model) of each event bit plus PE.
+ * PWD_EMBED_RESNET: the model table's StabilizerEmbedder, Linear(1 -> d_model) followed by a
+ * residual block of two Conv1d(d_model, d_model) layers along the flattened (d+1)x(d+1)
+ * stabilizer array, ahead of PE (syndrome-convolution section): with E the Linear output at
+ * every cell (e = 0 at cells without a stabilizer), E + Conv2(ReLU(Conv1(E))), kernel 3,
+ * zero padding 1, biases. */
+enum { PWD_EMBED_LINEAR = 0, PWD_EMBED_RESNET = 1 };
 
 /* Window types (App. A.1.1): the initial window has zero padding in place of its left
  * buffer, the final window in place of its right buffer. */
@@ -88,7 +96,7 @@ typedef enum {
  *     [2] distance  [3] window_rounds  [4] d_model  [5] n_layers  [6] n_heads
  *     [7] mlp hidden size F = mlp_ratio * d_model  [8] dtype
  *     [9] fold constant kappa (float32 bits; App. A.2 uses 0.707)
- *     [10] LayerNorm epsilon (float32 bits)  [11] token set  [12..15] zero
+ *     [10] LayerNorm epsilon (float32 bits)  [11] token set  [12] embedder  [13..15] zero
  *   then float32 tensors, row-major, matrices stored [in][out] (y = x W + b):
  *     w_e[D], b_e[D]                                    StabilizerEmbedder Linear(1 -> D)
  *     per layer: Wq[D][D] bq[D] Wk[D][D] bk[D] Wv[D][D] bv[D] Wo[D][D] bo[D]
@@ -96,6 +104,9 @@ typedef enum {
  *     Wc[2][2][D][D] bc[D]                              readout 2x2 convolution
  *     w_o[d][D] b_o[1]                                  readout Linear(d*D -> 1)
  *     beta[3]                                           logit bias per window type
+ *     PWD_EMBED_RESNET only: Wr1[3][D][D] br1[D] Wr2[3][D][D] br2[D]   the two Conv1d layers,
+ *                                                       weights [tap][in][out], tap k reading
+ *                                                       the cell at offset k - 1
  * For PWD_DTYPE_BF16 the values are used rounded to bf16 (they should already be
  * bf16-representable). The positional encoding is not stored: the library computes it. */
 #define PWD_BLOB_MAGIC 0x31445750u
@@ -110,6 +121,7 @@ size_t decoder_blob_floats(const pwd_geometry* geom, const pwd_model_dims* dims)
  * sizes 16 and 32, up to 25 at 64); distance <= window_rounds <= 3*distance;
  * 1 <= max_windows <= 2^24; mlp_ratio 4 or 5; n_layers 1..8;
  * token_set PWD_TOKENS_STABILIZERS or PWD_TOKENS_GRID (n_tokens = d*d-1 or (d+1)^2);
+ * embedder PWD_EMBED_LINEAR or PWD_EMBED_RESNET;
  * PWD_DTYPE_BF16: d_model in {128, 256}, head size d_model/n_heads in {16, 32, 64}, and the
  * attention tile (K and V of one head: (2 ceil(n_tokens/16) + 1) KB, twice that for head size
  * 64) within 160 KB of LDS;

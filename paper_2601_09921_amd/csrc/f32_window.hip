@@ -149,12 +149,21 @@ __global__ __launch_bounds__(THREADS) void f32_window_kernel(F32Params p) {
         for (int wd = threadIdx.x; wd < p.in.words; wd += THREADS)
             ev[wd] = type > WIN_FINAL ? 0u : event_word(meas, p.in.words, t, wd, type, p.in.b_left, d);
         __syncthreads();
-        // embedding + fold: X = kappa (E w_e + b_e + PE + X), X = 0 before round 0
+        // embedding + fold: X = kappa (E w_e + b_e + PE + X), X = 0 before round 0; with the
+        // embedder's residual block, plus its output looked up by the events of the five cells
+        // around the token's cell and the cell's position class
+        auto ev_bit = [&](int st) { return st >= 0 ? (ev[st >> 5] >> (st & 31)) & 1u : 0u; };
         for (int idx = threadIdx.x; idx < N * D; idx += THREADS) {
             const int n = idx / D, k = idx % D;
             const int st = p.tok_stab ? p.tok_stab[n] : n;   // the token's stabilizer, or -1
-            const float e = st >= 0 ? (float)((ev[st >> 5] >> (st & 31)) & 1u) : 0.f;
-            const float s = fmaf(e, we[k], p.S0[idx]);
+            const float e = (float)ev_bit(st);
+            float s = fmaf(e, we[k], p.S0[idx]);
+            if (p.emb_tab) {
+                const int* nb = p.emb_nb + n * 8;
+                uint32_t pat = 0u;
+                for (int j = 0; j < 5; ++j) pat |= ev_bit(nb[j]) << j;
+                s += p.emb_tab[(size_t)(nb[5] * 32 + (int)pat) * D + k];
+            }
             X[idx] = p.kappa * (s + (t > 0 ? X[idx] : 0.f));
         }
         __syncthreads();

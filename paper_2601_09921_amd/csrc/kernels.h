@@ -12,7 +12,7 @@ struct SyndromeIn {
 };
 
 // Stage flags of the token-local kernel.
-enum { TOK_POST = 1, TOK_EMBED = 2, TOK_QKV = 4 };
+enum { TOK_POST = 1, TOK_EMBED = 2, TOK_QKV = 4, TOK_RESNET = 8 };   // RESNET: with EMBED
 
 struct TokParams {
     SyndromeIn in;          // in.N: stabilizers (bits per measurement round)
@@ -33,6 +33,10 @@ struct TokParams {
     const float* post_vecs;   // POST layer vectors [b_o g1 be1 b2 g2 be2 | b1], 10 D floats
     const float* bqkv;      // [6D] bias of the Q/K/V projection: b_q, b_k, then b_v with each value x 4
     uint16_t* state_out;    // POST|EMBED: if not null, D_t (before the fold) as bf16 C fragments
+    // TOK_RESNET: the embedder's residual Conv1d block as a lookup (see pwdec.cpp)
+    const int* emb_nb;      // [ntok][8]: stabilizers at cells c-2 .. c+2 of the token's cell c
+                            // (-1: none), then the cell's position class (0..4), 0, 0
+    const float* emb_tab;   // [5 * 32][D]: block output by (position class, 5 event bits)
 };
 
 struct AttnParams {
@@ -75,6 +79,8 @@ struct F32Params {
     uint8_t* bits;
     int* err;
     int D, L, H, F;
+    const int* emb_nb;      // embedder residual block as in TokParams, or null
+    const float* emb_tab;
     int readouts;           // readouts after the last `readouts` rounds (1: final state only)
     float kappa, eps;
 };

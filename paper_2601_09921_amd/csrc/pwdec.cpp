@@ -3,6 +3,7 @@
 // fragments, device allocation and the per-round launch sequence (Algorithm 1).
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -122,6 +123,67 @@ void append_qkv_stream(std::vector<uint16_t>& out, const float* Wqkv, int D) {
 
 size_t layer_floats(int D, int F) { return (size_t)4 * D * D + 2 * (size_t)D * F + F + 9 * (size_t)D; }
 
+// The embedder's residual block (model table: 2 x Conv1d(D, D) after Linear(1 -> D); the
+// syndrome-convolution section puts it on the flattened (d+1)^2 array ahead of PE) as a
+// lookup. Its input at cell q is E(q) = e_q w_e + b_e, one event bit lifted to D features,
+// and zero outside the array (padding 1). Two kernel-3 layers make the output at cell c,
+//   R(c) = b2 + sum_{k=-1..1} [c+k in range] h(c+k) Wr2[k+1],
+//   h(p) = ReLU(b1 + sum_{k=-1..1} [p+k in range] E(p+k) Wr1[k+1]),
+// a function of the event bits at cells c-2 .. c+2 and of which of those cells exist; the
+// latter is one of five position classes (c = 0, c = 1, interior, c = L-2, c = L-1 with
+// L = (d+1)^2 >= 16). tab[class * 32 + bits] = R in double precision, rounded once.
+// nb[token] = the stabilizers at cells c-2 .. c+2 (-1: empty cell or outside), the class.
+void emb_tables(const std::vector<std::pair<int, int>>& cells, const std::vector<int>& cell_stab, int d,
+                int D, const float* w_e, const float* b_e, const float* res, std::vector<int>& nb,
+                std::vector<float>& tab) {
+    const int L = (d + 1) * (d + 1);
+    const float *W1 = res, *b1 = W1 + 3 * (size_t)D * D, *W2 = b1 + D, *b2 = W2 + 3 * (size_t)D * D;
+    auto cls_of = [&](int c) { return c == 0 ? 0 : c == 1 ? 1 : c == L - 2 ? 3 : c == L - 1 ? 4 : 2; };
+    nb.assign(cells.size() * 8, 0);
+    for (size_t s = 0; s < cells.size(); ++s) {
+        const int c = cells[s].first * (d + 1) + cells[s].second;
+        for (int j = 0; j < 5; ++j) {
+            const int q = c + j - 2;
+            nb[s * 8 + j] = q >= 0 && q < L ? cell_stab[q] : -1;
+        }
+        nb[s * 8 + 5] = cls_of(c);
+    }
+    const int rep_cell[5] = {0, 1, 2, L - 2, L - 1};
+    tab.assign((size_t)5 * 32 * D, 0.f);
+    std::vector<double> E(5 * (size_t)D), h(3 * (size_t)D), R(D);
+    for (int cls = 0; cls < 5; ++cls) {
+        const int c = rep_cell[cls];
+        auto in_range = [&](int off) { return c + off >= 0 && c + off < L; };
+        for (int pat = 0; pat < 32; ++pat) {
+            for (int j = 0; j < 5; ++j)   // E at offsets -2 .. 2
+                for (int f = 0; f < D; ++f)
+                    E[j * D + f] = in_range(j - 2) ? ((pat >> j) & 1) * (double)w_e[f] + b_e[f] : 0.0;
+            for (int pp = 0; pp < 3; ++pp) {   // h at offsets -1 .. 1
+                double* hp = &h[pp * D];
+                for (int o = 0; o < D; ++o) hp[o] = b1[o];
+                for (int k = 0; k < 3; ++k) {
+                    const int off = pp - 1 + k - 1;   // input offset
+                    if (!in_range(off)) continue;
+                    const double* x = &E[(off + 2) * D];
+                    const float* Wk = W1 + (size_t)k * D * D;
+                    for (int i = 0; i < D; ++i)
+                        for (int o = 0; o < D; ++o) hp[o] += x[i] * Wk[(size_t)i * D + o];
+                }
+                for (int o = 0; o < D; ++o) hp[o] = in_range(pp - 1) ? std::max(hp[o], 0.0) : 0.0;
+            }
+            for (int o = 0; o < D; ++o) R[o] = b2[o];
+            for (int k = 0; k < 3; ++k) {
+                if (!in_range(k - 1)) continue;
+                const double* x = &h[k * D];
+                const float* Wk = W2 + (size_t)k * D * D;
+                for (int i = 0; i < D; ++i)
+                    for (int o = 0; o < D; ++o) R[o] += x[i] * Wk[(size_t)i * D + o];
+            }
+            for (int o = 0; o < D; ++o) tab[((size_t)cls * 32 + pat) * D + o] = (float)R[o];
+        }
+    }
+}
+
 }  // namespace
 
 struct pwd_decoder {
@@ -155,6 +217,8 @@ struct pwd_decoder {
     const float* bc = nullptr;
     const float* wo = nullptr;
     const int* cell_token = nullptr;
+    const int* emb_nb = nullptr;   // embedder residual block (PWD_EMBED_RESNET): see emb_tables
+    const float* emb_tab = nullptr;
     const float* f32w = nullptr;   // fp32 path: the blob tensors as given
     float bo_out = 0.f, beta[3] = {0.f, 0.f, 0.f};
     // per-stage timing (decoder_profile)
@@ -200,8 +264,9 @@ const char* decoder_last_error(void) { return g_last_error.c_str(); }
 size_t decoder_blob_floats(const pwd_geometry* geom, const pwd_model_dims* dims) {
     if (!geom || !dims) return 0;
     const int D = dims->d_model, F = dims->mlp_ratio * dims->d_model, d = geom->distance;
+    const size_t res = dims->embedder == PWD_EMBED_RESNET ? 6 * (size_t)D * D + 2 * (size_t)D : 0;
     return 2 * (size_t)D + (size_t)dims->n_layers * layer_floats(D, F) + 4 * (size_t)D * D + D +
-           (size_t)d * D + 1 + 3;
+           (size_t)d * D + 1 + 3 + res;
 }
 
 int decoder_validate_config(const pwd_geometry* g, const pwd_model_dims* m) {
@@ -221,6 +286,8 @@ int decoder_validate_config(const pwd_geometry* g, const pwd_model_dims* m) {
     const int dh = m->d_model / m->n_heads;
     if (m->token_set != PWD_TOKENS_STABILIZERS && m->token_set != PWD_TOKENS_GRID)
         return fail(PWD_EUNSUPPORTED, "token_set %d: need 0 (stabilizers) or 1 (grid)", m->token_set);
+    if (m->embedder != PWD_EMBED_LINEAR && m->embedder != PWD_EMBED_RESNET)
+        return fail(PWD_EUNSUPPORTED, "embedder %d: need 0 (linear) or 1 (linear + residual Conv1d)", m->embedder);
     const int N = m->token_set == PWD_TOKENS_GRID ? (d + 1) * (d + 1) : d * d - 1;   // tokens
     if (m->dtype == PWD_DTYPE_BF16) {
         if (m->d_model != 128 && m->d_model != 256)
@@ -263,6 +330,8 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
             return fail(PWD_EBLOB, "blob header word %d is %d, expected %d", 2 + i, (int)hdr[2 + i], expect[i]);
     if ((int)hdr[11] != dims->token_set)
         return fail(PWD_EBLOB, "blob header word 11 (token set) is %d, expected %d", (int)hdr[11], dims->token_set);
+    if ((int)hdr[12] != dims->embedder)
+        return fail(PWD_EBLOB, "blob header word 12 (embedder) is %d, expected %d", (int)hdr[12], dims->embedder);
     float kappa, eps;
     std::memcpy(&kappa, &hdr[9], 4);
     std::memcpy(&eps, &hdr[10], 4);
@@ -328,6 +397,18 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
     };
     const size_t off_cell = put(cell_token.data(), cell_token.size() * sizeof(int));
     const size_t off_tok_stab = grid ? put(tok_stab.data(), tok_stab.size() * sizeof(int)) : 0;
+    size_t off_emb_nb = 0, off_emb_tab = 0;
+    if (dims->embedder == PWD_EMBED_RESNET) {
+        std::vector<int> cell_stab((size_t)(d + 1) * (d + 1), -1);
+        for (size_t s = 0; s < stab_cells.size(); ++s)
+            cell_stab[stab_cells[s].first * (d + 1) + stab_cells[s].second] = (int)s;
+        std::vector<int> nb;
+        std::vector<float> tab;
+        const float* res = w.data() + nf - (6 * (size_t)D * D + 2 * D);   // the blob's last tensors
+        emb_tables(cells, cell_stab, d, D, w.data(), w.data() + D, res, nb, tab);
+        off_emb_nb = put(nb.data(), nb.size() * sizeof(int));
+        off_emb_tab = put(tab.data(), tab.size() * sizeof(float));
+    }
 
     struct LayerOff { size_t post, qkv, post_vecs, bqkv; };
     std::vector<LayerOff> loff(L);
@@ -414,6 +495,10 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
     auto hptr = [&](size_t off) { return reinterpret_cast<const uint16_t*>(base + off); };
     dec->cell_token = reinterpret_cast<const int*>(base + off_cell);
     if (grid) dec->tok_stab = reinterpret_cast<const int*>(base + off_tok_stab);
+    if (dims->embedder == PWD_EMBED_RESNET) {
+        dec->emb_nb = reinterpret_cast<const int*>(base + off_emb_nb);
+        dec->emb_tab = fptr(off_emb_tab);
+    }
     dec->S0 = fptr(off_S0);
     if (dims->dtype == PWD_DTYPE_BF16) {
         dec->we = fptr(off_we);
@@ -510,6 +595,8 @@ static int decode_impl(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* 
         p.S0 = dec->S0;
         p.ntok = dec->ntok;
         p.tok_stab = dec->tok_stab;
+        p.emb_nb = dec->emb_nb;
+        p.emb_tab = dec->emb_tab;
         p.cell_token = dec->cell_token;
         p.logits = d_logits;
         p.bits = d_bits;
@@ -536,6 +623,9 @@ static int decode_impl(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* 
     tp.S0 = dec->S0;
     tp.ntok = dec->ntok;
     tp.tok_stab = dec->tok_stab;
+    tp.emb_nb = dec->emb_nb;
+    tp.emb_tab = dec->emb_tab;
+    const int RES = dec->emb_tab ? TOK_RESNET : 0;
     tp.we = dec->we;
     auto set_post = [&](int l) {
         const auto& ly = dec->layers[l];
@@ -582,7 +672,7 @@ static int decode_impl(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* 
     // round 0: embed (state D_0 = 0) and project layer 0
     tp.t = 0;
     set_qkv(0);
-    HIP_OK(timed(dec, PWD_STAGE_EMBED_QKV, s, [&] { return launch_tok(dec->D, dec->F, TOK_EMBED | TOK_QKV, tp, n_tb, s); }));
+    HIP_OK(timed(dec, PWD_STAGE_EMBED_QKV, s, [&] { return launch_tok(dec->D, dec->F, TOK_EMBED | TOK_QKV | RES, tp, n_tb, s); }));
     for (int t = 0; t < dec->W; ++t) {
         const bool read_t = t >= dec->W - readouts;
         for (int l = 0; l < dec->L; ++l) {
@@ -597,7 +687,7 @@ static int decode_impl(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* 
                 // D_t for a readout goes to the Y buffer: each workgroup has read its own Y
                 // tiles by then, and the next writer of Y is the next round's attention
                 tp.state_out = read_t ? dec->Y : nullptr;
-                HIP_OK(timed(dec, PWD_STAGE_POST_EMBED_QKV, s, [&] { return launch_tok(dec->D, dec->F, TOK_POST | TOK_EMBED | TOK_QKV, tp, n_tb, s); }));
+                HIP_OK(timed(dec, PWD_STAGE_POST_EMBED_QKV, s, [&] { return launch_tok(dec->D, dec->F, TOK_POST | TOK_EMBED | TOK_QKV | RES, tp, n_tb, s); }));
                 tp.state_out = nullptr;
                 if (read_t) HIP_OK(readout(t - (dec->W - readouts), dec->Y));
             } else {

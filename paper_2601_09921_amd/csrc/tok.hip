@@ -6,7 +6,11 @@
 //          post-norm residual blocks).
 //   EMBED: the stabilizer embedding of round t and the recurrent fold
 //          X = kappa * (E_t w_e + b_e + PE + X) (App. A.1 embedder and positional
-//          encoding; App. A.2 fold equation; Algorithm 1, D_0 = 0 at t = 0).
+//          encoding; App. A.2 fold equation; Algorithm 1, D_0 = 0 at t = 0). With RESNET
+//          the embedder's residual Conv1d block adds its output R, a function of the events
+//          at the five cells around the token's cell (two kernel-3 layers) and of how close
+//          the cell is to the ends of the flattened array, looked up in a host-built table.
+//          Its input is one bit per cell lifted by Linear(1 -> D), so the lookup is exact.
 //   QKV  : the Q, K, V projections of the following layer.
 // The residual stream stays fp32 in registers; only GEMM operands are rounded to bf16.
 // GEMMs are transposed (Out^T = W^T In^T) so tokens lie along MFMA columns: LayerNorm
@@ -341,7 +345,10 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(To
 
     // detection events of round t for this lane's token of each block (EMBED), computed while
     // few registers are live
+    constexpr bool RES = (FLAGS & TOK_RESNET) != 0;
+    static_assert(!RES || (FLAGS & TOK_EMBED) != 0, "the residual block is part of the embedding");
     float ev[TB];
+    int row[TB];   // RESNET: the token's row of the block's table
     if constexpr ((FLAGS & TOK_EMBED) != 0) {
 #pragma unroll
         for (int b = 0; b < TB; ++b) {
@@ -349,12 +356,28 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(To
             const int64_t w = tb / p.nbw;
             const int s = (int)(tb - w * p.nbw) * 16 + col;   // token
             ev[b] = 0.f;
+            row[b] = 0;
             const int st = s < p.ntok ? (p.tok_stab ? p.tok_stab[s] : s) : -1;   // its stabilizer
-            if (w < p.in.nwin && st >= 0) {
+            if (w < p.in.nwin) {
                 const uint32_t* m = p.in.meas + w * (int64_t)(p.in.W + 1) * p.in.words;
-                const uint32_t word = event_word(m, p.in.words, p.t, st >> 5, p.in.types[w],
-                                                 p.in.b_left, p.in.d);
-                ev[b] = (float)((word >> (st & 31)) & 1u);
+                const int type = p.in.types[w];
+                auto bit = [&](int q) -> uint32_t {   // event of stabilizer q in round t
+                    const uint32_t word = event_word(m, p.in.words, p.t, q >> 5, type, p.in.b_left, p.in.d);
+                    return (word >> (q & 31)) & 1u;
+                };
+                if (st >= 0) ev[b] = (float)bit(st);
+                if constexpr (RES) {
+                    if (s < p.ntok) {
+                        const int* nb = p.emb_nb + (size_t)s * 8;
+                        uint32_t pat = 0u;
+#pragma unroll
+                        for (int j = 0; j < 5; ++j) {
+                            const int q = nb[j];
+                            if (q >= 0) pat |= bit(q) << j;
+                        }
+                        row[b] = nb[5] * 32 + (int)pat;
+                    }
+                }
             }
         }
     }
@@ -500,8 +523,9 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(To
             const float e = ev[b];
 #pragma unroll
             for (int rt = 0; rt < RT; ++rt) {
-                const f32x4 s0 = ld4(p.S0 + (((int64_t)blk * RT + rt) * 64 + lane) * 4);
+                f32x4 s0 = ld4(p.S0 + (((int64_t)blk * RT + rt) * 64 + lane) * 4);
                 const f32x4 we = ld4(p.we + rt * 16 + 4 * g);
+                if constexpr (RES) s0 += ld4(p.emb_tab + (size_t)row[b] * D + rt * 16 + 4 * g);
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const float emb = real ? e * we[i] + s0[i] : 0.f;
@@ -625,6 +649,10 @@ hipError_t launch_tok_d(int flags, const TokParams& p, int64_t n_tb, hipStream_t
         case TOK_POST | TOK_QKV: launch_variant<D, MR, TOK_POST | TOK_QKV>(p, n_tb, s); break;
         case TOK_POST | TOK_EMBED | TOK_QKV: launch_variant<D, MR, TOK_POST | TOK_EMBED | TOK_QKV>(p, n_tb, s); break;
         case TOK_POST: launch_variant<D, MR, TOK_POST>(p, n_tb, s); break;
+        case TOK_EMBED | TOK_QKV | TOK_RESNET: launch_variant<D, MR, TOK_EMBED | TOK_QKV | TOK_RESNET>(p, n_tb, s); break;
+        case TOK_POST | TOK_EMBED | TOK_QKV | TOK_RESNET:
+            launch_variant<D, MR, TOK_POST | TOK_EMBED | TOK_QKV | TOK_RESNET>(p, n_tb, s);
+            break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

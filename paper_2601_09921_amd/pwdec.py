@@ -36,7 +36,8 @@ class Geometry(ctypes.Structure):
 
 class ModelDims(ctypes.Structure):
     _fields_ = [("d_model", ctypes.c_int32), ("n_layers", ctypes.c_int32), ("n_heads", ctypes.c_int32),
-                ("mlp_ratio", ctypes.c_int32), ("dtype", ctypes.c_int32), ("token_set", ctypes.c_int32)]
+                ("mlp_ratio", ctypes.c_int32), ("dtype", ctypes.c_int32), ("token_set", ctypes.c_int32),
+                ("embedder", ctypes.c_int32)]
 
 
 NUM_STAGES = 9
@@ -100,8 +101,12 @@ def geometry(d: int, W: int, max_windows: int) -> Geometry:
 TOKENS_STABILIZERS, TOKENS_GRID = 0, 1
 
 
-def dims(D: int, L: int, H: int, mlp_ratio: int, dtype: int, token_set: int = TOKENS_STABILIZERS) -> ModelDims:
-    return ModelDims(D, L, H, mlp_ratio, dtype, token_set)
+EMBED_LINEAR, EMBED_RESNET = 0, 1
+
+
+def dims(D: int, L: int, H: int, mlp_ratio: int, dtype: int, token_set: int = TOKENS_STABILIZERS,
+         embedder: int = EMBED_LINEAR) -> ModelDims:
+    return ModelDims(D, L, H, mlp_ratio, dtype, token_set, embedder)
 
 
 def make_blob(d: int, W: int, D: int, L: int, H: int, F: int, dtype: int, weights: dict,
@@ -111,12 +116,15 @@ def make_blob(d: int, W: int, D: int, L: int, H: int, F: int, dtype: int, weight
     eps = np.float32(weights["eps"])
     hdr = [BLOB_MAGIC, BLOB_VERSION, d, W, D, L, H, F, dtype,
            struct.unpack("<I", struct.pack("<f", kappa))[0],
-           struct.unpack("<I", struct.pack("<f", eps))[0], token_set, 0, 0, 0, 0]
+           struct.unpack("<I", struct.pack("<f", eps))[0], token_set,
+           EMBED_RESNET if "res" in weights else EMBED_LINEAR, 0, 0, 0]
     parts = [weights["w_e"], weights["b_e"]]
     for lw in weights["layers"]:
         parts += [lw[k] for k in ("Wq", "bq", "Wk", "bk", "Wv", "bv", "Wo", "bo", "g1", "be1",
                                   "W1", "b1", "W2", "b2", "g2", "be2")]
     parts += [weights["Wc"], weights["bc"], weights["w_o"], weights["b_o"], weights["beta"]]
+    if "res" in weights:
+        parts += [weights["res"][k] for k in ("W1", "b1", "W2", "b2")]
     body = np.concatenate([np.asarray(p, dtype=np.float64).ravel() for p in parts]).astype("<f4")
     return struct.pack("<16I", *hdr) + body.tobytes()
 
@@ -132,13 +140,13 @@ class Decoder:
     """Owns one pwd_decoder handle."""
 
     def __init__(self, d: int, W: int, max_windows: int, D: int, L: int, H: int, mlp_ratio: int,
-                 dtype: int, blob: bytes, token_set: int = TOKENS_STABILIZERS):
+                 dtype: int, blob: bytes, token_set: int = TOKENS_STABILIZERS, embedder: int = EMBED_LINEAR):
         lib = load_library()
         self._lib = lib
         self.d, self.W, self.max_windows = d, W, max_windows
         self.N = d * d - 1
         self.words = (self.N + 31) // 32
-        g, m = geometry(d, W, max_windows), dims(D, L, H, mlp_ratio, dtype, token_set)
+        g, m = geometry(d, W, max_windows), dims(D, L, H, mlp_ratio, dtype, token_set, embedder)
         h = ctypes.c_void_p()
         buf = ctypes.create_string_buffer(blob, len(blob))
         _check(lib.decoder_create(ctypes.byref(g), ctypes.byref(m), buf, len(blob), ctypes.byref(h)))
@@ -147,8 +155,9 @@ class Decoder:
     @classmethod
     def from_workload(cls, wl, weights: dict, max_windows: int | None = None) -> "Decoder":
         ts = TOKENS_GRID if getattr(wl, "grid", False) else TOKENS_STABILIZERS
+        emb = EMBED_RESNET if "res" in weights else EMBED_LINEAR
         blob = make_blob(wl.d, wl.W, wl.D, wl.L, wl.H, wl.F, wl.dtype, weights, ts)
-        return cls(wl.d, wl.W, max_windows or wl.B, wl.D, wl.L, wl.H, wl.mlp_ratio, wl.dtype, blob, ts)
+        return cls(wl.d, wl.W, max_windows or wl.B, wl.D, wl.L, wl.H, wl.mlp_ratio, wl.dtype, blob, ts, emb)
 
     def decode(self, meas, types, logits, bits, stream=None):
         """meas: int32/uint32 [n][W+1][words] cuda tensor; types: uint8 [n]; outputs float32/uint8 [n]."""

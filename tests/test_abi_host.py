@@ -1,6 +1,7 @@
 """Host-only checks of the C ABI: the library loads, exports every function the header
 declares, and validates configurations and weight blobs without touching a device."""
 import ctypes
+import dataclasses
 import struct
 
 import pytest
@@ -21,8 +22,8 @@ def test_exports_every_header_function(lib):
         assert hasattr(lib, n), n
 
 
-def validate(lib, d=7, W=14, B=16, D=128, L=3, H=8, r=4, dt=1, ts=0):
-    g, m = pwdec.geometry(d, W, B), pwdec.dims(D, L, H, r, dt, ts)
+def validate(lib, d=7, W=14, B=16, D=128, L=3, H=8, r=4, dt=1, ts=0, emb=0):
+    g, m = pwdec.geometry(d, W, B), pwdec.dims(D, L, H, r, dt, ts, emb)
     return lib.decoder_validate_config(ctypes.byref(g), ctypes.byref(m))
 
 
@@ -35,7 +36,7 @@ def test_workloads_are_supported(lib, wl):
     dict(d=4), dict(d=1), dict(d=65), dict(d=37, W=37), dict(d=27, W=27, D=256, H=4),
     dict(W=6), dict(W=22), dict(B=0), dict(r=3), dict(r=6), dict(L=0),
     dict(H=3), dict(D=96, H=6), dict(D=128, H=1), dict(D=256, H=2), dict(dt=2), dict(dt=0, D=256, H=8),
-    dict(ts=2), dict(ts=-1), dict(ts=1, d=35, W=35),
+    dict(ts=2), dict(ts=-1), dict(ts=1, d=35, W=35), dict(emb=2), dict(emb=-1),
     dict(dt=0, d=11, W=22, D=64, H=4),
 ])
 def test_rejects_unsupported(lib, kw):
@@ -49,6 +50,7 @@ def test_rejects_unsupported(lib, kw):
     dict(d=27, W=54, D=256, H=8), dict(d=35, W=35, D=128, H=8), dict(d=35, W=105, D=256, H=8),
     dict(ts=1), dict(ts=1, d=25, W=50, D=256, H=8), dict(ts=1, d=33, W=33), dict(ts=1, dt=0, d=3, W=6, D=64, H=4),
     dict(r=5), dict(r=5, d=25, W=50, D=256, H=8), dict(r=5, dt=0, d=3, W=6, D=64, H=4),
+    dict(emb=1), dict(emb=1, ts=1, d=25, W=50, D=256, H=8), dict(emb=1, dt=0, d=3, W=6, D=64, H=4),
 ])
 def test_supported_head_sizes(lib, kw):
     """Head sizes 16, 32 and 64 on the bf16 path (LDS for K and V of one head of 64 at
@@ -81,6 +83,13 @@ def test_blob_size_matches_header_formula(lib, name):
     wl, blob = blob_for(name)
     g, m = pwdec.geometry(wl.d, wl.W, 4), pwdec.dims(wl.D, wl.L, wl.H, wl.mlp_ratio, wl.dtype)
     assert len(blob) == 64 + 4 * lib.decoder_blob_floats(ctypes.byref(g), ctypes.byref(m))
+    # with the embedder's residual block: two Conv1d(D, D, 3) layers and their biases more
+    rw = dataclasses.replace(wl, resnet=True)
+    rblob = pwdec.make_blob(rw.d, rw.W, rw.D, rw.L, rw.H, rw.F, rw.dtype, synth.make_weights(rw))
+    assert struct.unpack("<I", rblob[48:52])[0] == pwdec.EMBED_RESNET
+    m = pwdec.dims(wl.D, wl.L, wl.H, wl.mlp_ratio, wl.dtype, 0, pwdec.EMBED_RESNET)
+    assert len(rblob) == 64 + 4 * lib.decoder_blob_floats(ctypes.byref(g), ctypes.byref(m))
+    assert len(rblob) - len(blob) == 4 * (6 * wl.D * wl.D + 2 * wl.D)
 
 
 def corrupt(blob, word, value):
@@ -89,7 +98,8 @@ def corrupt(blob, word, value):
     return bytes(b)
 
 
-@pytest.mark.parametrize("how", ["magic", "version", "distance", "layers", "dtype", "token_set", "short", "long"])
+@pytest.mark.parametrize("how", ["magic", "version", "distance", "layers", "dtype", "token_set", "embedder",
+                                 "short", "long"])
 def test_bad_blobs_rejected_before_device_use(lib, how):
     wl, blob = blob_for("d3")
     bad = {"magic": lambda b: corrupt(b, 0, 0x12345678),
@@ -98,6 +108,7 @@ def test_bad_blobs_rejected_before_device_use(lib, how):
            "layers": lambda b: corrupt(b, 5, 3),
            "dtype": lambda b: corrupt(b, 8, 1),
            "token_set": lambda b: corrupt(b, 11, 1),
+           "embedder": lambda b: corrupt(b, 12, 1),
            "short": lambda b: b[:-4],
            "long": lambda b: b + b"\0\0\0\0"}[how](blob)
     g, m = pwdec.geometry(wl.d, wl.W, 4), pwdec.dims(wl.D, wl.L, wl.H, wl.mlp_ratio, wl.dtype)
