@@ -13,6 +13,8 @@ It follows the paper's statement of the method step by step:
   * the recurrent fold D_n = RNNCore((S_n + D_{n-1}) * 0.707) with D_0 = 0
     (Algorithm 1 inference branch; App. A.2 fold equation),
   * Syndrome Transformer layers of multi-head self-attention and feed-forward (App. A.2),
+    optionally with the dilated convolutions over the 2-D stabilizer array (model table;
+    App. A.2 text: the attention output is scattered onto the grid for them),
   * the readout: 2x2 valid convolution, logical pooling, linear projection (App. A.3),
   * the XOR combination of per-window bits (eq. global_xor).
 
@@ -23,6 +25,10 @@ replaces BatchNorm; ReLU feed-forward; attention has Q/K/V/O biases and scale 1/
 the readout convolution is followed by a bias and ReLU, pooling averages over columns;
 the embedder's Conv1d layers have kernel 3, zero padding 1, biases and a ReLU between them,
 and the block adds its input back (E + Conv2(ReLU(Conv1(E))));
+the dilated convolutions sit between the attention block (after LayerNorm 1) and the
+feed-forward, need the (d+1)^2 token set (every cell a token), and are three residual units
+C = C + ReLU(Conv2d_j(C)), 3x3 kernels with dilations from the weights and zero padding equal
+to the dilation (the grid keeps its size);
 the window type adds a learned bias to the logit on top of the boundary padding masks.
 
 Everything is float64 numpy. Matrices are stored [in][out] so a projection is X @ W.
@@ -288,15 +294,48 @@ def feed_forward(X: np.ndarray, lw: dict) -> np.ndarray:
     return np.maximum(X @ lw["W1"] + lw["b1"], 0.0) @ lw["W2"] + lw["b2"]
 
 
-def transformer_layer(X: np.ndarray, lw: dict, H: int, eps: float) -> np.ndarray:
-    """One Syndrome Transformer layer, post-norm: X = LN1(X + MHA(X)); X = LN2(X + FF(X))."""
+def conv2d_dilated(G: np.ndarray, Wk: np.ndarray, b: np.ndarray, dil: int) -> np.ndarray:
+    """Conv2d(D, D) with a 3x3 kernel, dilation dil and zero padding dil on a square grid:
+    y[r][c] = b + sum_{a,e in 0..2} x[r + dil (a-1)][c + dil (e-1)] @ Wk[a][e], where x is
+    zero outside the grid. G: [B][S][S][D]; Wk: [3][3][D][D] ([a][e][in][out])."""
+    S = G.shape[1]
+    y = np.broadcast_to(b, G.shape).astype(np.float64).copy()
+    for a in range(3):
+        for e in range(3):
+            dr, dc = dil * (a - 1), dil * (e - 1)
+            for r in range(S):
+                for c in range(S):
+                    rr, cc = r + dr, c + dc
+                    if 0 <= rr < S and 0 <= cc < S:
+                        y[:, r, c, :] += G[:, rr, cc, :] @ Wk[a, e]
+    return y
+
+
+def dilated_block(X: np.ndarray, lw: dict, dilations) -> np.ndarray:
+    """The Syndrome Transformer's dilated convolutions (model table: 3 x Conv2d(D, D)) on
+    the (d+1) x (d+1) grid of tokens X [B][(d+1)^2][D] (row-major cells): three residual
+    units C = C + ReLU(Conv2d_j(C)) with the given dilations."""
+    B, N, D = X.shape
+    S = int(round(math.sqrt(N)))
+    assert S * S == N, "the dilated convolutions need one token per grid cell"
+    G = X.reshape(B, S, S, D)
+    for j, dil in enumerate(dilations):
+        G = G + np.maximum(conv2d_dilated(G, lw["Wd"][j], lw["bd"][j], dil), 0.0)
+    return G.reshape(B, N, D)
+
+
+def transformer_layer(X: np.ndarray, lw: dict, H: int, eps: float, dilations=None) -> np.ndarray:
+    """One Syndrome Transformer layer, post-norm: X = LN1(X + MHA(X)); with dilated
+    convolutions X = DilatedBlock(X); X = LN2(X + FF(X))."""
     X = layer_norm(X + attention(X, lw, H), lw["g1"], lw["be1"], eps)
+    if dilations:
+        X = dilated_block(X, lw, dilations)
     return layer_norm(X + feed_forward(X, lw), lw["g2"], lw["be2"], eps)
 
 
 def rnn_core(X: np.ndarray, w: dict, H: int) -> np.ndarray:
     for lw in w["layers"]:
-        X = transformer_layer(X, lw, H, w["eps"])
+        X = transformer_layer(X, lw, H, w["eps"], w.get("dilations"))
     return X
 
 

@@ -37,6 +37,8 @@ class Workload:
        d*d-1 stabilizers (inputs stay one bit per stabilizer).
     resnet: add the embedder's residual block of two Conv1d(D, D, kernel 3) over the
        flattened (d+1)^2 array (App. A model table and syndrome-convolution section).
+    dil: dilations of the three 3x3 Conv2d(D, D) units each layer runs on the grid between
+       attention and feed-forward (model table); empty: none. Needs grid=True.
     """
 
     name: str
@@ -52,6 +54,7 @@ class Workload:
     dtype: int
     grid: bool = False
     resnet: bool = False
+    dil: tuple = ()
 
     @property
     def N(self) -> int:
@@ -111,7 +114,8 @@ def make_weights(wl: Workload, seed: int = WEIGHT_SEED, gain: float = 1.0) -> di
 
     The draw order is fixed: embedding, then each layer (q, k, v, o, ln1, mlp1, mlp2, ln2),
     then readout, then (resnet) the embedder's two Conv1d layers, weights [k][in][out]
-    N(0, 1/(3D)); each tensor is drawn in one call in row-major order.
+    N(0, 1/(3D)), then (dil) per layer the three dilated Conv2d layers, weights
+    [j][a][e][in][out] N(0, 1/(9D)); each tensor is drawn in one call in row-major order.
     """
     rng = np.random.default_rng(seed)
     D, F, d = wl.D, wl.F, wl.d
@@ -143,6 +147,11 @@ def make_weights(wl: Workload, seed: int = WEIGHT_SEED, gain: float = 1.0) -> di
     w["beta"] = 0.25 * rng.standard_normal(3)
     if wl.resnet:   # drawn last, so the other tensors match the network without it
         w["res"] = {"W1": mat(3 * D, (3, D, D)), "b1": bias(D), "W2": mat(3 * D, (3, D, D)), "b2": bias(D)}
+    if wl.dil:      # after that, for the same reason
+        assert len(wl.dil) == 3
+        w["dilations"] = list(wl.dil)
+        for lw in w["layers"]:
+            lw["Wd"], lw["bd"] = mat(9 * D, (3, 3, 3, D, D)), bias((3, D))
     w["kappa"] = 0.707
     w["eps"] = 1e-5
     if wl.dtype == DTYPE_BF16:
