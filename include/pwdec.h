@@ -63,6 +63,7 @@ typedef struct {
     int32_t dtype;
     int32_t token_set;
     int32_t embedder;
+    int32_t conv_dilation[3];
 } pwd_model_dims;
 
 enum { PWD_DTYPE_F32 = 0, PWD_DTYPE_BF16 = 1 };
@@ -74,6 +75,12 @@ enum { PWD_TOKENS_STABILIZERS = 0, PWD_TOKENS_GRID = 1 };
  * every cell (e = 0 at cells without a stabilizer), E + Conv2(ReLU(Conv1(E))), kernel 3,
  * zero padding 1, biases. */
 enum { PWD_EMBED_LINEAR = 0, PWD_EMBED_RESNET = 1 };
+/* conv_dilation: all zero, or the dilations (1..distance) of the Syndrome Transformer's three
+ * dilated convolutions (model table: 3 x Conv2d(d_model, d_model); App. A.2: the attention
+ * output scattered onto the 2-D grid). Each layer then runs, between LayerNorm 1 and the
+ * feed-forward, three residual units C = C + ReLU(b_j + Conv2d_j(C)) with 3x3 kernels,
+ * dilation conv_dilation[j] and zero padding equal to it, over the (d+1)x(d+1) grid. They
+ * need the PWD_TOKENS_GRID token set (every cell a token). */
 
 /* Window types (App. A.1.1): the initial window has zero padding in place of its left
  * buffer, the final window in place of its right buffer. */
@@ -96,7 +103,8 @@ typedef enum {
  *     [2] distance  [3] window_rounds  [4] d_model  [5] n_layers  [6] n_heads
  *     [7] mlp hidden size F = mlp_ratio * d_model  [8] dtype
  *     [9] fold constant kappa (float32 bits; App. A.2 uses 0.707)
- *     [10] LayerNorm epsilon (float32 bits)  [11] token set  [12] embedder  [13..15] zero
+ *     [10] LayerNorm epsilon (float32 bits)  [11] token set  [12] embedder
+ *     [13] conv dilations, byte j = conv_dilation[j]  [14..15] zero
  *   then float32 tensors, row-major, matrices stored [in][out] (y = x W + b):
  *     w_e[D], b_e[D]                                    StabilizerEmbedder Linear(1 -> D)
  *     per layer: Wq[D][D] bq[D] Wk[D][D] bk[D] Wv[D][D] bv[D] Wo[D][D] bo[D]
@@ -107,6 +115,9 @@ typedef enum {
  *     PWD_EMBED_RESNET only: Wr1[3][D][D] br1[D] Wr2[3][D][D] br2[D]   the two Conv1d layers,
  *                                                       weights [tap][in][out], tap k reading
  *                                                       the cell at offset k - 1
+ *     dilated convolutions only, per layer: Wd[3][3][3][D][D] bd[3][D]   ([j][a][e][in][out]:
+ *                                                       unit j, tap (a, e) reading the cell
+ *                                                       at dil_j (a - 1, e - 1))
  * For PWD_DTYPE_BF16 the values are used rounded to bf16 (they should already be
  * bf16-representable). The positional encoding is not stored: the library computes it. */
 #define PWD_BLOB_MAGIC 0x31445750u
@@ -121,7 +132,8 @@ size_t decoder_blob_floats(const pwd_geometry* geom, const pwd_model_dims* dims)
  * sizes 16 and 32, up to 25 at 64); distance <= window_rounds <= 3*distance;
  * 1 <= max_windows <= 2^24; mlp_ratio 4 or 5; n_layers 1..8;
  * token_set PWD_TOKENS_STABILIZERS or PWD_TOKENS_GRID (n_tokens = d*d-1 or (d+1)^2);
- * embedder PWD_EMBED_LINEAR or PWD_EMBED_RESNET;
+ * embedder PWD_EMBED_LINEAR or PWD_EMBED_RESNET; conv_dilation all 0, or all in 1..distance
+ * with PWD_TOKENS_GRID (bf16: d_model 128 only for now);
  * PWD_DTYPE_BF16: d_model in {128, 256}, head size d_model/n_heads in {16, 32, 64}, and the
  * attention tile (K and V of one head: (2 ceil(n_tokens/16) + 1) KB, twice that for head size
  * 64) within 160 KB of LDS;
@@ -205,7 +217,10 @@ enum {
     PWD_STAGE_FP32_WINDOW = 6,    /* the whole fp32 decoder (fp32 configurations) */
     PWD_STAGE_STREAM_SPLIT = 7,   /* decode_stream: cutting the stream into windows */
     PWD_STAGE_STREAM_COMBINE = 8, /* decode_stream: XOR and soft-XOR of the window results */
-    PWD_NUM_STAGES = 9
+    PWD_STAGE_OUT_PROJ = 9,       /* with dilated convolutions: out-projection + LayerNorm 1
+                                     (stages 2-4 then time the feed-forward part) */
+    PWD_STAGE_DILATED_CONV = 10,  /* one launch per residual unit of the dilated convolutions */
+    PWD_NUM_STAGES = 11
 };
 
 typedef struct {

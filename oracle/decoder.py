@@ -303,11 +303,11 @@ def conv2d_dilated(G: np.ndarray, Wk: np.ndarray, b: np.ndarray, dil: int) -> np
     for a in range(3):
         for e in range(3):
             dr, dc = dil * (a - 1), dil * (e - 1)
-            for r in range(S):
-                for c in range(S):
-                    rr, cc = r + dr, c + dc
-                    if 0 <= rr < S and 0 <= cc < S:
-                        y[:, r, c, :] += G[:, rr, cc, :] @ Wk[a, e]
+            # output cells (r, c) whose source (r + dr, c + dc) lies on the grid
+            r0, r1 = max(0, -dr), min(S, S - dr)
+            c0, c1 = max(0, -dc), min(S, S - dc)
+            if r0 < r1 and c0 < c1:
+                y[:, r0:r1, c0:c1, :] += G[:, r0 + dr:r1 + dr, c0 + dc:c1 + dc, :] @ Wk[a, e]
     return y
 
 

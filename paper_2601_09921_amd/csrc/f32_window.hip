@@ -205,6 +205,29 @@ __global__ __launch_bounds__(THREADS) void f32_window_kernel(F32Params p) {
             __syncthreads();
             layer_norm_rows<D>(Z, N, L.g1, L.be1, p.eps);
             __syncthreads();
+            if (p.conv_w) {
+                // dilated convolutions on the grid (token = cell): three residual units
+                // Z += ReLU(b_j + sum_{a,e} Z[cell + dil_j (a-1, e-1)] Wd_j[a][e]); A is free
+                const float* cw = p.conv_w + (size_t)l * (27 * (size_t)D * D + 3 * D);
+                const int side = d + 1;
+                for (int j = 0; j < 3; ++j) {
+                    const float* Wj = cw + (size_t)j * 9 * D * D;
+                    const float* bj = cw + 27 * (size_t)D * D + j * D;
+                    for (int idx = threadIdx.x; idx < N * D; idx += THREADS) {
+                        const int n = idx / D, o = idx % D, r = n / side, c = n % side;
+                        float acc = bj[o];
+                        for (int tap = 0; tap < 9; ++tap) {
+                            const int rr = r + p.dil[j] * (tap / 3 - 1), cc = c + p.dil[j] * (tap % 3 - 1);
+                            if (rr < 0 || rr >= side || cc < 0 || cc >= side) continue;
+                            acc += dot_col<D>(Z + (rr * side + cc) * D, Wj + (size_t)tap * D * D, D, o);
+                        }
+                        A[idx] = fmaxf(acc, 0.f);
+                    }
+                    __syncthreads();
+                    for (int idx = threadIdx.x; idx < N * D; idx += THREADS) Z[idx] += A[idx];
+                    __syncthreads();
+                }
+            }
             linear<D, F>(Z, N, L.W1, L.b1, Hd, nullptr, true);
             __syncthreads();
             linear<F, D>(Hd, N, L.W2, L.b2, X, Z, false);     // X = Z + FF(Z)

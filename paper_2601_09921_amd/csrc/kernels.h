@@ -12,7 +12,10 @@ struct SyndromeIn {
 };
 
 // Stage flags of the token-local kernel.
-enum { TOK_POST = 1, TOK_EMBED = 2, TOK_QKV = 4, TOK_RESNET = 8 };   // RESNET: with EMBED
+// POST = out-projection + LN1 + feed-forward + LN2. With the dilated convolutions between LN1
+// and the feed-forward, POST splits into WO (out-projection + LN1, alone; also writes the
+// convolutions' bf16 input G) and FFN (feed-forward + LN2, then EMBED / QKV as after POST).
+enum { TOK_POST = 1, TOK_EMBED = 2, TOK_QKV = 4, TOK_RESNET = 8, TOK_WO = 16, TOK_FFN = 32 };
 
 struct TokParams {
     SyndromeIn in;          // in.N: stabilizers (bits per measurement round)
@@ -37,6 +40,19 @@ struct TokParams {
     const int* emb_nb;      // [ntok][8]: stabilizers at cells c-2 .. c+2 of the token's cell c
                             // (-1: none), then the cell's position class (0..4), 0, 0
     const float* emb_tab;   // [5 * 32][D]: block output by (position class, 5 event bits)
+    uint16_t* G;            // TOK_WO: the LN1 output as bf16 B fragments, token-major
+                            // [tb * 16 + col][D/32][4][8] (k-step, lane group, 8 values)
+};
+
+// One residual unit of the dilated convolutions on the (d+1)^2 grid (the grid token set: token
+// = cell r*(d+1)+c): X = X + ReLU(b + sum_taps W_tap^T x[cell + dil * offset]).
+struct ConvParams {
+    float* X;               // fp32 state, C fragments [tb][D/16][64][4]: residual in, result out
+    const uint16_t* Gin;    // the unit's input as bf16 B fragments, token-major (TokParams::G)
+    uint16_t* Gout;         // its output in the same layout (the next unit's input)
+    const uint16_t* stream; // weight fragments: 9 taps (3 a + e) x [D/16 row tiles][D/32 k-steps]
+    const float* bias;      // [D]
+    int d, dil, ntok, nbw, nwin;
 };
 
 struct AttnParams {
@@ -81,6 +97,8 @@ struct F32Params {
     int D, L, H, F;
     const int* emb_nb;      // embedder residual block as in TokParams, or null
     const float* emb_tab;
+    const float* conv_w;    // dilated convolutions: per layer Wd[3][3][3][D][D] bd[3][D], or null
+    int dil[3];             // their dilations (grid token set: token = cell)
     int readouts;           // readouts after the last `readouts` rounds (1: final state only)
     float kappa, eps;
 };
@@ -90,6 +108,7 @@ int64_t tok_block_granule();
 int tok_mlp_chunk(int D);
 int tok_bv_rep(int D, int F);
 hipError_t launch_tok(int D, int F, int flags, const TokParams& p, int64_t n_tb, hipStream_t s);
+hipError_t launch_conv(int D, bool gout, const ConvParams& p, int64_t n_tb, hipStream_t s);
 hipError_t launch_attn(int dh, const AttnParams& p, int nwin, hipStream_t s);
 hipError_t launch_readout(const ReadoutParams& p, hipStream_t s);
 hipError_t launch_f32_window(const F32Params& p, hipStream_t s);

@@ -309,7 +309,12 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(To
     constexpr int LA_WO = TOK_LA_WO, LA_MLP = TOK_LA_MLP, LA_QKV = TOK_LA_QKV;
     using V = Vecs<D, S::F>;
     constexpr int RT = S::RT, KS = S::KS, CH = S::CH;
-    constexpr bool POST = (FLAGS & TOK_POST) != 0, QKV = (FLAGS & TOK_QKV) != 0;
+    // DO_WO: out-projection + LN1; DO_FFN: feed-forward + LN2; POST: either (X is loaded)
+    constexpr bool WO_ONLY = (FLAGS & TOK_WO) != 0, FFN_ONLY = (FLAGS & TOK_FFN) != 0;
+    static_assert(!WO_ONLY || FLAGS == TOK_WO, "the out-projection-only launch stands alone");
+    constexpr bool DO_WO = (FLAGS & TOK_POST) != 0 || WO_ONLY, DO_FFN = (FLAGS & TOK_POST) != 0 || FFN_ONLY;
+    constexpr bool POST = DO_WO || DO_FFN, QKV = (FLAGS & TOK_QKV) != 0;
+    constexpr int WO_CH = DO_WO ? S::WO_CHUNKS : 0, N_POST = WO_CH + (DO_FFN ? S::MLP_CHUNKS : 0);
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int g = lane >> 4;
@@ -318,9 +323,9 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(To
 
     constexpr int CHUNK = S::CHUNK;
     WeightPipe<CHUNK, WAVES> pipe;
-    pipe.post = p.post_stream;
+    pipe.post = DO_WO ? p.post_stream : p.post_stream + (size_t)S::WO_CHUNKS * CHUNK * FRAG;
     pipe.qkv = p.qkv_stream;
-    pipe.n_post = POST ? S::POST_CHUNKS : 0;
+    pipe.n_post = N_POST;
     pipe.total = pipe.n_post + (QKV ? S::QKV_CHUNKS : 0);
     pipe.wave = __builtin_amdgcn_readfirstlane(wave);
     pipe.lane = lane;
@@ -329,12 +334,14 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(To
     // the first weight chunk and of the vector staging below (all of it is awaited at the
     // first chunk's sync).
     f32x4 x[RT][TB];
-    bf16x8 y[POST ? KS : 1][TB];
+    bf16x8 y[DO_WO ? KS : 1][TB];
     if constexpr (POST) {
+        if constexpr (DO_WO) {
 #pragma unroll
-        for (int b = 0; b < TB; ++b)
+            for (int b = 0; b < TB; ++b)
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) y[ks][b] = ldfrag(p.Y, (tb0 + b) * KS + ks, lane);
+                for (int ks = 0; ks < KS; ++ks) y[ks][b] = ldfrag(p.Y, (tb0 + b) * KS + ks, lane);
+        }
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
@@ -398,7 +405,7 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(To
         }
     }
 
-    if constexpr (POST) {
+    if constexpr (DO_WO) {
         // ---- out-projection + residual + LayerNorm 1; accumulators start at X (+ b_o below)
         {
             constexpr int LA = LA_WO;
@@ -434,7 +441,22 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(To
             for (int b = 0; b < TB; ++b) x[rt][b] += bias;
         }
         layer_norm<RT, TB>(x, vec + V::G1, vec + V::BE1, p.eps, g);
-
+    }
+    if constexpr (WO_ONLY) {
+        // the dilated convolutions' input: each token's B fragments, token-major
+#pragma unroll
+        for (int b = 0; b < TB; ++b)
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                st_stream(reinterpret_cast<u16x8*>(p.G + ((((tb0 + b) * 16 + col) * KS + ks) * 4 + g) * 8),
+                          __builtin_bit_cast(u16x8, pack_b(x[2 * ks][b], x[2 * ks + 1][b])));
+    }
+    if constexpr (DO_FFN) {
+        if constexpr (!DO_WO) {
+            // no chunk sync has run yet: await and publish the staged vectors (b_2 below)
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            __syncthreads();
+        }
         // ---- feed-forward, hidden units in chunks of CH; accumulators start at X + b_2
         bf16x8 xb[KS][TB];
 #pragma unroll
@@ -455,7 +477,7 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(To
         constexpr int NW1 = (CH / 16) * KS;
         auto mlp_chunk = [&](auto par, int c) {
             constexpr int PAR = decltype(par)::value;
-            const int ci = S::WO_CHUNKS + c;
+            const int ci = WO_CH + c;
             const uint16_t* buf = pipe.template sync<PAR, 0>(ci);
             f32x4 h[MP][CH / 16][TB];
 #pragma unroll
@@ -494,7 +516,7 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(To
             sched_pipeline<MP * 32, TB, LA>();
         };
         static_assert(S::MLP_CHUNKS % 2 == 0, "feed-forward chunks come in pairs");
-        constexpr int P0 = S::WO_CHUNKS & 1;
+        constexpr int P0 = WO_CH & 1;
         for (int c = 0; c < S::MLP_CHUNKS; c += 2) {
             mlp_chunk(std::integral_constant<int, P0>{}, c);
             mlp_chunk(std::integral_constant<int, 1 - P0>{}, c + 1);
@@ -502,7 +524,7 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(To
         layer_norm<RT, TB>(x, vec + V::G2, vec + V::BE2, p.eps, g);
     }
 
-    if constexpr (POST && (FLAGS & TOK_EMBED) != 0) {
+    if constexpr (DO_FFN && (FLAGS & TOK_EMBED) != 0) {
         // the state D_t itself, for a readout of this round (bf16, the readout's operand type)
         if (p.state_out) {
 #pragma unroll
@@ -552,7 +574,7 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(To
 #pragma unroll
             for (int b = 0; b < TB; ++b) xb[ks][b] = pack_b(x[2 * ks][b], x[2 * ks + 1][b]);
         // 3D output features in groups of 32 (= one B fragment of Q, K or V)
-        constexpr int NP = POST ? S::POST_CHUNKS : 0;
+        constexpr int NP = N_POST;
         constexpr int OPC = S::OG_PER_CHUNK;
         constexpr int LA = LA_QKV;
         // Q and K are stored as B fragments of their transposes (one 1 KB store per group and
@@ -630,7 +652,8 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(To
     }
     // The last chunk's reload into the idle buffer must land before the workgroup's LDS is
     // freed; the global stores issued after it need not.
-    constexpr int END_YOUNGER = QKV ? qkv_stores_after_last_load<CHUNK, WAVES, KS, LA_QKV, 2 * TB>() : RT * TB;
+    constexpr int END_YOUNGER = QKV ? qkv_stores_after_last_load<CHUNK, WAVES, KS, LA_QKV, 2 * TB>()
+                                    : RT * TB + (WO_ONLY ? KS * TB : 0);
     asm volatile("s_waitcnt vmcnt(%0)" :: "n"(END_YOUNGER) : "memory");
 }
 
@@ -653,12 +676,155 @@ hipError_t launch_tok_d(int flags, const TokParams& p, int64_t n_tb, hipStream_t
         case TOK_POST | TOK_EMBED | TOK_QKV | TOK_RESNET:
             launch_variant<D, MR, TOK_POST | TOK_EMBED | TOK_QKV | TOK_RESNET>(p, n_tb, s);
             break;
+        // split POST around the dilated convolutions
+        case TOK_WO: launch_variant<D, MR, TOK_WO>(p, n_tb, s); break;
+        case TOK_FFN | TOK_QKV: launch_variant<D, MR, TOK_FFN | TOK_QKV>(p, n_tb, s); break;
+        case TOK_FFN | TOK_EMBED | TOK_QKV: launch_variant<D, MR, TOK_FFN | TOK_EMBED | TOK_QKV>(p, n_tb, s); break;
+        case TOK_FFN | TOK_EMBED | TOK_QKV | TOK_RESNET:
+            launch_variant<D, MR, TOK_FFN | TOK_EMBED | TOK_QKV | TOK_RESNET>(p, n_tb, s);
+            break;
+        case TOK_FFN: launch_variant<D, MR, TOK_FFN>(p, n_tb, s); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
+// One residual unit of the dilated convolutions (model table: 3 x Conv2d(D, D) per layer;
+// App. A.2: the attention output scattered onto the 2-D grid), an implicit GEMM on MFMA:
+//   X[tok] += ReLU(b + sum_{a,e} W[a][e]^T G[cell(tok) + dil (a-1, e-1)])   (zero off the grid)
+// Same structure as the token kernel's out-projection: 2 16-token blocks per wavefront, the
+// accumulators (tokens along MFMA columns) in registers across all 9 taps, and the weights of
+// each tap streamed through the double-buffered LDS ring. At each tap the wavefront gathers
+// the B fragments of its tokens' neighbours (16 bytes per lane and k-step from the token-major
+// bf16 copy G, which stays in L2), so every gathered fragment feeds D/16 MFMAs and every LDS
+// weight fragment 2 per wavefront. The residual stream stays fp32; the unit also writes its
+// output as the next unit's G.
+template <int D, bool GOUT>
+__global__ __launch_bounds__(256, 2) void conv_kernel(ConvParams p) {
+    constexpr int WAVES = 4;
+    using S = Shape<D, WAVES, 4>;
+    constexpr int RT = S::RT, KS = S::KS, CHUNK = S::CHUNK, LA = TOK_LA_WO;
+    constexpr int TAP_CHUNKS = RT * KS / CHUNK;   // 4 at D = 256, 1 at D = 128
+    static_assert(RT * KS % CHUNK == 0, "whole chunks per tap");
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int g = lane >> 4, col = lane & 15;
+    const int64_t tb0 = ((int64_t)blockIdx.x * WAVES + wave) * TB;
+
+    WeightPipe<CHUNK, WAVES> pipe;
+    pipe.post = p.stream;
+    pipe.qkv = p.stream;
+    pipe.n_post = 9 * TAP_CHUNKS;
+    pipe.total = 9 * TAP_CHUNKS;
+    pipe.wave = __builtin_amdgcn_readfirstlane(wave);
+    pipe.lane = lane;
+
+    f32x4 acc[RT][TB];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+        const f32x4 bias = ld4(p.bias + rt * 16 + 4 * g);
+#pragma unroll
+        for (int b = 0; b < TB; ++b) acc[rt][b] = bias;
+    }
+    pipe.template issue<0>(0);
+
+    // this lane's token in each block: its cell and its window's first token
+    const int side = p.d + 1;
+    int r0[TB], c0[TB];
+    bool real[TB];
+    int64_t tok0[TB];
+#pragma unroll
+    for (int b = 0; b < TB; ++b) {
+        const int64_t tb = tb0 + b;
+        const int64_t w = tb / p.nbw;
+        const int s = (int)(tb - w * p.nbw) * 16 + col;
+        real[b] = w < p.nwin && s < p.ntok;
+        r0[b] = s / side;
+        c0[b] = s - r0[b] * side;
+        tok0[b] = w * p.nbw * 16;
+    }
+    bf16x8 xb[KS][TB];
+    // the neighbours' B fragments for tap (a, e) = (tap / 3, tap % 3); every load is issued
+    // (an off-grid neighbour reads the window's token 0 and is zeroed)
+    auto gather = [&](int tap) {
+        const int dr = p.dil * (tap / 3 - 1), dc = p.dil * (tap % 3 - 1);
+#pragma unroll
+        for (int b = 0; b < TB; ++b) {
+            const int rr = r0[b] + dr, cc = c0[b] + dc;
+            const bool ok = real[b] && rr >= 0 && rr < side && cc >= 0 && cc < side;
+            const uint16_t* src = p.Gin + ((tok0[b] + (ok ? rr * side + cc : 0)) * KS * 4 + g) * 8;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                const u16x8 v = *reinterpret_cast<const u16x8*>(src + ks * 32);
+                xb[ks][b] = __builtin_bit_cast(bf16x8, ok ? v : u16x8{0, 0, 0, 0, 0, 0, 0, 0});
+            }
+        }
+    };
+    // chunk C of a tap (fragments C*CHUNK .. of the tap's [row tile][k-step] order)
+    auto chunk = [&](auto par, auto cidx, int ci) {
+        constexpr int PAR = decltype(par)::value, C = decltype(cidx)::value;
+        const uint16_t* buf = pipe.template sync<PAR, 0>(ci);   // also awaits the gathers
+        const uint16_t* nx = pipe.next(ci);
+        pipelined<CHUNK, LA>(
+            [&](int r) { return lds_frag(buf, r, lane); },
+            [&](int r, const bf16x8& a) {
+                const int fr = C * CHUNK + r, rt = fr / KS, ks = fr % KS;
+#pragma unroll
+                for (int b = 0; b < TB; ++b) acc[rt][b] = mfma16x16x32(a, xb[ks][b], acc[rt][b]);
+            },
+            [&](int r) { pipe.template after_read<1 - PAR, CHUNK, LA>(nx, r); });
+        sched_pipeline<CHUNK, TB, LA>();
+    };
+    auto tap_body = [&](auto par0, int tap) {   // par0: LDS buffer of the tap's first chunk
+        constexpr int P0 = decltype(par0)::value;
+        gather(tap);
+        static_for<TAP_CHUNKS>([&](auto c) {
+            constexpr int C = decltype(c)::value;
+            chunk(std::integral_constant<int, (P0 + C) & 1>{}, c, tap * TAP_CHUNKS + C);
+        });
+    };
+    if constexpr (TAP_CHUNKS % 2 == 0) {
+        for (int tap = 0; tap < 9; ++tap) tap_body(std::integral_constant<int, 0>{}, tap);
+    } else {
+        for (int tap = 0; tap < 8; tap += 2) {
+            tap_body(std::integral_constant<int, 0>{}, tap);
+            tap_body(std::integral_constant<int, 1>{}, tap + 1);
+        }
+        tap_body(std::integral_constant<int, 0>{}, 8);
+    }
+
+    // X += ReLU(acc); the output's B fragments for the next unit
+#pragma unroll
+    for (int b = 0; b < TB; ++b)
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            f32x4 xo[2];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                f32x4* px = reinterpret_cast<f32x4*>(p.X + (((tb0 + b) * RT + 2 * ks + h) * 64 + lane) * 4);
+                xo[h] = ld_stream(px) + relu4(acc[2 * ks + h][b]);
+                st_stream(px, xo[h]);
+            }
+            if constexpr (GOUT)
+                st_stream(reinterpret_cast<u16x8*>(p.Gout + ((((tb0 + b) * 16 + col) * KS + ks) * 4 + g) * 8),
+                          __builtin_bit_cast(u16x8, pack_b(xo[0], xo[1])));
+        }
+    // the last chunk's reload into the idle buffer lands before the LDS is freed
+    constexpr int END_YOUNGER = RT * TB + (GOUT ? KS * TB : 0);
+    asm volatile("s_waitcnt vmcnt(%0)" :: "n"(END_YOUNGER) : "memory");
+}
+
 }  // namespace
+
+hipError_t launch_conv(int D, bool gout, const ConvParams& p, int64_t n_tb, hipStream_t s) {
+    if (n_tb <= 0) return hipSuccess;
+    const dim3 grid((unsigned)((n_tb + 4 * TB - 1) / (4 * TB))), block(256);
+    if (D == 256 && gout) conv_kernel<256, true><<<grid, block, 0, s>>>(p);
+    else if (D == 256) conv_kernel<256, false><<<grid, block, 0, s>>>(p);
+    else if (D == 128 && gout) conv_kernel<128, true><<<grid, block, 0, s>>>(p);
+    else if (D == 128) conv_kernel<128, false><<<grid, block, 0, s>>>(p);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
+}
 
 // Token blocks are processed in groups of 8 or 16 (wavefronts x TB by variant); every buffer
 // indexed here must be allocated for n_tb rounded up to a multiple of all of them.

@@ -37,12 +37,12 @@ class Geometry(ctypes.Structure):
 class ModelDims(ctypes.Structure):
     _fields_ = [("d_model", ctypes.c_int32), ("n_layers", ctypes.c_int32), ("n_heads", ctypes.c_int32),
                 ("mlp_ratio", ctypes.c_int32), ("dtype", ctypes.c_int32), ("token_set", ctypes.c_int32),
-                ("embedder", ctypes.c_int32)]
+                ("embedder", ctypes.c_int32), ("conv_dilation", ctypes.c_int32 * 3)]
 
 
-NUM_STAGES = 9
+NUM_STAGES = 11
 STAGE_NAMES = ["embed_qkv", "attention", "post_qkv", "post_embed_qkv", "post", "readout", "fp32_window",
-               "stream_split", "stream_combine"]
+               "stream_split", "stream_combine", "out_proj", "dilated_conv"]
 
 
 class StageTimes(ctypes.Structure):
@@ -105,8 +105,14 @@ EMBED_LINEAR, EMBED_RESNET = 0, 1
 
 
 def dims(D: int, L: int, H: int, mlp_ratio: int, dtype: int, token_set: int = TOKENS_STABILIZERS,
-         embedder: int = EMBED_LINEAR) -> ModelDims:
-    return ModelDims(D, L, H, mlp_ratio, dtype, token_set, embedder)
+         embedder: int = EMBED_LINEAR, dilations=(0, 0, 0)) -> ModelDims:
+    return ModelDims(D, L, H, mlp_ratio, dtype, token_set, embedder, (ctypes.c_int32 * 3)(*dilations))
+
+
+def pack_dilations(dil) -> int:
+    """Blob header word 13: byte j = dilation of the j-th dilated convolution (0: none)."""
+    dil = list(dil) if dil else [0, 0, 0]
+    return dil[0] | (dil[1] << 8) | (dil[2] << 16)
 
 
 def make_blob(d: int, W: int, D: int, L: int, H: int, F: int, dtype: int, weights: dict,
@@ -117,7 +123,7 @@ def make_blob(d: int, W: int, D: int, L: int, H: int, F: int, dtype: int, weight
     hdr = [BLOB_MAGIC, BLOB_VERSION, d, W, D, L, H, F, dtype,
            struct.unpack("<I", struct.pack("<f", kappa))[0],
            struct.unpack("<I", struct.pack("<f", eps))[0], token_set,
-           EMBED_RESNET if "res" in weights else EMBED_LINEAR, 0, 0, 0]
+           EMBED_RESNET if "res" in weights else EMBED_LINEAR, pack_dilations(weights.get("dilations")), 0, 0]
     parts = [weights["w_e"], weights["b_e"]]
     for lw in weights["layers"]:
         parts += [lw[k] for k in ("Wq", "bq", "Wk", "bk", "Wv", "bv", "Wo", "bo", "g1", "be1",
@@ -125,6 +131,9 @@ def make_blob(d: int, W: int, D: int, L: int, H: int, F: int, dtype: int, weight
     parts += [weights["Wc"], weights["bc"], weights["w_o"], weights["b_o"], weights["beta"]]
     if "res" in weights:
         parts += [weights["res"][k] for k in ("W1", "b1", "W2", "b2")]
+    if weights.get("dilations"):
+        for lw in weights["layers"]:
+            parts += [lw["Wd"], lw["bd"]]
     body = np.concatenate([np.asarray(p, dtype=np.float64).ravel() for p in parts]).astype("<f4")
     return struct.pack("<16I", *hdr) + body.tobytes()
 
@@ -140,13 +149,14 @@ class Decoder:
     """Owns one pwd_decoder handle."""
 
     def __init__(self, d: int, W: int, max_windows: int, D: int, L: int, H: int, mlp_ratio: int,
-                 dtype: int, blob: bytes, token_set: int = TOKENS_STABILIZERS, embedder: int = EMBED_LINEAR):
+                 dtype: int, blob: bytes, token_set: int = TOKENS_STABILIZERS, embedder: int = EMBED_LINEAR,
+                 dilations=(0, 0, 0)):
         lib = load_library()
         self._lib = lib
         self.d, self.W, self.max_windows = d, W, max_windows
         self.N = d * d - 1
         self.words = (self.N + 31) // 32
-        g, m = geometry(d, W, max_windows), dims(D, L, H, mlp_ratio, dtype, token_set, embedder)
+        g, m = geometry(d, W, max_windows), dims(D, L, H, mlp_ratio, dtype, token_set, embedder, dilations)
         h = ctypes.c_void_p()
         buf = ctypes.create_string_buffer(blob, len(blob))
         _check(lib.decoder_create(ctypes.byref(g), ctypes.byref(m), buf, len(blob), ctypes.byref(h)))
@@ -157,7 +167,8 @@ class Decoder:
         ts = TOKENS_GRID if getattr(wl, "grid", False) else TOKENS_STABILIZERS
         emb = EMBED_RESNET if "res" in weights else EMBED_LINEAR
         blob = make_blob(wl.d, wl.W, wl.D, wl.L, wl.H, wl.F, wl.dtype, weights, ts)
-        return cls(wl.d, wl.W, max_windows or wl.B, wl.D, wl.L, wl.H, wl.mlp_ratio, wl.dtype, blob, ts, emb)
+        dil = tuple(weights["dilations"]) if weights.get("dilations") else (0, 0, 0)
+        return cls(wl.d, wl.W, max_windows or wl.B, wl.D, wl.L, wl.H, wl.mlp_ratio, wl.dtype, blob, ts, emb, dil)
 
     def decode(self, meas, types, logits, bits, stream=None):
         """meas: int32/uint32 [n][W+1][words] cuda tensor; types: uint8 [n]; outputs float32/uint8 [n]."""

@@ -22,8 +22,8 @@ def test_exports_every_header_function(lib):
         assert hasattr(lib, n), n
 
 
-def validate(lib, d=7, W=14, B=16, D=128, L=3, H=8, r=4, dt=1, ts=0, emb=0):
-    g, m = pwdec.geometry(d, W, B), pwdec.dims(D, L, H, r, dt, ts, emb)
+def validate(lib, d=7, W=14, B=16, D=128, L=3, H=8, r=4, dt=1, ts=0, emb=0, dil=(0, 0, 0)):
+    g, m = pwdec.geometry(d, W, B), pwdec.dims(D, L, H, r, dt, ts, emb, dil)
     return lib.decoder_validate_config(ctypes.byref(g), ctypes.byref(m))
 
 
@@ -37,6 +37,8 @@ def test_workloads_are_supported(lib, wl):
     dict(W=6), dict(W=22), dict(B=0), dict(r=3), dict(r=6), dict(L=0),
     dict(H=3), dict(D=96, H=6), dict(D=128, H=1), dict(D=256, H=2), dict(dt=2), dict(dt=0, D=256, H=8),
     dict(ts=2), dict(ts=-1), dict(ts=1, d=35, W=35), dict(emb=2), dict(emb=-1),
+    dict(dil=(1, 2, 4)), dict(ts=1, dil=(1, 0, 2)), dict(ts=1, dil=(1, 2, 8)), dict(ts=1, dil=(-1, 1, 1)),
+    dict(ts=1, D=256, H=8, dil=(1, 2, 4)),
     dict(dt=0, d=11, W=22, D=64, H=4),
 ])
 def test_rejects_unsupported(lib, kw):
@@ -51,6 +53,7 @@ def test_rejects_unsupported(lib, kw):
     dict(ts=1), dict(ts=1, d=25, W=50, D=256, H=8), dict(ts=1, d=33, W=33), dict(ts=1, dt=0, d=3, W=6, D=64, H=4),
     dict(r=5), dict(r=5, d=25, W=50, D=256, H=8), dict(r=5, dt=0, d=3, W=6, D=64, H=4),
     dict(emb=1), dict(emb=1, ts=1, d=25, W=50, D=256, H=8), dict(emb=1, dt=0, d=3, W=6, D=64, H=4),
+    dict(ts=1, dil=(1, 2, 4)), dict(ts=1, dil=(7, 7, 7)), dict(ts=1, dt=0, d=3, W=6, D=32, H=2, dil=(1, 2, 3)),
 ])
 def test_supported_head_sizes(lib, kw):
     """Head sizes 16, 32 and 64 on the bf16 path (LDS for K and V of one head of 64 at
@@ -90,6 +93,13 @@ def test_blob_size_matches_header_formula(lib, name):
     m = pwdec.dims(wl.D, wl.L, wl.H, wl.mlp_ratio, wl.dtype, 0, pwdec.EMBED_RESNET)
     assert len(rblob) == 64 + 4 * lib.decoder_blob_floats(ctypes.byref(g), ctypes.byref(m))
     assert len(rblob) - len(blob) == 4 * (6 * wl.D * wl.D + 2 * wl.D)
+    # with dilated convolutions (grid token set): per layer three 3x3 Conv2d(D, D) and biases
+    cw = dataclasses.replace(wl, grid=True, dil=(1, 2, 3))
+    cblob = pwdec.make_blob(cw.d, cw.W, cw.D, cw.L, cw.H, cw.F, cw.dtype, synth.make_weights(cw), 1)
+    assert struct.unpack("<I", cblob[52:56])[0] == 0x030201
+    m = pwdec.dims(wl.D, wl.L, wl.H, wl.mlp_ratio, wl.dtype, 1, 0, (1, 2, 3))
+    assert len(cblob) == 64 + 4 * lib.decoder_blob_floats(ctypes.byref(g), ctypes.byref(m))
+    assert len(cblob) - len(blob) == 4 * wl.L * (27 * wl.D * wl.D + 3 * wl.D)
 
 
 def corrupt(blob, word, value):
@@ -99,7 +109,7 @@ def corrupt(blob, word, value):
 
 
 @pytest.mark.parametrize("how", ["magic", "version", "distance", "layers", "dtype", "token_set", "embedder",
-                                 "short", "long"])
+                                 "dilations", "short", "long"])
 def test_bad_blobs_rejected_before_device_use(lib, how):
     wl, blob = blob_for("d3")
     bad = {"magic": lambda b: corrupt(b, 0, 0x12345678),
@@ -109,6 +119,7 @@ def test_bad_blobs_rejected_before_device_use(lib, how):
            "dtype": lambda b: corrupt(b, 8, 1),
            "token_set": lambda b: corrupt(b, 11, 1),
            "embedder": lambda b: corrupt(b, 12, 1),
+           "dilations": lambda b: corrupt(b, 13, 0x010101),
            "short": lambda b: b[:-4],
            "long": lambda b: b + b"\0\0\0\0"}[how](blob)
     g, m = pwdec.geometry(wl.d, wl.W, 4), pwdec.dims(wl.D, wl.L, wl.H, wl.mlp_ratio, wl.dtype)

@@ -1,0 +1,100 @@
+"""GPU parity of the Syndrome Transformer's dilated convolutions (model table: 3 x Conv2d(D, D)
+per layer; App. A.2: the attention output scattered onto the 2-D grid) against the fp64
+oracle: three residual units between LayerNorm 1 and the feed-forward, on the (d+1)^2 token
+set. fp32 (one workgroup per window) and bf16 (out-projection + LN1, three implicit-GEMM
+convolution launches, feed-forward + LN2), d_model 128 and 256, feed-forward 4D and 5D, with
+and without the embedder's Conv1d block, the inference and recurrent branches."""
+import numpy as np
+import pytest
+
+from gpu_helpers import BF16_ATOL, FP32_ATOL, FP32_RTOL, check_bits, gpu_decode, say, to_device
+from oracle import decoder as O
+from paper_2601_09921_amd import pwdec, synth
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+BF16, F32 = synth.DTYPE_BF16, synth.DTYPE_F32
+def ids(shapes):
+    return [f"d{s[0]}_D{s[3]}_r{s[6]}_{'f32' if s[7] == F32 else 'bf16'}{'_res' if s[8] else ''}_dil"
+            + "".join(map(str, s[9])) for s in shapes]
+
+
+# (d, W, B, D, L, H, mlp_ratio, dtype, resnet, dilations)
+SHAPES = [
+    (3, 6, 7, 32, 2, 2, 4, F32, False, (1, 2, 3)),
+    (3, 9, 5, 64, 1, 4, 5, F32, True, (1, 3, 2)),
+    (5, 10, 6, 128, 2, 8, 4, BF16, False, (1, 2, 4)),
+    (7, 14, 5, 128, 2, 8, 5, BF16, True, (2, 1, 3)),
+    (11, 22, 3, 256, 2, 8, 4, BF16, False, (1, 2, 4)),
+    (13, 13, 3, 256, 1, 4, 5, BF16, True, (1, 3, 5)),
+    (25, 25, 2, 256, 1, 8, 4, BF16, False, (1, 2, 4)),
+]
+# d_model 256 is switched off in the library (its first GPU run ended in a memory fault whose
+# cause is not yet shown); these cases stay skipped until it is.
+D256_OFF = "dilated convolutions at bf16 d_model 256 are switched off: unexplained GPU fault"
+
+
+def cases(shapes):
+    return [pytest.param(*s, id=i, marks=[pytest.mark.skip(reason=D256_OFF)] if s[3] == 256 else [])
+            for s, i in zip(shapes, ids(shapes))]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def within(g, o, dtype):
+    if dtype == F32:
+        return (np.abs(g - o) <= FP32_RTOL * np.abs(o) + FP32_ATOL).all()
+    return (np.abs(g - o) <= BF16_ATOL).all()
+
+
+def workload(d, W, B, D, L, H, r, dtype, res, dil):
+    return synth.Workload(f"c{d}", d, W, B, 0.05, 0.0, D, L, H, r, dtype, grid=True, resnet=res, dil=dil)
+
+
+@pytest.mark.parametrize("d,W,B,D,L,H,r,dtype,res,dil", cases(SHAPES))
+def test_dilated_parity(d, W, B, D, L, H, r, dtype, res, dil):
+    wl = workload(d, W, B, D, L, H, r, dtype, res, dil)
+    w = synth.make_weights(wl, seed=d + 1100)
+    meas, types = synth.make_windows(wl, seed=d + 1101, realistic_boundaries=False)
+    say(f"dilated conv d={d} W={W} B={B} D={D} L={L} H={H} r={r} dtype={dtype} res={res} dil={dil}")
+    dec = pwdec.Decoder.from_workload(wl, w, max_windows=B)
+    logits, bits, rc = gpu_decode(dec, meas, types)
+    assert rc == pwdec.PWD_OK
+    o_logits, _ = O.forward_windows(meas, types, w, d, H, grid=True)
+    err = np.abs(logits - o_logits)
+    say(f"  max |gpu - oracle| = {err.max():.3e}")
+    assert within(logits, o_logits, dtype), (logits, o_logits)
+    check_bits(bits, o_logits)
+    sub, _, _ = gpu_decode(dec, meas[1:], types[1:])
+    assert np.array_equal(sub.view(np.uint32), logits[1:].view(np.uint32))
+    dec.close()
+    # the convolutions matter: the same draws without them give other logits
+    plain = {k: v for k, v in w.items() if k != "dilations"}
+    p_logits, _ = O.forward_windows(meas, types, plain, d, H, grid=True)
+    assert np.abs(p_logits - o_logits).max() > 10 * max(err.max(), 1e-6)
+
+
+@pytest.mark.parametrize("d,W,B,D,L,H,r,dtype,res,dil", cases([SHAPES[0], SHAPES[3], SHAPES[4]]))
+def test_dilated_recurrent(d, W, B, D, L, H, r, dtype, res, dil):
+    wl = workload(d, W, B, D, L, H, r, dtype, res, dil)
+    w = synth.make_weights(wl, seed=d + 1102)
+    meas, types = synth.make_windows(wl, seed=d + 1103, realistic_boundaries=False)
+    say(f"dilated conv recurrent d={d} D={D} dtype={dtype} dil={dil}")
+    dec = pwdec.Decoder.from_workload(wl, w, max_windows=B)
+    meas_t, types_t = to_device(meas, types)
+    logits = torch.full((B, d), float("nan"), dtype=torch.float32, device="cuda")
+    bits = torch.full((B, d), 7, dtype=torch.uint8, device="cuda")
+    dec.decode_recurrent(meas_t, types_t, logits, bits)
+    torch.cuda.synchronize()
+    assert dec.sync_status() == pwdec.PWD_OK
+    gl = logits.cpu().numpy()
+    dec.close()
+    ol, _ = O.forward_windows_recurrent(meas, types, w, d, H, grid=True)
+    say(f"  max |gpu - oracle| = {np.abs(gl - ol).max():.3e}")
+    assert within(gl, ol, dtype), (gl, ol)
+    assert np.array_equal(bits.cpu().numpy(), (gl > 0).astype(np.uint8))
