@@ -151,6 +151,41 @@ def grid_measurement(wl, weights, torch, pwdec, dev_meas, dev_types):
     return {"tokens": (wl.d + 1) ** 2, "ms": round(dt * 1e3, 2), "us_per_round": dt / (wl.B * wl.d) * 1e6}
 
 
+def paper_variant_measurement(wl, torch, pwdec, synth, dev_meas, dev_types):
+    """The same batch through the paper's own network shape (App. A model table) at
+    d_model 128: the (d+1)^2 token set, the embedder's residual Conv1d block, feed-forward
+    5 d_model, and three dilated 3x3 convolutions per layer (dilations 1, 2, 4) between
+    attention and feed-forward, 3 layers, random weights. One warm-up and one timed decode
+    with per-stage HIP-event timing; the convolution kernel's rate counts all 9 taps of every
+    token (18 D^2 FLOP per token and unit)."""
+    import dataclasses
+    vwl = dataclasses.replace(wl, name=wl.name + "_paper", D=128, L=3, H=8, mlp_ratio=5, grid=True,
+                              resnet=True, dil=(1, 2, 4))
+    dec = pwdec.Decoder.from_workload(vwl, synth.make_weights(vwl))
+    logits = torch.empty(wl.B, dtype=torch.float32, device="cuda")
+    bits = torch.empty(wl.B, dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    dec.decode(dev_meas, dev_types, logits, bits, stream)     # warm-up
+    torch.cuda.synchronize()
+    dec.profile(True)
+    t0 = time.perf_counter()
+    dec.decode(dev_meas, dev_types, logits, bits, stream)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    stages = dec.profile_read()
+    dec.profile(False)
+    dec.close()
+    T, D = (wl.d + 1) ** 2, vwl.D
+    conv_ms, conv_n = stages["dilated_conv"]
+    conv_tf = wl.B * 18 * T * D * D / (conv_ms / conv_n * 1e-3) / 1e12
+    return {"network": {"d_model": D, "layers": vwl.L, "heads": vwl.H, "mlp_ratio": vwl.mlp_ratio, "tokens": T,
+                        "embedder": "linear + residual Conv1d x2", "dilations": list(vwl.dil)},
+            "ms": round(dt * 1e3, 2), "us_per_round": dt / (wl.B * wl.d) * 1e6,
+            "stage_ms": {k: round(v[0], 2) for k, v in stages.items()},
+            "dilated_conv": {"kernel": "conv_kernel<128>", "launches": conv_n, "avg_ms": round(conv_ms / conv_n, 3),
+                             "TFLOPs": round(conv_tf, 1), "frac_of_bf16_peak": round(conv_tf / MFMA_BF16_PEAK_TFLOPS, 3)}}
+
+
 def input_stage_measurement(dec, wl, torch, dev_meas, dev_types, reps=5):
     """The input stage on its own: decoder_detection_events over the batch (packed measurement
     rounds in, packed detection events out; the same event_word the token kernel fuses),
@@ -214,6 +249,8 @@ def main():
     ap.add_argument("--no-stream", action="store_true", help="skip the decode_stream measurement")
     ap.add_argument("--no-recurrent", action="store_true", help="skip the recurrent-readout measurement")
     ap.add_argument("--no-grid", action="store_true", help="skip the (d+1)^2 token-set measurement")
+    ap.add_argument("--no-variant", action="store_true",
+                    help="skip the paper-shaped network measurement (d_model 128, convolutions, FFN 5x)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first copy 1 GiB device-to-device 3 times (the known-size reference that "
                          "scales rocprofv3 FETCH_SIZE / WRITE_SIZE counters)")
@@ -332,6 +369,8 @@ def main():
     dec.close()
     if not args.no_grid and wl.dtype == synth.DTYPE_BF16:
         out["grid_tokens"] = grid_measurement(wl, weights, torch, pwdec, dev_meas, dev_types)
+    if not args.no_variant and wl.dtype == synth.DTYPE_BF16:
+        out["paper_variant"] = paper_variant_measurement(wl, torch, pwdec, synth, dev_meas, dev_types)
     if args.cpu_sample > 0:
         out["cpu_baseline"] = cpu_baseline(wl, weights, args.cpu_sample)
     print(json.dumps(out), flush=True)

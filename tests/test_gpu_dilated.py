@@ -26,6 +26,7 @@ SHAPES = [
     (3, 9, 5, 64, 1, 4, 5, F32, True, (1, 3, 2)),
     (5, 10, 6, 128, 2, 8, 4, BF16, False, (1, 2, 4)),
     (7, 14, 5, 128, 2, 8, 5, BF16, True, (2, 1, 3)),
+    (25, 25, 2, 128, 1, 8, 5, BF16, True, (1, 2, 4)),    # the bench's paper-shaped network, 676 tokens
     (11, 22, 3, 256, 2, 8, 4, BF16, False, (1, 2, 4)),
     (13, 13, 3, 256, 1, 4, 5, BF16, True, (1, 3, 5)),
     (25, 25, 2, 256, 1, 8, 4, BF16, False, (1, 2, 4)),
@@ -79,7 +80,7 @@ def test_dilated_parity(d, W, B, D, L, H, r, dtype, res, dil):
     assert np.abs(p_logits - o_logits).max() > 10 * max(err.max(), 1e-6)
 
 
-@pytest.mark.parametrize("d,W,B,D,L,H,r,dtype,res,dil", cases([SHAPES[0], SHAPES[3], SHAPES[4]]))
+@pytest.mark.parametrize("d,W,B,D,L,H,r,dtype,res,dil", cases([SHAPES[0], SHAPES[3], SHAPES[5]]))
 def test_dilated_recurrent(d, W, B, D, L, H, r, dtype, res, dil):
     wl = workload(d, W, B, D, L, H, r, dtype, res, dil)
     w = synth.make_weights(wl, seed=d + 1102)
