@@ -697,8 +697,10 @@ hipError_t launch_tok_d(int flags, const TokParams& p, int64_t n_tb, hipStream_t
 // each tap streamed through the double-buffered LDS ring. At each tap the wavefront gathers
 // the B fragments of its tokens' neighbours (16 bytes per lane and k-step from the token-major
 // bf16 copy G, which stays in L2), so every gathered fragment feeds D/16 MFMAs and every LDS
-// weight fragment 2 per wavefront. The residual stream stays fp32; the unit also writes its
-// output as the next unit's G.
+// weight fragment 2 per wavefront. Where registers allow (D = 128) the gathers are double-
+// buffered: tap t+1's are issued right after tap t's first chunk sync, so their latency
+// overlaps tap t's MFMAs. The residual stream stays fp32; the unit also writes its output as
+// the next unit's G.
 template <int D, bool GOUT>
 __global__ __launch_bounds__(256, 2) void conv_kernel(ConvParams p) {
     constexpr int WAVES = 4;
@@ -742,10 +744,12 @@ __global__ __launch_bounds__(256, 2) void conv_kernel(ConvParams p) {
         c0[b] = s - r0[b] * side;
         tok0[b] = w * p.nbw * 16;
     }
-    bf16x8 xb[KS][TB];
-    // the neighbours' B fragments for tap (a, e) = (tap / 3, tap % 3); every load is issued
-    // (an off-grid neighbour reads the window's token 0 and is zeroed)
-    auto gather = [&](int tap) {
+    constexpr bool PF = D <= 128;   // double-buffered gathers (32 more registers at D = 128)
+    bf16x8 xb[PF ? 2 : 1][KS][TB];
+    // the neighbours' B fragments for tap (a, e) = (tap / 3, tap % 3) into buffer SLOT; every
+    // load is issued (an off-grid neighbour reads the window's token 0 and is zeroed)
+    auto gather = [&](auto slot, int tap) {
+        constexpr int SLOT = decltype(slot)::value;
         const int dr = p.dil * (tap / 3 - 1), dc = p.dil * (tap % 3 - 1);
 #pragma unroll
         for (int b = 0; b < TB; ++b) {
@@ -755,41 +759,55 @@ __global__ __launch_bounds__(256, 2) void conv_kernel(ConvParams p) {
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
                 const u16x8 v = *reinterpret_cast<const u16x8*>(src + ks * 32);
-                xb[ks][b] = __builtin_bit_cast(bf16x8, ok ? v : u16x8{0, 0, 0, 0, 0, 0, 0, 0});
+                xb[SLOT][ks][b] = __builtin_bit_cast(bf16x8, ok ? v : u16x8{0, 0, 0, 0, 0, 0, 0, 0});
             }
         }
     };
-    // chunk C of a tap (fragments C*CHUNK .. of the tap's [row tile][k-step] order)
-    auto chunk = [&](auto par, auto cidx, int ci) {
-        constexpr int PAR = decltype(par)::value, C = decltype(cidx)::value;
+    // chunk C of a tap (fragments C*CHUNK .. of the tap's [row tile][k-step] order) on the
+    // gathered fragments in buffer SLOT; after_sync() runs once the chunk is visible
+    auto chunk = [&](auto par, auto cidx, auto slot, int ci, const auto& after_sync) {
+        constexpr int PAR = decltype(par)::value, C = decltype(cidx)::value, SLOT = decltype(slot)::value;
         const uint16_t* buf = pipe.template sync<PAR, 0>(ci);   // also awaits the gathers
+        after_sync();
         const uint16_t* nx = pipe.next(ci);
         pipelined<CHUNK, LA>(
             [&](int r) { return lds_frag(buf, r, lane); },
             [&](int r, const bf16x8& a) {
                 const int fr = C * CHUNK + r, rt = fr / KS, ks = fr % KS;
 #pragma unroll
-                for (int b = 0; b < TB; ++b) acc[rt][b] = mfma16x16x32(a, xb[ks][b], acc[rt][b]);
+                for (int b = 0; b < TB; ++b) acc[rt][b] = mfma16x16x32(a, xb[SLOT][ks][b], acc[rt][b]);
             },
             [&](int r) { pipe.template after_read<1 - PAR, CHUNK, LA>(nx, r); });
         sched_pipeline<CHUNK, TB, LA>();
     };
-    auto tap_body = [&](auto par0, int tap) {   // par0: LDS buffer of the tap's first chunk
-        constexpr int P0 = decltype(par0)::value;
-        gather(tap);
+    // par0: LDS buffer of the tap's first chunk; slot: the tap's gather buffer (tap % 2 with
+    // double buffering, which then prefetches tap + 1 into the other one)
+    auto tap_body = [&](auto par0, auto slot, int tap) {
+        constexpr int P0 = decltype(par0)::value, SLOT = decltype(slot)::value;
+        if constexpr (!PF) gather(slot, tap);
         static_for<TAP_CHUNKS>([&](auto c) {
             constexpr int C = decltype(c)::value;
-            chunk(std::integral_constant<int, (P0 + C) & 1>{}, c, tap * TAP_CHUNKS + C);
+            chunk(std::integral_constant<int, (P0 + C) & 1>{}, c, slot, tap * TAP_CHUNKS + C, [&] {
+                if constexpr (PF && C == 0)
+                    if (tap + 1 < 9) gather(std::integral_constant<int, 1 - SLOT>{}, tap + 1);
+            });
         });
     };
-    if constexpr (TAP_CHUNKS % 2 == 0) {
-        for (int tap = 0; tap < 9; ++tap) tap_body(std::integral_constant<int, 0>{}, tap);
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    if constexpr (PF) gather(I0{}, 0);
+    if constexpr (TAP_CHUNKS % 2 == 0 && !PF) {
+        for (int tap = 0; tap < 9; ++tap) tap_body(I0{}, I0{}, tap);
     } else {
+        // taps in pairs: the LDS buffer parity (odd chunk counts per tap) and the gather slot
+        // alternate with the tap; tap 8 is even
+        static_assert(TAP_CHUNKS % 2 == 1 || PF, "pairs");
+        constexpr int Q = TAP_CHUNKS & 1;   // parity step per tap
         for (int tap = 0; tap < 8; tap += 2) {
-            tap_body(std::integral_constant<int, 0>{}, tap);
-            tap_body(std::integral_constant<int, 1>{}, tap + 1);
+            tap_body(I0{}, I0{}, tap);
+            tap_body(std::integral_constant<int, Q>{}, I1{}, tap + 1);
         }
-        tap_body(std::integral_constant<int, 0>{}, 8);
+        tap_body(I0{}, I0{}, 8);
     }
 
     // X += ReLU(acc); the output's B fragments for the next unit
