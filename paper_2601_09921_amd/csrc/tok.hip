@@ -788,8 +788,8 @@ __global__ __launch_bounds__(256, 2) void conv_kernel(ConvParams p) {
         static_for<TAP_CHUNKS>([&](auto c) {
             constexpr int C = decltype(c)::value;
             chunk(std::integral_constant<int, (P0 + C) & 1>{}, c, slot, tap * TAP_CHUNKS + C, [&] {
-                if constexpr (PF && C == 0)
-                    if (tap + 1 < 9) gather(std::integral_constant<int, 1 - SLOT>{}, tap + 1);
+                if constexpr (PF && C == 0)   // (slot 0 when single-buffered: never instantiated)
+                    if (tap + 1 < 9) gather(std::integral_constant<int, PF ? 1 - SLOT : 0>{}, tap + 1);
             });
         });
     };
