@@ -230,10 +230,9 @@ def conv1d_same(x: np.ndarray, Wk: np.ndarray, b: np.ndarray) -> np.ndarray:
     y = np.broadcast_to(b, x.shape).astype(np.float64).copy()
     for k in range(3):
         off = k - 1
-        for p in range(L):
-            q = p + off
-            if 0 <= q < L:
-                y[:, p, :] += x[:, q, :] @ Wk[k]
+        # output positions p whose source p + off lies in the sequence
+        p0, p1 = max(0, -off), min(L, L - off)
+        y[:, p0:p1, :] += x[:, p0 + off:p1 + off, :] @ Wk[k]
     return y
 
 
