@@ -39,7 +39,8 @@ typedef struct pwd_decoder pwd_decoder; /* opaque handle */
 
 /* Window geometry (Sec. 3.1, App. A.1.1). A window has window_rounds rounds: a left
  * buffer of floor((window_rounds - distance) / 2) rounds, a core of `distance` rounds and
- * a right buffer of the rest. distance: odd, 3..25. window_rounds: distance..3*distance.
+ * a right buffer of the rest. distance: odd, 3..63 within the on-chip limits that
+ * decoder_validate_config states (bf16: up to 35). window_rounds: distance..3*distance.
  * max_windows: the largest batch decode_windows will be given (scratch is sized for it). */
 typedef struct {
     int32_t distance;
@@ -48,8 +49,8 @@ typedef struct {
 } pwd_geometry;
 
 /* Network dimensions (App. A model table): d_model, layers, heads, MLP expansion (the
- * feed-forward width is mlp_ratio * d_model; the model table gives 5), the arithmetic type
- * and the token set. PWD_DTYPE_BF16: bf16 weights and matrix operands, fp32
+ * feed-forward width is mlp_ratio * d_model; the model table gives 5), the arithmetic type,
+ * the token set, the embedder and the dilated convolutions (see the enums below). PWD_DTYPE_BF16: bf16 weights and matrix operands, fp32
  * accumulation, softmax, LayerNorm, residual stream and recurrent state. PWD_DTYPE_F32: fp32
  * throughout. PWD_TOKENS_STABILIZERS: one token per stabilizer (d*d-1); PWD_TOKENS_GRID: one
  * token per cell of the (d+1)x(d+1) stabilizer array (App. A.1.2 and the (d+1)^2 x d_model
