@@ -1,0 +1,46 @@
+"""Host-side pieces of bench.py that need no GPU: the algorithmic FLOP counts the roofline
+uses, the keying of the committed HBM-traffic record to the kernel sources, and the refusal
+to run on more than one GPU."""
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+from paper_2601_09921_amd import synth  # noqa: E402
+
+
+def test_stage_flops_closed_forms():
+    """Per real token and layer: Q/K/V 6 D^2, out-projection 2 D^2, feed-forward 4 D F,
+    attention 4 N D (scores and weighted sum); the readout 8 d^2 D^2 + 2 d D per window."""
+    wl = synth.WORKLOADS["d25"]
+    B, N, D, F, d = 8192, wl.N, wl.D, wl.F, wl.d
+    f, total = bench.stage_flops(wl, B)
+    assert f["post_qkv"] == B * N * (8 * D * D + 4 * D * F)
+    assert f["embed_qkv"] == B * N * 6 * D * D
+    assert f["attention"] == B * 4 * N * N * D
+    assert f["readout"] == B * (8 * d * d * D * D + 2 * d * D)
+    assert total == B * (wl.W * wl.L * N * (8 * D * D + 4 * D * F + 4 * N * D)
+                         + 8 * d * d * D * D + 2 * d * D)
+    # 24 D^2 per token for post + QKV at F = 4 D: 1.573 MFLOP at D = 256
+    assert f["post_qkv"] / (B * N) == 24 * D * D == 1572864
+
+
+def test_traffic_record_is_keyed_to_the_sources(monkeypatch):
+    t = json.load(open(bench.TRAFFIC_FILE))
+    assert set(t) >= {"source_hash", "fetch_scale", "write_scale", "bytes_per_launch"}
+    monkeypatch.setattr(bench, "source_hash", lambda: t["source_hash"])
+    assert bench.load_traffic("post_qkv") == t["bytes_per_launch"].get("post_qkv")
+    monkeypatch.setattr(bench, "source_hash", lambda: "0" * 16)
+    assert bench.load_traffic("post_qkv") is None
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120, cwd=ROOT)
+    assert "one GPU" in (r.stdout + r.stderr)
+    assert not r.stdout.strip().startswith("{")
