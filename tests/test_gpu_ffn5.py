@@ -22,6 +22,7 @@ SHAPES = [
     (11, 22, 4, 256, 2, 8, BF16, False),
     (13, 26, 3, 256, 1, 4, BF16, True),    # head size 64
     (25, 25, 2, 256, 1, 8, BF16, False),   # the d = 25 network with the model table's width
+    (35, 35, 1, 128, 1, 8, BF16, False),   # 1224 tokens, 77 key blocks
 ]
 
 

@@ -20,6 +20,7 @@ SHAPES = [
     (7, 14, 5, 128, 3, 8, BF16),    # 64 tokens: four whole blocks
     (11, 22, 3, 256, 2, 8, BF16),   # 144 tokens
     (25, 25, 2, 256, 1, 8, BF16),   # 676 tokens, 43 key blocks
+    (33, 33, 1, 128, 1, 8, BF16),   # 1156 tokens, 73 key blocks: the largest grid that fits
 ]
 
 

@@ -25,6 +25,7 @@ SHAPES = [
     (11, 22, 4, 256, 2, 8, 5, BF16, True),
     (13, 26, 3, 256, 1, 4, 4, BF16, False),
     (25, 25, 2, 256, 1, 8, 4, BF16, True),
+    (33, 33, 1, 128, 1, 8, 4, BF16, True),     # the largest grid: 1156 cells, 5 position classes
 ]
 
 
