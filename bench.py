@@ -214,7 +214,8 @@ def environment(torch):
 
 
 def cpu_baseline(wl, weights, sample):
-    """The fp64 oracle on `sample` windows (one per window type) on the host cores."""
+    """The fp64 oracle on the batch's first `sample` windows (window types cycle, so all three
+    appear from 3 on) on the host cores; the default sample takes 10-15 s there."""
     from oracle import decoder as O
     from paper_2601_09921_amd import synth
     try:
@@ -245,7 +246,7 @@ def main():
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="d25")
-    ap.add_argument("--cpu-sample", type=int, default=3, help="oracle windows for the CPU baseline (0: skip)")
+    ap.add_argument("--cpu-sample", type=int, default=4, help="oracle windows for the CPU baseline (0: skip)")
     ap.add_argument("--no-stream", action="store_true", help="skip the decode_stream measurement")
     ap.add_argument("--no-recurrent", action="store_true", help="skip the recurrent-readout measurement")
     ap.add_argument("--no-grid", action="store_true", help="skip the (d+1)^2 token-set measurement")
