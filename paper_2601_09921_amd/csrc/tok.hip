@@ -12,6 +12,10 @@
 //          the cell is to the ends of the flattened array, looked up in a host-built table.
 //          Its input is one bit per cell lifted by Linear(1 -> D), so the lookup is exact.
 //   QKV  : the Q, K, V projections of the following layer.
+// With the dilated convolutions between LayerNorm 1 and the feed-forward, POST runs as two
+// launches, WO (out-projection, residual, LayerNorm 1; it also writes the convolutions' input)
+// and FFN (feed-forward, residual, LayerNorm 2, then EMBED / QKV as after POST), around the
+// convolution units of conv_kernel at the end of this file.
 // The residual stream stays fp32 in registers; only GEMM operands are rounded to bf16.
 // GEMMs are transposed (Out^T = W^T In^T) so tokens lie along MFMA columns: LayerNorm
 // reduces over the four lanes that share a token, and each accumulator becomes the next
