@@ -99,3 +99,32 @@ def test_dilated_recurrent(d, W, B, D, L, H, r, dtype, res, dil):
     say(f"  max |gpu - oracle| = {np.abs(gl - ol).max():.3e}")
     assert within(gl, ol, dtype), (gl, ol)
     assert np.array_equal(bits.cpu().numpy(), (gl > 0).astype(np.uint8))
+
+
+def test_dilated_stream_and_stage_profile():
+    """decode_stream with the dilated convolutions (per-window logits against the oracle, the
+    stream bit as the XOR of the window bits), and the per-stage profile: one out-projection
+    launch and three convolution launches per layer and round."""
+    wl = workload(7, 14, 1, 128, 2, 8, 4, BF16, False, (1, 2, 3))
+    w = synth.make_weights(wl, seed=1104)
+    T = 6 * wl.d - 3
+    m = -(-T // wl.d)
+    R = synth.make_stream(wl.N, T, 0.05, seed=1105)
+    say(f"dilated conv stream d7 T={T}")
+    dec = pwdec.Decoder.from_workload(wl, w, max_windows=m)
+    rounds = torch.from_numpy(O.pack_bits(R).view(np.int32)).cuda()
+    bit = torch.zeros(1, dtype=torch.uint8, device="cuda")
+    wlog = torch.zeros(m, dtype=torch.float32, device="cuda")
+    wbits = torch.zeros(m, dtype=torch.uint8, device="cuda")
+    dec.profile(True)
+    dec.decode_stream(rounds, bit, window_logits=wlog, window_bits=wbits)
+    torch.cuda.synchronize()
+    stages = dec.profile_read()
+    dec.profile(False)
+    assert dec.sync_status() == pwdec.PWD_OK
+    dec.close()
+    assert stages["out_proj"][1] == wl.W * wl.L and stages["dilated_conv"][1] == 3 * wl.W * wl.L
+    meas, types = O.split_stream(R, wl.d, wl.W)
+    ol, _ = O.forward_windows(meas, types, w, wl.d, wl.H, grid=True)
+    assert (np.abs(wlog.cpu().numpy() - ol) <= BF16_ATOL).all()
+    assert int(bit.item()) == O.combine_bits(wbits.cpu().numpy())
