@@ -714,7 +714,15 @@ __global__ __launch_bounds__(256, 2) void conv_kernel(ConvParams p) {
     static_assert(RT * KS % CHUNK == 0, "whole chunks per tap");
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int g = lane >> 4, col = lane & 15;
-    const int64_t tb0 = ((int64_t)blockIdx.x * WAVES + wave) * TB;
+    // XCD-aware tiles: workgroups are dispatched round-robin over the 8 XCDs, so workgroup i
+    // takes tile (i % 8) * (grid / 8) + i / 8 and each XCD sweeps a contiguous run of tiles,
+    // whose neighbour gathers then share that XCD's L2. The grid is padded to a multiple of 8;
+    // a workgroup past the last tile leaves before touching memory.
+    const int n_wg = (int)(((int64_t)p.nwin * p.nbw + WAVES * TB - 1) / (WAVES * TB));
+    const int per_xcd = (int)gridDim.x / 8;
+    const int wg = (int)(blockIdx.x % 8) * per_xcd + (int)(blockIdx.x / 8);
+    if (wg >= n_wg) return;
+    const int64_t tb0 = ((int64_t)wg * WAVES + wave) * TB;
 
     WeightPipe<CHUNK, WAVES> pipe;
     pipe.post = p.stream;
@@ -839,7 +847,9 @@ __global__ __launch_bounds__(256, 2) void conv_kernel(ConvParams p) {
 
 hipError_t launch_conv(int D, bool gout, const ConvParams& p, int64_t n_tb, hipStream_t s) {
     if (n_tb <= 0) return hipSuccess;
-    const dim3 grid((unsigned)((n_tb + 4 * TB - 1) / (4 * TB))), block(256);
+    // the kernel maps workgroups to tiles XCD by XCD: the grid is padded to a multiple of 8
+    const int64_t n_wg = (n_tb + 4 * TB - 1) / (4 * TB);
+    const dim3 grid((unsigned)((n_wg + 7) / 8 * 8)), block(256);
     if (D == 256 && gout) conv_kernel<256, true><<<grid, block, 0, s>>>(p);
     else if (D == 256) conv_kernel<256, false><<<grid, block, 0, s>>>(p);
     else if (D == 128 && gout) conv_kernel<128, true><<<grid, block, 0, s>>>(p);
