@@ -52,6 +52,7 @@ struct ConvParams {
     uint16_t* Gout;         // its output in the same layout (the next unit's input)
     const uint16_t* stream; // weight fragments: 9 taps (3 a + e) x [D/16 row tiles][D/32 k-steps]
     const float* bias;      // [D]
+    const uint16_t* zero;   // D zero values: what an off-grid neighbour reads
     int d, dil, ntok, nbw, nwin;
 };
 

@@ -233,6 +233,7 @@ struct pwd_decoder {
     const uint16_t* Wc = nullptr;
     const float* bc = nullptr;
     const float* wo = nullptr;
+    const uint16_t* zero = nullptr;   // dilated convolutions: D zero values (off-grid neighbours)
     const int* cell_token = nullptr;
     const int* emb_nb = nullptr;   // embedder residual block (PWD_EMBED_RESNET): see emb_tables
     const float* emb_tab = nullptr;
@@ -446,7 +447,7 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
 
     struct LayerOff { size_t post, qkv, post_vecs, bqkv, conv[3], conv_b[3]; };
     std::vector<LayerOff> loff(L);
-    size_t off_S0 = 0, off_we = 0, off_Wc = 0, off_bc = 0, off_wo = 0, off_f32 = 0;
+    size_t off_S0 = 0, off_we = 0, off_Wc = 0, off_bc = 0, off_wo = 0, off_f32 = 0, off_zero = 0;
     const size_t lf = layer_floats(D, F);
     const float* tail = w.data() + 2 * D + (size_t)L * lf;   // Wc, bc, w_o, b_o, beta
     if (dims->dtype == PWD_DTYPE_BF16) {
@@ -509,6 +510,10 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
             off_Wc = put(fr.data(), fr.size() * 2);
         }
         off_bc = put(tail + 4 * (size_t)D * D, D * 4);
+        if (has_conv(dims)) {
+            const std::vector<uint16_t> zeros((size_t)D, 0);
+            off_zero = put(zeros.data(), zeros.size() * 2);
+        }
         off_wo = put(tail + 4 * (size_t)D * D + D, (size_t)d * D * 4);
     } else {
         std::vector<float> s0((size_t)dec->ntok * D);
@@ -550,6 +555,7 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
         dec->we = fptr(off_we);
         dec->Wc = hptr(off_Wc);
         dec->bc = fptr(off_bc);
+        if (has_conv(dims)) dec->zero = hptr(off_zero);
         dec->wo = fptr(off_wo);
         for (int l = 0; l < L; ++l) {
             pwd_decoder::Layer ly;
@@ -743,6 +749,7 @@ static int decode_impl(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* 
     cp.ntok = dec->ntok;
     cp.nbw = dec->nbw;
     cp.nwin = (int)n;
+    cp.zero = dec->zero;
     auto post = [&](int l, int flags, int stage) -> hipError_t {
         if (!dec->dil[0]) return timed(dec, stage, s, [&] { return launch_tok(dec->D, dec->F, TOK_POST | flags, tp, n_tb, s); });
         tp.G = dec->G[0];

@@ -701,10 +701,9 @@ hipError_t launch_tok_d(int flags, const TokParams& p, int64_t n_tb, hipStream_t
 // each tap streamed through the double-buffered LDS ring. At each tap the wavefront gathers
 // the B fragments of its tokens' neighbours (16 bytes per lane and k-step from the token-major
 // bf16 copy G, which stays in L2), so every gathered fragment feeds D/16 MFMAs and every LDS
-// weight fragment 2 per wavefront. Where registers allow (D = 128) the gathers are double-
-// buffered: tap t+1's are issued right after tap t's first chunk sync, so their latency
-// overlaps tap t's MFMAs. The residual stream stays fp32; the unit also writes its output as
-// the next unit's G.
+// weight fragment 2 per wavefront. Where registers allow (D = 128) the gathers run two taps
+// ahead (see below). The residual stream stays fp32; the unit also writes its output as the
+// next unit's G.
 template <int D, bool GOUT>
 __global__ __launch_bounds__(256, 2) void conv_kernel(ConvParams p) {
     constexpr int WAVES = 4;
@@ -756,10 +755,16 @@ __global__ __launch_bounds__(256, 2) void conv_kernel(ConvParams p) {
         c0[b] = s - r0[b] * side;
         tok0[b] = w * p.nbw * 16;
     }
-    constexpr bool PF = D <= 128;   // double-buffered gathers (32 more registers at D = 128)
-    bf16x8 xb[PF ? 2 : 1][KS][TB];
-    // the neighbours' B fragments for tap (a, e) = (tap / 3, tap % 3) into buffer SLOT; every
-    // load is issued (an off-grid neighbour reads the window's token 0 and is zeroed)
+    // D = 128: the gathers run two taps ahead in three register slots (tap t in slot t % 3),
+    // each issued right after the last weight load of the chunk two taps earlier, so a chunk
+    // sync need not wait for the newest gathers: vector memory completes in issue order, and
+    // waiting until KS * TB operations remain leaves exactly those. D = 256: one slot,
+    // gathered at the tap (no registers for more).
+    constexpr int NSLOT = D <= 128 ? 3 : 1;
+    bf16x8 xb[NSLOT][KS][TB];
+    // the neighbours' B fragments for tap (a, e) = (tap / 3, tap % 3) into slot SLOT; every
+    // load is issued, and an off-grid neighbour reads a row of zeros, so the loaded values
+    // need no fix-up (which the compiler would schedule ahead, waiting on the prefetch early)
     auto gather = [&](auto slot, int tap) {
         constexpr int SLOT = decltype(slot)::value;
         const int dr = p.dil * (tap / 3 - 1), dc = p.dil * (tap % 3 - 1);
@@ -767,20 +772,18 @@ __global__ __launch_bounds__(256, 2) void conv_kernel(ConvParams p) {
         for (int b = 0; b < TB; ++b) {
             const int rr = r0[b] + dr, cc = c0[b] + dc;
             const bool ok = real[b] && rr >= 0 && rr < side && cc >= 0 && cc < side;
-            const uint16_t* src = p.Gin + ((tok0[b] + (ok ? rr * side + cc : 0)) * KS * 4 + g) * 8;
+            const uint16_t* src = (ok ? p.Gin + (tok0[b] + rr * side + cc) * KS * 32 : p.zero) + g * 8;
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                const u16x8 v = *reinterpret_cast<const u16x8*>(src + ks * 32);
-                xb[SLOT][ks][b] = __builtin_bit_cast(bf16x8, ok ? v : u16x8{0, 0, 0, 0, 0, 0, 0, 0});
-            }
+            for (int ks = 0; ks < KS; ++ks)
+                xb[SLOT][ks][b] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(src + ks * 32));
         }
     };
     // chunk C of a tap (fragments C*CHUNK .. of the tap's [row tile][k-step] order) on the
-    // gathered fragments in buffer SLOT; after_sync() runs once the chunk is visible
-    auto chunk = [&](auto par, auto cidx, auto slot, int ci, const auto& after_sync) {
+    // gathered fragments in slot SLOT. YOUNGER: vector memory operations issued after this
+    // chunk's last weight load (prefetched gathers); extra(r) runs after fragment read r.
+    auto chunk = [&](auto par, auto cidx, auto slot, auto younger, int ci, const auto& extra) {
         constexpr int PAR = decltype(par)::value, C = decltype(cidx)::value, SLOT = decltype(slot)::value;
-        const uint16_t* buf = pipe.template sync<PAR, 0>(ci);   // also awaits the gathers
-        after_sync();
+        const uint16_t* buf = pipe.template sync<PAR, decltype(younger)::value>(ci);
         const uint16_t* nx = pipe.next(ci);
         pipelined<CHUNK, LA>(
             [&](int r) { return lds_frag(buf, r, lane); },
@@ -789,37 +792,39 @@ __global__ __launch_bounds__(256, 2) void conv_kernel(ConvParams p) {
 #pragma unroll
                 for (int b = 0; b < TB; ++b) acc[rt][b] = mfma16x16x32(a, xb[SLOT][ks][b], acc[rt][b]);
             },
-            [&](int r) { pipe.template after_read<1 - PAR, CHUNK, LA>(nx, r); });
-        sched_pipeline<CHUNK, TB, LA>();
-    };
-    // par0: LDS buffer of the tap's first chunk; slot: the tap's gather buffer (tap % 2 with
-    // double buffering, which then prefetches tap + 1 into the other one)
-    auto tap_body = [&](auto par0, auto slot, int tap) {
-        constexpr int P0 = decltype(par0)::value, SLOT = decltype(slot)::value;
-        if constexpr (!PF) gather(slot, tap);
-        static_for<TAP_CHUNKS>([&](auto c) {
-            constexpr int C = decltype(c)::value;
-            chunk(std::integral_constant<int, (P0 + C) & 1>{}, c, slot, tap * TAP_CHUNKS + C, [&] {
-                if constexpr (PF && C == 0)   // (slot 0 when single-buffered: never instantiated)
-                    if (tap + 1 < 9) gather(std::integral_constant<int, PF ? 1 - SLOT : 0>{}, tap + 1);
+            [&](int r) {
+                pipe.template after_read<1 - PAR, CHUNK, LA>(nx, r);
+                extra(r);
             });
-        });
+        sched_pipeline<CHUNK, TB, LA>();
     };
     using I0 = std::integral_constant<int, 0>;
     using I1 = std::integral_constant<int, 1>;
-    if constexpr (PF) gather(I0{}, 0);
-    if constexpr (TAP_CHUNKS % 2 == 0 && !PF) {
-        for (int tap = 0; tap < 9; ++tap) tap_body(I0{}, I0{}, tap);
+    if constexpr (NSLOT == 3) {
+        static_assert(TAP_CHUNKS == 1, "one chunk per tap");
+        constexpr int LAST = WeightPipe<CHUNK, WAVES>::template last_load_read<CHUNK, LA>();
+        gather(I0{}, 0);
+        gather(I1{}, 1);
+        static_for<9>([&](auto tc) {
+            constexpr int T = decltype(tc)::value;
+            // at chunk T's sync, tap T + 1's gathers (issued after chunk T - 1's last weight
+            // load, or after chunk 0's first loads in the prologue) may still be in flight
+            constexpr int YOUNGER = T + 1 < 9 ? KS * TB : 0;
+            chunk(std::integral_constant<int, T & 1>{}, I0{}, std::integral_constant<int, T % 3>{},
+                  std::integral_constant<int, YOUNGER>{}, T, [&](int r) {
+                      if constexpr (T + 2 < 9)
+                          if (r == LAST) gather(std::integral_constant<int, (T + 2) % 3>{}, T + 2);
+                  });
+        });
     } else {
-        // taps in pairs: the LDS buffer parity (odd chunk counts per tap) and the gather slot
-        // alternate with the tap; tap 8 is even
-        static_assert(TAP_CHUNKS % 2 == 1 || PF, "pairs");
-        constexpr int Q = TAP_CHUNKS & 1;   // parity step per tap
-        for (int tap = 0; tap < 8; tap += 2) {
-            tap_body(I0{}, I0{}, tap);
-            tap_body(std::integral_constant<int, Q>{}, I1{}, tap + 1);
+        static_assert(TAP_CHUNKS % 2 == 0, "chunk parity is the chunk's index within its tap");
+        for (int tap = 0; tap < 9; ++tap) {
+            gather(I0{}, tap);
+            static_for<TAP_CHUNKS>([&](auto c) {
+                constexpr int C = decltype(c)::value;
+                chunk(std::integral_constant<int, C & 1>{}, c, I0{}, I0{}, tap * TAP_CHUNKS + C, [](int) {});
+            });
         }
-        tap_body(I0{}, I0{}, 8);
     }
 
     // X += ReLU(acc); the output's B fragments for the next unit
