@@ -444,6 +444,11 @@ PWD_DEV void attn_passes(const AttnShape& sh, const AttnItem& it, int qbeg, int 
 
 // One workgroup per (window, head); K/V stay in LDS for the whole item. Up to 4 wavefronts
 // two workgroups share a CU; 8 wavefronts (tiles above 80 KB) keep two per SIMD on their own.
+// Heads of 16 share their K/V fragments with the neighbouring head, so a workgroup stages
+// the fragments once and runs both heads of the pair in turn.
+template <int DH>
+constexpr int heads_per_item() { return DH == 16 ? 2 : 1; }
+
 template <int DH, int WAVES>
 __global__ __launch_bounds__(WAVES * 64, WAVES == 8 ? 1 : 2) void attn_kernel(AttnParams p) {
     constexpr int NF = Frag<DH>::NF, QM = Frag<DH>::QMAX;
@@ -454,7 +459,8 @@ __global__ __launch_bounds__(WAVES * 64, WAVES == 8 ? 1 : 2) void attn_kernel(At
     uint16_t* ks = reinterpret_cast<uint16_t*>(smem);   // [nbw][NF][512]: K fragments
     uint16_t* vs = ks + (size_t)nbw * NF * 512;          // [nbw + 1][NF][512]: V tiles, + a zero block
     __shared__ float kmax_w[WAVES];
-    AttnItem it = make_item<DH>(p, sh, blockIdx.x);
+    constexpr int HPI = heads_per_item<DH>();
+    AttnItem it = make_item<DH>(p, sh, blockIdx.x * HPI);   // the pair's first head
     it.ks = ks;
     it.vs = vs;
 
@@ -472,14 +478,35 @@ __global__ __launch_bounds__(WAVES * 64, WAVES == 8 ? 1 : 2) void attn_kernel(At
             reinterpret_cast<uint32_t*>(vs + (size_t)nbw * NF * 512)[i] = 0u;
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-    const float kw = kmax2_blocks<DH>(sh, ks, it.slot0, wave, WAVES, lane);
-    if (lane == 0) kmax_w[wave] = kw;
-    __syncthreads();
-    float kmax2 = 0.f;
+    if constexpr (HPI == 1) {
+        const float kw = kmax2_blocks<DH>(sh, ks, it.slot0, wave, WAVES, lane);
+        if (lane == 0) kmax_w[wave] = kw;
+        __syncthreads();
+        float kmax2 = 0.f;
 #pragma unroll
-    for (int w = 0; w < WAVES; ++w) kmax2 = fmaxf(kmax2, kmax_w[w]);
-    it.kmax = sqrtf(kmax2);
-    if (qbeg < qend) attn_passes<DH>(sh, it, qbeg, qend, qnext, ones_row(lane), lane);
+        for (int w = 0; w < WAVES; ++w) kmax2 = fmaxf(kmax2, kmax_w[w]);
+        it.kmax = sqrtf(kmax2);
+        if (qbeg < qend) attn_passes<DH>(sh, it, qbeg, qend, qnext, ones_row(lane), lane);
+    } else {
+        // both heads of the pair in turn: each its slots of the same fragments and its own
+        // max |k| (the second reloads its Q after a barrier that retires the first's kmax_w)
+        for (int hh = 0; hh < 2; ++hh) {
+            if (hh > 0) {
+                it.slot0 += 4;
+                it.vhalf += 1;
+                if (qbeg < qend) load_q<NF, QM>(sh, it.q0, qbeg, qend, lane, qnext);
+                __syncthreads();
+            }
+            const float kw = kmax2_blocks<DH>(sh, ks, it.slot0, wave, WAVES, lane);
+            if (lane == 0) kmax_w[wave] = kw;
+            __syncthreads();
+            float kmax2 = 0.f;
+#pragma unroll
+            for (int w = 0; w < WAVES; ++w) kmax2 = fmaxf(kmax2, kmax_w[w]);
+            it.kmax = sqrtf(kmax2);
+            if (qbeg < qend) attn_passes<DH>(sh, it, qbeg, qend, qnext, ones_row(lane), lane);
+        }
+    }
 }
 
 template <int DH, int WAVES>
@@ -488,7 +515,7 @@ hipError_t launch_shape(const AttnParams& p, int nwin, hipStream_t s) {
     hipError_t e = hipFuncSetAttribute((const void*)attn_kernel<DH, WAVES>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     if (e != hipSuccess) return e;
-    attn_kernel<DH, WAVES><<<dim3((unsigned)nwin * p.H), dim3(WAVES * 64), smem, s>>>(p);
+    attn_kernel<DH, WAVES><<<dim3((unsigned)nwin * p.H / heads_per_item<DH>()), dim3(WAVES * 64), smem, s>>>(p);
     return hipGetLastError();
 }
 
