@@ -37,11 +37,16 @@ extern "C" {
 
 typedef struct pwd_decoder pwd_decoder; /* opaque handle */
 
-/* Window geometry (Sec. 3.1, App. A.1.1). A window has window_rounds rounds: a left
- * buffer of floor((window_rounds - distance) / 2) rounds, a core of `distance` rounds and
- * a right buffer of the rest. distance: odd, 3..63 within the on-chip limits that
- * decoder_validate_config states (bf16: up to 35). window_rounds: distance..3*distance.
- * max_windows: the largest batch decode_windows will be given (scratch is sized for it). */
+/* Window geometry (Sec. 3.1, App. A.1.1 boundary padding, App. A.1.2: a window is b + c + b
+ * rounds). A window has window_rounds rounds: a left buffer of
+ * floor((window_rounds - distance) / 2) rounds, a core of `distance` rounds and a right
+ * buffer of the rest. There is no separate core-length field: the core length c always
+ * equals the code distance (the paper's windows take c = d; every window of a stream then
+ * owns exactly d rounds, App. A.1.1), so the geometry is fixed by distance and
+ * window_rounds alone. distance: odd, 3..63 within the on-chip limits that
+ * decoder_validate_config states (bf16: up to 35). window_rounds: distance..3*distance (the
+ * paper's b = c = d is window_rounds = 3*distance). max_windows: the largest batch
+ * decode_windows will be given (scratch is sized for it). */
 typedef struct {
     int32_t distance;
     int32_t window_rounds;
@@ -143,10 +148,17 @@ size_t decoder_blob_floats(const pwd_geometry* geom, const pwd_model_dims* dims)
  * d <= 5 at d_model 64). Returns PWD_OK, PWD_EINVAL (null) or PWD_EUNSUPPORTED. */
 int decoder_validate_config(const pwd_geometry* geom, const pwd_model_dims* dims);
 
-/* Creates a decoder on the current HIP device: validates, parses the blob (blob_bytes
- * must equal 64 + 4 * decoder_blob_floats), rearranges the weights into the kernels'
- * layouts, uploads them and allocates scratch for max_windows windows. The caller may
- * free weight_blob on return. *out is set only on success. */
+/* Creates a decoder on the current HIP device. The blob carries the parameters of the
+ * network of the App. A model table (StabilizerEmbedder Linear(1 -> d_model), the Syndrome
+ * Transformer layers of App. A.2 with the fold of the recurrent state, the readout of
+ * App. A.3) in the order listed above; decoder_create validates the dimensions, parses the
+ * blob (blob_bytes must equal 64 + 4 * decoder_blob_floats; PWD_EBLOB on a bad magic,
+ * version, size or a header word that disagrees with geom / dims), computes the
+ * positional encoding of App. A.1.4 on the host, rearranges the weights into the kernels'
+ * layouts, uploads them and allocates scratch for max_windows windows (PWD_ENOMEM if the
+ * device allocation fails). The caller keeps ownership of weight_blob and may free it on
+ * return; the handle owns its device memory until decoder_destroy. *out is set only on
+ * success. */
 int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims,
                    const void* weight_blob, size_t blob_bytes, pwd_decoder** out);
 
@@ -174,9 +186,18 @@ int decode_windows(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_ty
 int decode_windows_recurrent(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_types,
                              int64_t n_windows, float* d_logits, uint8_t* d_bits, void* hip_stream);
 
-/* Writes the detection events the decoder feeds to its network:
- * d_events uint32 [n_windows][window_rounds][words], packed as the input. Same masks and
- * type check as decode_windows (an invalid type yields all-zero events). */
+/* Writes the detection events the decoder feeds to its network (Sec. 2.2: a detector is the
+ * parity of two consecutive measurements of one stabilizer; Sec. 3.2: the model takes hard
+ * detection events as its only input; App. A.1.1: zero padding in place of the missing
+ * buffer of the initial and final windows):
+ *   E[t] = M[t+1] xor M[t], t = 0 .. window_rounds - 1; an initial window zeroes E[t] for
+ *   t < left buffer and compares its first core round with the all-zero state; a final
+ *   window zeroes E[t] from the end of its core on.
+ * d_meas and d_types as for decode_windows; d_events: uint32 [n_windows][window_rounds][words]
+ * out (caller-allocated, device), packed as the input with bits >= d*d-1 written as 0. An
+ * invalid type yields all-zero events for that window and makes the next
+ * decoder_sync_status return PWD_EDEVICE. PWD_EINVAL on a null buffer or negative n,
+ * PWD_EBATCH if n_windows > max_windows; n_windows = 0 is a no-op. */
 int decoder_detection_events(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_types,
                              int64_t n_windows, uint32_t* d_events, void* hip_stream);
 

@@ -138,6 +138,34 @@ def make_blob(d: int, W: int, D: int, L: int, H: int, F: int, dtype: int, weight
     return struct.pack("<16I", *hdr) + body.tobytes()
 
 
+def _dtype_names(t) -> str:
+    return str(t.dtype).replace("torch.", "")
+
+
+def require(t, name: str, dtypes: tuple, device: int, shape: tuple | None = None, min_numel: int | None = None):
+    """Checks a device buffer before its pointer crosses the ABI: a CUDA tensor on the decoder's
+    device, of one of `dtypes` (names such as "int32"), contiguous, and of exactly `shape` or at
+    least `min_numel` elements. The kernels index these buffers with the decoder's geometry, so
+    a mismatch would be an out-of-bounds device access; it raises ValueError instead."""
+    if t is None:
+        raise ValueError(f"{name}: a tensor is required")
+    if not getattr(t, "is_cuda", False):
+        raise ValueError(f"{name}: must be a CUDA tensor (got device {getattr(t, 'device', '?')})")
+    if t.device.index is not None and t.device.index != device:
+        raise ValueError(f"{name}: on cuda:{t.device.index}, the decoder is on cuda:{device}")
+    if _dtype_names(t) not in dtypes:
+        raise ValueError(f"{name}: dtype {_dtype_names(t)}, need one of {', '.join(dtypes)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: shape {tuple(t.shape)}, need {tuple(shape)}")
+    if min_numel is not None and t.numel() < min_numel:
+        raise ValueError(f"{name}: {t.numel()} elements, need at least {min_numel}")
+
+
+WORDS = ("int32", "uint32")
+
+
 def _stream_ptr(stream) -> ctypes.c_void_p:
     if stream is None:
         import torch
@@ -161,6 +189,8 @@ class Decoder:
         buf = ctypes.create_string_buffer(blob, len(blob))
         _check(lib.decoder_create(ctypes.byref(g), ctypes.byref(m), buf, len(blob), ctypes.byref(h)))
         self._h = h
+        import torch
+        self.device = torch.cuda.current_device()   # decoder_create uses the current HIP device
 
     @classmethod
     def from_workload(cls, wl, weights: dict, max_windows: int | None = None) -> "Decoder":
@@ -170,9 +200,21 @@ class Decoder:
         dil = tuple(weights["dilations"]) if weights.get("dilations") else (0, 0, 0)
         return cls(wl.d, wl.W, max_windows or wl.B, wl.D, wl.L, wl.H, wl.mlp_ratio, wl.dtype, blob, ts, emb, dil)
 
+    def _windows_in(self, meas, types) -> int:
+        require(types, "types", ("uint8",), self.device)
+        if types.dim() != 1:
+            raise ValueError(f"types: shape {tuple(types.shape)}, need (n,)")
+        n = types.shape[0]
+        if n > self.max_windows:
+            raise ValueError(f"{n} windows, the decoder was created for at most {self.max_windows}")
+        require(meas, "meas", WORDS, self.device, shape=(n, self.W + 1, self.words))
+        return n
+
     def decode(self, meas, types, logits, bits, stream=None):
         """meas: int32/uint32 [n][W+1][words] cuda tensor; types: uint8 [n]; outputs float32/uint8 [n]."""
-        n = types.shape[0]
+        n = self._windows_in(meas, types)
+        require(logits, "logits", ("float32",), self.device, min_numel=n)
+        require(bits, "bits", ("uint8",), self.device, min_numel=n)
         _check(self._lib.decode_windows(self._h, ctypes.c_void_p(meas.data_ptr()),
                                         ctypes.c_void_p(types.data_ptr()), n,
                                         ctypes.c_void_p(logits.data_ptr()), ctypes.c_void_p(bits.data_ptr()),
@@ -181,7 +223,9 @@ class Decoder:
     def decode_recurrent(self, meas, types, logits, bits, stream=None):
         """As decode, with outputs float32 / uint8 [n][distance]: a readout after each of the
         last `distance` rounds (the recurrent branch of Algorithm 1)."""
-        n = types.shape[0]
+        n = self._windows_in(meas, types)
+        require(logits, "logits", ("float32",), self.device, min_numel=n * self.d)
+        require(bits, "bits", ("uint8",), self.device, min_numel=n * self.d)
         _check(self._lib.decode_windows_recurrent(self._h, ctypes.c_void_p(meas.data_ptr()),
                                                   ctypes.c_void_p(types.data_ptr()), n,
                                                   ctypes.c_void_p(logits.data_ptr()),
@@ -192,11 +236,24 @@ class Decoder:
         out; prob: float32 [1] out or None; window_logits / window_bits: float32 / uint8
         [ceil(T/d)] out or None."""
         ptr = lambda t: ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+        require(rounds, "rounds", WORDS, self.device)
+        if rounds.dim() != 2 or rounds.shape[1] != self.words:
+            raise ValueError(f"rounds: shape {tuple(rounds.shape)}, need (T, {self.words})")
+        m = -(-rounds.shape[0] // self.d)
+        require(bit, "bit", ("uint8",), self.device, min_numel=1)
+        if prob is not None:
+            require(prob, "prob", ("float32",), self.device, min_numel=1)
+        if window_logits is not None:
+            require(window_logits, "window_logits", ("float32",), self.device, min_numel=m)
+        if window_bits is not None:
+            require(window_bits, "window_bits", ("uint8",), self.device, min_numel=m)
         _check(self._lib.decode_stream(self._h, ptr(rounds), rounds.shape[0], ptr(window_logits),
                                        ptr(window_bits), ptr(bit), ptr(prob), _stream_ptr(stream)))
 
     def detection_events(self, meas, types, events, stream=None):
-        n = types.shape[0]
+        """events: int32/uint32 [n][W][words] out."""
+        n = self._windows_in(meas, types)
+        require(events, "events", WORDS, self.device, shape=(n, self.W, self.words))
         _check(self._lib.decoder_detection_events(self._h, ctypes.c_void_p(meas.data_ptr()),
                                                   ctypes.c_void_p(types.data_ptr()), n,
                                                   ctypes.c_void_p(events.data_ptr()), _stream_ptr(stream)))

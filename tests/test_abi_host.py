@@ -129,3 +129,71 @@ def test_bad_blobs_rejected_before_device_use(lib, how):
     assert rc == pwdec.PWD_EBLOB
     assert not h.value
     assert b"blob" in lib.decoder_last_error()
+
+
+class FakeTensor:
+    """Stands in for a torch tensor in the binding's argument checks (no device needed)."""
+
+    def __init__(self, shape, dtype="int32", cuda=True, index=0, contiguous=True):
+        self.shape, self._contig = tuple(shape), contiguous
+        self.dtype = f"torch.{dtype}"
+        self.is_cuda = cuda
+        self.device = type("Dev", (), {"index": index})()
+
+    def is_contiguous(self):
+        return self._contig
+
+    def numel(self):
+        n = 1
+        for s in self.shape:
+            n *= s
+        return n
+
+    def dim(self):
+        return len(self.shape)
+
+
+def test_binding_rejects_buffers_the_kernels_would_overrun():
+    """Every device buffer is checked before its pointer crosses the ABI: a mismatch raises
+    ValueError instead of an out-of-bounds access on the device."""
+    req = pwdec.require
+    req(FakeTensor((4, 15, 2)), "meas", pwdec.WORDS, 0, shape=(4, 15, 2))
+    req(FakeTensor((4,), "float32"), "logits", ("float32",), 0, min_numel=4)
+    bad = [
+        (FakeTensor((4, 15, 2), cuda=False), dict(shape=(4, 15, 2))),           # host memory
+        (FakeTensor((4, 15, 2), index=1), dict(shape=(4, 15, 2))),              # another GPU
+        (FakeTensor((4, 15, 2), "int64"), dict(shape=(4, 15, 2))),              # wrong dtype
+        (FakeTensor((4, 15, 2), contiguous=False), dict(shape=(4, 15, 2))),     # a strided view
+        (FakeTensor((4, 14, 2)), dict(shape=(4, 15, 2))),                       # W rows, not W + 1
+        (FakeTensor((3,)), dict(min_numel=4)),                                  # too few outputs
+    ]
+    for t, kw in bad:
+        with pytest.raises(ValueError):
+            req(t, "x", pwdec.WORDS, 0, **kw)
+    with pytest.raises(ValueError):
+        req(None, "x", pwdec.WORDS, 0)
+
+
+def test_binding_checks_every_entry_point():
+    """The Decoder methods check their buffers against the handle's geometry before calling
+    the library: decode's [n] outputs are too small for the recurrent [n][d] outputs, a meas
+    tensor of the wrong geometry or a batch above max_windows is refused."""
+    dec = object.__new__(pwdec.Decoder)
+    dec.d, dec.W, dec.words, dec.max_windows, dec.device = 7, 14, 2, 8, 0
+    dec._lib, dec._h = None, None     # never reached: every call below fails its checks
+    meas, types = FakeTensor((4, 15, 2)), FakeTensor((4,), "uint8")
+    f4, u4 = FakeTensor((4,), "float32"), FakeTensor((4,), "uint8")
+    with pytest.raises(ValueError):
+        dec.decode_recurrent(meas, types, f4, u4)                      # needs n * d outputs
+    with pytest.raises(ValueError):
+        dec.decode(FakeTensor((4, 14, 2)), types, f4, u4)              # meas of another window
+    with pytest.raises(ValueError):
+        dec.decode(FakeTensor((9, 15, 2)), FakeTensor((9,), "uint8"), FakeTensor((9,), "float32"),
+                   FakeTensor((9,), "uint8"))                           # above max_windows
+    with pytest.raises(ValueError):
+        dec.detection_events(meas, types, FakeTensor((4, 15, 2)))      # events have W rows
+    with pytest.raises(ValueError):
+        dec.decode_stream(FakeTensor((40, 3)), FakeTensor((1,), "uint8"))   # 3 words per round
+    with pytest.raises(ValueError):
+        dec.decode_stream(FakeTensor((40, 2)), FakeTensor((1,), "uint8"),
+                          window_logits=FakeTensor((5,), "float32"))    # 6 windows

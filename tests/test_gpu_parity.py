@@ -4,6 +4,7 @@ Small batches (several token tiles and a ragged tail) compare every window; at t
 batch sizes of each workload, windows the oracle can afford are compared one by one and
 the rest are checked through batch invariance and output consistency."""
 import copy
+import ctypes
 import math
 
 import numpy as np
@@ -114,16 +115,22 @@ def test_invalid_type_and_batch_limits(name):
     ok = np.arange(B) != 4
     assert np.array_equal(logits[ok].view(np.uint32), good[ok].view(np.uint32))
     assert dec.sync_status() == pwdec.PWD_OK
-    # n = 0 is a no-op; n > max_windows is refused before any launch
+    # n = 0 is a no-op; n > max_windows is refused before any launch, by the binding
+    # (ValueError) and by the library itself (PWD_EBATCH through the raw ABI)
+    wl = synth.WORKLOADS[name]
     z = torch.zeros(1, dtype=torch.float32, device="cuda")
     zb = torch.zeros(1, dtype=torch.uint8, device="cuda")
-    mt = torch.zeros((1, 1), dtype=torch.int32, device="cuda")
+    mt = torch.zeros((0, wl.W + 1, wl.words), dtype=torch.int32, device="cuda")
     dec.decode(mt, torch.zeros(0, dtype=torch.uint8, device="cuda"), z, zb)
     big = SMALL[name] + 1
-    with pytest.raises(pwdec.PwdError) as ei:
-        dec.decode(torch.zeros((big, 1), dtype=torch.int32, device="cuda"),
-                   torch.zeros(big, dtype=torch.uint8, device="cuda"), z, zb)
-    assert ei.value.code == pwdec.PWD_EBATCH
+    mb = torch.zeros((big, wl.W + 1, wl.words), dtype=torch.int32, device="cuda")
+    tb = torch.zeros(big, dtype=torch.uint8, device="cuda")
+    with pytest.raises(ValueError):
+        dec.decode(mb, tb, z, zb)
+    vp = ctypes.c_void_p
+    rc = dec._lib.decode_windows(dec._h, vp(mb.data_ptr()), vp(tb.data_ptr()), big, vp(z.data_ptr()),
+                                 vp(zb.data_ptr()), vp(torch.cuda.current_stream().cuda_stream))
+    assert rc == pwdec.PWD_EBATCH
 
 
 @pytest.mark.parametrize("name", ["d7", "d11", "d17", "d25"])
