@@ -59,7 +59,12 @@ def load_library() -> ctypes.CDLL:
         return _lib
     if not os.path.exists(LIB_PATH):
         raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_2601_09921_amd.build.build()")
-    lib = ctypes.CDLL(LIB_PATH)
+    _lib = bind(ctypes.CDLL(LIB_PATH))
+    return _lib
+
+
+def bind(lib: ctypes.CDLL) -> ctypes.CDLL:
+    """Declares the argument and result types of the include/pwdec.h entry points on `lib`."""
     P, I64, VP = ctypes.POINTER, ctypes.c_int64, ctypes.c_void_p
     sig = {
         "decoder_blob_floats": (ctypes.c_size_t, [P(Geometry), P(ModelDims)]),
@@ -78,7 +83,6 @@ def load_library() -> ctypes.CDLL:
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
         fn.restype, fn.argtypes = res, args
-    _lib = lib
     return lib
 
 

@@ -1,0 +1,287 @@
+// simt.h - a host (x86-64) stand-in for the HIP runtime and the gfx950 device features the
+// decoder's kernels use, so that the library's own kernel sources can be compiled for the CPU
+// and run there under memory checks. Test infrastructure only: nothing in the library loads it.
+//
+// Execution model. A launch runs its workgroups one after another; each work-item is a fiber
+// with its own stack, and fibers switch only at synchronisation points:
+//   * __syncthreads: every live work-item of the workgroup arrives;
+//   * cross-lane operations (MFMA, shuffles, readfirstlane, ballot): every live lane of the
+//     wavefront arrives, each having posted its operands to the wavefront's exchange slots.
+// So the kernel code runs unmodified, lane by lane, with the same data exchange as on the GPU.
+// Lanes of a wavefront that disagree on the sequence of cross-lane operations, or a barrier
+// that not every work-item reaches, end in a reported deadlock.
+//
+// Memory checks. hipMalloc places every allocation against a PROT_NONE guard page (after its
+// end, or before its start with EMU_GUARD=start), so an access past it faults on the host with
+// the allocation, the kernel, the workgroup and the work-item named. LDS (static __shared__
+// arrays and the dynamic allocation) lives in one linker section, is filled with 0xff (a NaN
+// pattern) before every workgroup, and the direct global->LDS loads land only when the issuing
+// lane waits for its vector memory counter, so LDS read before its wait shows up as NaN.
+#pragma once
+#include <cmath>
+#include <cstddef>
+#include <cstdint>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+#include <tuple>
+#include <type_traits>
+#include <utility>
+
+// ---- qualifiers
+#define __global__
+#define __device__
+#define __host__
+#define __forceinline__ inline
+#define __launch_bounds__(...)
+#define __align__(n) __attribute__((aligned(n)))
+#define __shared__ static __attribute__((section("emu_lds")))
+
+// ---- runtime types
+typedef enum hipError_t {
+    hipSuccess = 0,
+    hipErrorInvalidValue = 1,
+    hipErrorOutOfMemory = 2,
+    hipErrorLaunchFailure = 719,
+} hipError_t;
+typedef enum hipMemcpyKind {
+    hipMemcpyHostToHost = 0,
+    hipMemcpyHostToDevice = 1,
+    hipMemcpyDeviceToHost = 2,
+    hipMemcpyDeviceToDevice = 3,
+    hipMemcpyDefault = 4
+} hipMemcpyKind;
+typedef enum hipFuncAttribute { hipFuncAttributeMaxDynamicSharedMemorySize = 8 } hipFuncAttribute;
+struct ihipStream_t;
+typedef ihipStream_t* hipStream_t;
+struct ihipEvent_t;
+typedef ihipEvent_t* hipEvent_t;
+
+struct dim3 {
+    uint32_t x, y, z;
+    constexpr dim3(uint32_t x_ = 1, uint32_t y_ = 1, uint32_t z_ = 1) : x(x_), y(y_), z(z_) {}
+};
+struct emu_uint3 {
+    uint32_t x, y, z;
+};
+
+hipError_t hipMalloc(void** p, size_t bytes);
+template <class T>
+hipError_t hipMalloc(T** p, size_t bytes) { return hipMalloc(reinterpret_cast<void**>(p), bytes); }
+hipError_t hipFree(void* p);
+hipError_t hipMemcpy(void* dst, const void* src, size_t bytes, hipMemcpyKind);
+hipError_t hipMemcpyAsync(void* dst, const void* src, size_t bytes, hipMemcpyKind, hipStream_t = nullptr);
+hipError_t hipMemset(void* p, int v, size_t bytes);
+hipError_t hipMemsetAsync(void* p, int v, size_t bytes, hipStream_t = nullptr);
+hipError_t hipGetDevice(int* d);
+hipError_t hipSetDevice(int d);
+hipError_t hipGetLastError();
+const char* hipGetErrorString(hipError_t e);
+hipError_t hipStreamSynchronize(hipStream_t);
+hipError_t hipDeviceSynchronize();
+hipError_t hipEventCreate(hipEvent_t* e);
+hipError_t hipEventDestroy(hipEvent_t e);
+hipError_t hipEventRecord(hipEvent_t e, hipStream_t = nullptr);
+hipError_t hipEventSynchronize(hipEvent_t e);
+hipError_t hipEventElapsedTime(float* ms, hipEvent_t a, hipEvent_t b);
+hipError_t hipFuncSetAttribute(const void*, hipFuncAttribute, int);
+hipError_t hipGetSymbolAddress(void** p, const void* symbol);
+#define HIP_SYMBOL(x) (&(x))
+
+// ---- device-side vector types (identical to the kernels' own typedefs)
+typedef __bf16 emu_bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 emu_bf16x4 __attribute__((ext_vector_type(4)));
+typedef float emu_f32x4 __attribute__((ext_vector_type(4)));
+
+namespace emu {
+
+struct Group {
+    uint64_t gen = 0;
+    int arrived = 0;
+    int alive = 0;
+};
+
+struct Wave {
+    Group bar;
+    alignas(16) unsigned char slot[2][64][64];   // double-buffered exchange, 64 bytes per lane
+    uint64_t tag[2][64];                         // (kind, sequence number) each lane posted
+};
+
+struct Fiber {
+    void* sp = nullptr;
+    void* stack = nullptr;
+    size_t stack_bytes = 0;
+    emu_uint3 tid{0, 0, 0}, bid{0, 0, 0};
+    int lane = 0, wave = 0, xset = 0;
+    uint32_t xseq = 0;   // cross-lane operations this lane has posted
+    bool done = false;
+    Group* wait_g = nullptr;
+    uint64_t wait_gen = 0;
+    // direct global->LDS loads issued by this lane and not yet waited for
+    struct Dma { uint32_t lds; int bytes; unsigned char data[16]; };
+    Dma pend[64];
+    int npend = 0;
+};
+
+extern Fiber* g_cur;
+extern emu_uint3 g_block_dim, g_grid_dim;
+extern Wave* g_waves;
+extern Group g_block;
+
+void barrier(Group& g);
+void check_tags();
+inline void wave_sync() {
+    barrier(g_waves[g_cur->wave].bar);
+    check_tags();
+}
+inline void block_sync() { barrier(g_block); }
+
+// Posts this lane's operand of a cross-lane operation of the given kind; after the wavefront
+// barrier every lane checks that all lanes posted the same operation (a lane that skips or
+// adds one would otherwise silently pair with another operation).
+template <class T>
+inline void xput(const T& v, uint32_t kind = sizeof(T)) {
+    static_assert(sizeof(T) <= 64, "exchange slot");
+    Wave& w = g_waves[g_cur->wave];
+    std::memcpy(w.slot[g_cur->xset][g_cur->lane], &v, sizeof(T));
+    w.tag[g_cur->xset][g_cur->lane] = ((uint64_t)kind << 32) | g_cur->xseq++;
+}
+template <class T>
+inline T xget(int lane) {
+    T r;
+    std::memcpy(&r, g_waves[g_cur->wave].slot[g_cur->xset][lane & 63], sizeof(T));
+    return r;
+}
+inline void xdone() { g_cur->xset ^= 1; }
+template <class T>
+inline T exchange(const T& v, int src_lane) {
+    xput(v);
+    wave_sync();
+    const T r = xget<T>(src_lane);
+    xdone();
+    return r;
+}
+
+char* lds_base();
+size_t lds_bytes();
+void* dyn_smem();
+void lds_dma(int bytes, uint32_t voff, const void* sbase, uint32_t m0);
+void waitcnt();
+void report(const char* fmt, ...);
+int errors();
+
+// Launch: workgroups in order, each as block.x fibers that run k(args...).
+using Body = void (*)(void*);
+void run_grid(const char* what, dim3 grid, dim3 block, size_t smem, Body body, void* ctx);
+
+template <class K, class Tup>
+struct LaunchCtx {
+    K k;
+    Tup args;
+};
+template <class K, class Tup>
+void call_kernel(void* c) {
+    auto* x = static_cast<LaunchCtx<K, Tup>*>(c);
+    std::apply(x->k, x->args);
+}
+template <class K, class... A>
+void launch(const char* what, K k, dim3 grid, dim3 block, size_t smem, hipStream_t, A&&... args) {
+    using Tup = std::tuple<std::decay_t<A>...>;
+    LaunchCtx<K, Tup> ctx{k, Tup(std::forward<A>(args)...)};
+    run_grid(what, grid, block, smem, &call_kernel<K, Tup>, &ctx);
+}
+
+}  // namespace emu
+
+#define threadIdx (emu::g_cur->tid)
+#define blockIdx (emu::g_cur->bid)
+#define blockDim (emu::g_block_dim)
+#define gridDim (emu::g_grid_dim)
+
+inline void __syncthreads() { emu::block_sync(); }
+
+template <class T>
+inline T __shfl_xor(T v, int mask, int width = 64) {
+    const int lane = emu::g_cur->lane, src = lane ^ mask;
+    return emu::exchange(v, (src & ~(width - 1)) == (lane & ~(width - 1)) ? src : lane);
+}
+template <class T>
+inline T __shfl(T v, int src, int width = 64) {
+    const int lane = emu::g_cur->lane;
+    return emu::exchange(v, (lane & ~(width - 1)) + (src & (width - 1)));
+}
+
+template <class A, class B>
+inline std::common_type_t<A, B> min(A a, B b) { return a < b ? a : b; }
+template <class A, class B>
+inline std::common_type_t<A, B> max(A a, B b) { return a < b ? b : a; }
+inline float rsqrtf(float x) { return 1.0f / std::sqrt(x); }
+
+template <class T>
+inline T atomicOr(T* p, T v) {
+    const T old = *p;
+    *p = old | v;
+    return old;
+}
+
+// ---- the AMDGPU builtins the kernels call (their sources are renamed emu_amdgcn_*)
+template <class T>
+inline T emu_amdgcn_readfirstlane(T v) { return emu::exchange(v, 0); }
+inline uint64_t emu_amdgcn_ballot_w64(bool b) {
+    emu::xput<int>(b ? 1 : 0);
+    emu::wave_sync();
+    uint64_t m = 0;
+    for (int l = 0; l < 64; ++l)
+        if (emu::xget<int>(l)) m |= 1ull << l;
+    emu::xdone();
+    return m;
+}
+inline float emu_amdgcn_exp2f(float x) { return std::exp2(x); }
+inline void emu_amdgcn_sched_group_barrier(int, int, int) {}
+inline void emu_amdgcn_sched_barrier(int) {}
+
+// v_mfma_f32_16x16x{32,16}_bf16: D[row][col] = C + sum_k A[row][k] B[k][col]. Lane l holds
+// A row l % 16 and B column l % 16 with the k values of lane group l / 16 in its register
+// elements; the lane's D elements are rows 4 (l / 16) + i of column l % 16. The k order within
+// a lane group does not matter for the sum as long as A and B share it, which both kernels
+// and the host-side weight layout do.
+template <class V, int NV>
+inline emu_f32x4 emu_mfma_16x16(V a, V b, emu_f32x4 c) {
+    struct AB { V a, b; };
+    emu::xput(AB{a, b});
+    emu::wave_sync();
+    const int lane = emu::g_cur->lane, col = lane & 15, g = lane >> 4;
+    AB bcol[4];
+    for (int gg = 0; gg < 4; ++gg) bcol[gg] = emu::xget<AB>(col + 16 * gg);
+    emu_f32x4 d;
+    for (int i = 0; i < 4; ++i) {
+        const int row = 4 * g + i;
+        double s = 0.0;
+        for (int gg = 0; gg < 4; ++gg) {
+            const AB ar = emu::xget<AB>(row + 16 * gg);
+            for (int k = 0; k < NV; ++k) s += (double)(float)ar.a[k] * (double)(float)bcol[gg].b[k];
+        }
+        d[i] = c[i] + (float)s;
+    }
+    emu::xdone();
+    return d;
+}
+inline emu_f32x4 emu_amdgcn_mfma_f32_16x16x32_bf16(emu_bf16x8 a, emu_bf16x8 b, emu_f32x4 c, int, int, int) {
+    return emu_mfma_16x16<emu_bf16x8, 8>(a, b, c);
+}
+inline emu_f32x4 emu_amdgcn_mfma_f32_16x16x16bf16_1k(emu_bf16x4 a, emu_bf16x4 b, emu_f32x4 c, int, int, int) {
+    return emu_mfma_16x16<emu_bf16x4, 4>(a, b, c);
+}
+
+// ---- the kernels' inline assembly, as rewritten by the source transformation
+inline uint32_t emu_lds_off(const void* p) {
+    const char* c = static_cast<const char*>(p);
+    if (c < emu::lds_base() || c >= emu::lds_base() + emu::lds_bytes())
+        emu::report("lds_addr of a pointer outside LDS: %p", p);
+    return (uint32_t)(c - emu::lds_base());
+}
+inline void emu_lds_dma(int bytes, uint32_t voff, const void* sbase, uint32_t m0) {
+    emu::lds_dma(bytes, voff, sbase, m0);
+}
+inline void emu_waitcnt_vm(int) { emu::waitcnt(); }
