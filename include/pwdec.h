@@ -176,6 +176,28 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims,
 int decode_windows(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_types,
                    int64_t n_windows, float* d_logits, uint8_t* d_bits, void* hip_stream);
 
+/* Bytes of device scratch that decode_windows_noalloc can use on each GPU (see there). */
+#define PWD_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+
+/* For callers that cannot allocate device memory at call time or hold a per-handle workspace
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * decode_windows with its activations (fp32 state, Q/K/V, attention output, and the two
+ * convolution buffers with dilated convolutions) in a fixed array of PWD_NOALLOC_SCRATCH_BYTES
+ * that the library reserves in device memory when it is loaded, instead of the handle's
+ * scratch. Arguments, outputs, results and errors as for decode_windows; it calls no hipMalloc,
+ * hipFree or other allocating routine. The bf16 path needs
+ *   (48 * ceil(n_windows * ceil(n_tokens / 16) / 48) * 16 * d_model * 12 bytes
+ * (18 per token and feature with dilated convolutions), at most PWD_NOALLOC_SCRATCH_BYTES, e.g.
+ * up to 68 windows at d = 25 with d_model 256 and 1808 at d = 7 with d_model 128; a larger batch
+ * returns PWD_EBATCH and launches nothing. The fp32 path keeps each window on chip and uses none.
+ * The array is one per GPU and shared by every call and every handle on that GPU, so calls that
+ * overlap on one GPU (two streams, two threads) race and must be serialised by the caller. It
+ * keeps the previous call's contents; no part of it needs to start at any particular value
+ * (every element a decode reads is written earlier in the same decode, except padding blocks
+ * past the batch, whose results are discarded). */
+int decode_windows_noalloc(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_types,
+                           int64_t n_windows, float* d_logits, uint8_t* d_bits, void* hip_stream);
+
 /* The recurrent branch of Algorithm 1 (Sec. recurrent training): the same pass over each
  * window, with a readout of the decoder state after every round n > W - distance (the rounds
  * that complete a window of left buffer, tau core and right buffer rounds, tau = 1..distance).

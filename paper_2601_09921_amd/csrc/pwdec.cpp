@@ -8,6 +8,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -196,6 +197,29 @@ void emb_tables(const std::vector<std::pair<int, int>>& cells, const std::vector
     }
 }
 
+// Scratch of decode_windows_noalloc: the activations (X, Q/K/V, Y and the convolutions' G) of a
+// batch, in device memory the library reserves when it is loaded, so that the entry point needs
+// no allocation. Each GPU holds its own copy; its address is looked up once per device.
+static __device__ __align__(256) unsigned char scratch[PWD_NOALLOC_SCRATCH_BYTES];
+
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[64] = {};
+
+// The device address of `scratch` on `device` (which must be current); looked up on first use.
+int scratch_on(int device, void** out) {
+    if (device < 0 || device >= 64) return fail(PWD_EHIP, "device %d out of range", device);
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[device]) {
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fail(PWD_EHIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+        g_scratch_ptr[device] = p;
+    }
+    *out = g_scratch_ptr[device];
+    return PWD_OK;
+}
+
 }  // namespace
 
 struct pwd_decoder {
@@ -215,6 +239,7 @@ struct pwd_decoder {
     int dil[3] = {0, 0, 0};        // their dilations (0: none)
     size_t conv_off = 0;           // fp32 path: float offset of their tensors in the blob
     int* err = nullptr;
+    void* static_scratch = nullptr;   // device address of `scratch` on this device
     // decode_stream scratch: the windows cut from a stream and their results
     uint32_t* stream_meas = nullptr;   // [max_windows][W + 1][words]
     uint8_t* stream_types = nullptr;   // [max_windows]
@@ -376,9 +401,13 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
 
     int device = 0;
     HIP_OK(hipGetDevice(&device));
+    void* static_scratch = nullptr;   // decode_windows_noalloc's scratch on this device
+    rc = scratch_on(device, &static_scratch);
+    if (rc != PWD_OK) return rc;
     pwd_decoder* dec = new (std::nothrow) pwd_decoder();
     if (!dec) return fail(PWD_ENOMEM, "host allocation failed");
     dec->device = device;
+    dec->static_scratch = static_scratch;
     dec->d = d;
     dec->W = geom->window_rounds;
     dec->max_windows = geom->max_windows;
@@ -642,15 +671,43 @@ static SyndromeIn syndrome_in(const pwd_decoder* dec, const uint32_t* meas, cons
     return in;
 }
 
-// decode_windows with `readouts` readouts after the last `readouts` rounds (1: the inference
-// branch; distance: the recurrent branch), written to d_logits[win * readouts + k].
-static int decode_impl(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_types, int64_t n,
-                       float* d_logits, uint8_t* d_bits, void* hip_stream, int readouts) {
+// The activation buffers of one decode: the handle's own (sized for max_windows) or carved out
+// of the static scratch (decode_windows_noalloc).
+struct Activations {
+    float* X;
+    uint16_t* QKV;
+    uint16_t* Y;
+    uint16_t* G[2];
+};
+
+static Activations handle_activations(const pwd_decoder* dec) {
+    return Activations{dec->X, dec->QKV, dec->Y, {dec->G[0], dec->G[1]}};
+}
+
+// Bytes of X, Q/K/V, Y (and the two G buffers with dilated convolutions) for n_tb token blocks.
+static size_t activation_bytes(const pwd_decoder* dec, int64_t n_tb, size_t* xb, size_t* qb, size_t* yb) {
+    *xb = (size_t)n_tb * 16 * dec->D * sizeof(float);
+    *qb = (size_t)n_tb * 48 * dec->D * sizeof(uint16_t);
+    *yb = (size_t)n_tb * 16 * dec->D * sizeof(uint16_t);
+    return *xb + *qb + *yb + (dec->dil[0] ? 2 * *yb : 0);
+}
+
+static int check_batch(const pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_types, int64_t n,
+                       const float* d_logits, const uint8_t* d_bits) {
     if (!dec) return fail(PWD_EINVAL, "null decoder");
     if (n < 0) return fail(PWD_EINVAL, "negative n_windows");
     if (n > dec->max_windows) return fail(PWD_EBATCH, "n_windows %lld > max_windows %d", (long long)n, dec->max_windows);
+    if (n > 0 && (!d_meas || !d_types || !d_logits || !d_bits)) return fail(PWD_EINVAL, "null buffer");
+    return PWD_OK;
+}
+
+// decode_windows with `readouts` readouts after the last `readouts` rounds (1: the inference
+// branch; distance: the recurrent branch), written to d_logits[win * readouts + k].
+static int decode_impl(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_types, int64_t n,
+                       float* d_logits, uint8_t* d_bits, void* hip_stream, int readouts, const Activations& act) {
+    const int rc0 = check_batch(dec, d_meas, d_types, n, d_logits, d_bits);
+    if (rc0 != PWD_OK) return rc0;
     if (n == 0) return PWD_OK;
-    if (!d_meas || !d_types || !d_logits || !d_bits) return fail(PWD_EINVAL, "null buffer");
     DeviceGuard dg(dec->device);
     HIP_OK(dg.err);
     hipStream_t s = static_cast<hipStream_t>(hip_stream);
@@ -687,9 +744,9 @@ static int decode_impl(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* 
     tp.kappa = dec->kappa;
     tp.eps = dec->eps;
     tp.qscale = (float)(1.4426950408889634 / std::sqrt((double)dec->dh));
-    tp.X = dec->X;
-    tp.QKV = dec->QKV;
-    tp.Y = dec->Y;
+    tp.X = act.X;
+    tp.QKV = act.QKV;
+    tp.Y = act.Y;
     tp.S0 = dec->S0;
     tp.ntok = dec->ntok;
     tp.tok_stab = dec->tok_stab;
@@ -707,15 +764,15 @@ static int decode_impl(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* 
         tp.bqkv = dec->layers[l].bqkv;
     };
     AttnParams ap;
-    ap.QKV = dec->QKV;
-    ap.Y = dec->Y;
+    ap.QKV = act.QKV;
+    ap.Y = act.Y;
     ap.N = dec->ntok;
     ap.Npad = dec->Npad;
     ap.nbw = dec->nbw;
     ap.H = dec->H;
 
     ReadoutParams rp;
-    rp.X = dec->X;
+    rp.X = act.X;
     rp.Xb = nullptr;
     rp.types = d_types;
     rp.err = dec->err;
@@ -745,7 +802,7 @@ static int decode_impl(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* 
     // flags, timed as `stage`.
     ConvParams cp;
     std::memset(&cp, 0, sizeof cp);
-    cp.X = dec->X;
+    cp.X = act.X;
     cp.d = dec->d;
     cp.ntok = dec->ntok;
     cp.nbw = dec->nbw;
@@ -753,11 +810,11 @@ static int decode_impl(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* 
     cp.zero = dec->zero;
     auto post = [&](int l, int flags, int stage) -> hipError_t {
         if (!dec->dil[0]) return timed(dec, stage, s, [&] { return launch_tok(dec->D, dec->F, TOK_POST | flags, tp, n_tb, s); });
-        tp.G = dec->G[0];
+        tp.G = act.G[0];
         hipError_t e = timed(dec, PWD_STAGE_OUT_PROJ, s, [&] { return launch_tok(dec->D, dec->F, TOK_WO, tp, n_tb, s); });
         for (int j = 0; j < 3 && e == hipSuccess; ++j) {
-            cp.Gin = dec->G[j & 1];
-            cp.Gout = dec->G[(j + 1) & 1];
+            cp.Gin = act.G[j & 1];
+            cp.Gout = act.G[(j + 1) & 1];
             cp.stream = dec->layers[l].conv[j];
             cp.bias = dec->layers[l].conv_b[j];
             cp.dil = dec->dil[j];
@@ -784,10 +841,10 @@ static int decode_impl(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* 
                 set_qkv(0);
                 // D_t for a readout goes to the Y buffer: each workgroup has read its own Y
                 // tiles by then, and the next writer of Y is the next round's attention
-                tp.state_out = read_t ? dec->Y : nullptr;
+                tp.state_out = read_t ? act.Y : nullptr;
                 HIP_OK(post(l, TOK_EMBED | TOK_QKV | RES, PWD_STAGE_POST_EMBED_QKV));
                 tp.state_out = nullptr;
-                if (read_t) HIP_OK(readout(t - (dec->W - readouts), dec->Y));
+                if (read_t) HIP_OK(readout(t - (dec->W - readouts), act.Y));
             } else {
                 HIP_OK(post(l, 0, PWD_STAGE_POST));
             }
@@ -799,12 +856,40 @@ static int decode_impl(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* 
 
 int decode_windows(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_types, int64_t n,
                    float* d_logits, uint8_t* d_bits, void* hip_stream) {
-    return decode_impl(dec, d_meas, d_types, n, d_logits, d_bits, hip_stream, 1);
+    if (!dec) return fail(PWD_EINVAL, "null decoder");
+    return decode_impl(dec, d_meas, d_types, n, d_logits, d_bits, hip_stream, 1, handle_activations(dec));
 }
 
 int decode_windows_recurrent(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_types, int64_t n,
                              float* d_logits, uint8_t* d_bits, void* hip_stream) {
-    return decode_impl(dec, d_meas, d_types, n, d_logits, d_bits, hip_stream, dec ? dec->d : 1);
+    if (!dec) return fail(PWD_EINVAL, "null decoder");
+    return decode_impl(dec, d_meas, d_types, n, d_logits, d_bits, hip_stream, dec->d, handle_activations(dec));
+}
+
+int decode_windows_noalloc(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_types, int64_t n,
+                           float* d_logits, uint8_t* d_bits, void* hip_stream) {
+    const int rc = check_batch(dec, d_meas, d_types, n, d_logits, d_bits);
+    if (rc != PWD_OK || n == 0) return rc;
+    Activations act{nullptr, nullptr, nullptr, {nullptr, nullptr}};
+    if (dec->dtype == PWD_DTYPE_BF16) {
+        // the same token-block rounding as the handle's buffers: every launch's grid fits
+        const int64_t gran = tok_block_granule();
+        const int64_t n_tb = (n * dec->nbw + gran - 1) / gran * gran;
+        size_t xb, qb, yb;
+        const size_t need = activation_bytes(dec, n_tb, &xb, &qb, &yb);
+        if (need > (size_t)PWD_NOALLOC_SCRATCH_BYTES)
+            return fail(PWD_EBATCH, "%lld windows need %zu bytes of scratch; decode_windows_noalloc has %zu",
+                        (long long)n, need, (size_t)PWD_NOALLOC_SCRATCH_BYTES);
+        unsigned char* base = static_cast<unsigned char*>(dec->static_scratch);
+        act.X = reinterpret_cast<float*>(base);
+        act.QKV = reinterpret_cast<uint16_t*>(base + xb);
+        act.Y = reinterpret_cast<uint16_t*>(base + xb + qb);
+        if (dec->dil[0]) {
+            act.G[0] = reinterpret_cast<uint16_t*>(base + xb + qb + yb);
+            act.G[1] = reinterpret_cast<uint16_t*>(base + xb + qb + 2 * yb);
+        }
+    }
+    return decode_impl(dec, d_meas, d_types, n, d_logits, d_bits, hip_stream, 1, act);
 }
 
 int decoder_detection_events(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* d_types,

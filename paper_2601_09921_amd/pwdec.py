@@ -72,6 +72,7 @@ def bind(lib: ctypes.CDLL) -> ctypes.CDLL:
         "decoder_create": (ctypes.c_int, [P(Geometry), P(ModelDims), ctypes.c_void_p, ctypes.c_size_t, P(VP)]),
         "decode_windows": (ctypes.c_int, [VP, VP, VP, I64, VP, VP, VP]),
         "decode_windows_recurrent": (ctypes.c_int, [VP, VP, VP, I64, VP, VP, VP]),
+        "decode_windows_noalloc": (ctypes.c_int, [VP, VP, VP, I64, VP, VP, VP]),
         "decoder_detection_events": (ctypes.c_int, [VP, VP, VP, I64, VP, VP]),
         "decode_stream": (ctypes.c_int, [VP, VP, I64, VP, VP, VP, VP, VP]),
         "decoder_sync_status": (ctypes.c_int, [VP, VP]),
@@ -223,6 +224,17 @@ class Decoder:
                                         ctypes.c_void_p(types.data_ptr()), n,
                                         ctypes.c_void_p(logits.data_ptr()), ctypes.c_void_p(bits.data_ptr()),
                                         _stream_ptr(stream)))
+
+    def decode_noalloc(self, meas, types, logits, bits, stream=None):
+        """As decode, on the library's fixed per-GPU scratch instead of the handle's (no
+        allocation; calls on one GPU must not overlap)."""
+        n = self._windows_in(meas, types)
+        require(logits, "logits", ("float32",), self.device, min_numel=n)
+        require(bits, "bits", ("uint8",), self.device, min_numel=n)
+        _check(self._lib.decode_windows_noalloc(self._h, ctypes.c_void_p(meas.data_ptr()),
+                                                ctypes.c_void_p(types.data_ptr()), n,
+                                                ctypes.c_void_p(logits.data_ptr()), ctypes.c_void_p(bits.data_ptr()),
+                                                _stream_ptr(stream)))
 
     def decode_recurrent(self, meas, types, logits, bits, stream=None):
         """As decode, with outputs float32 / uint8 [n][distance]: a readout after each of the
