@@ -264,8 +264,25 @@ enum {
     PWD_STAGE_OUT_PROJ = 9,       /* with dilated convolutions: out-projection + LayerNorm 1
                                      (stages 2-4 then time the feed-forward part) */
     PWD_STAGE_DILATED_CONV = 10,  /* one launch per residual unit of the dilated convolutions */
-    PWD_NUM_STAGES = 11
+    PWD_STAGE_RESIDENT = 11,      /* the state-resident schedule: every round and layer in one launch */
+    PWD_NUM_STAGES = 12
 };
+
+/* Launch schedules of decode_windows (the network and its results are the same; Algorithm 1
+ * carries the state D_n from round to round either way):
+ *   PWD_SCHEDULE_LAYERS: one launch per layer and round for attention and one for the token-local
+ *     stages, the state and activations of the whole batch in HBM between launches;
+ *   PWD_SCHEDULE_RESIDENT: one launch for every round and layer, each window owned by one
+ *     wavefront with its state, Q, K and V kept in registers throughout (bf16, d_model 128, at
+ *     most 64 tokens and 4 layers, heads of 16 or 32, feed-forward 4 d_model, no dilated
+ *     convolutions or embedder block), then the readout;
+ *   PWD_SCHEDULE_AUTO (the default): RESIDENT where the configuration allows it, else LAYERS.
+ * The recurrent branch (decode_windows_recurrent) always uses LAYERS. */
+enum { PWD_SCHEDULE_AUTO = 0, PWD_SCHEDULE_LAYERS = 1, PWD_SCHEDULE_RESIDENT = 2 };
+
+/* Selects the schedule of the handle's later decodes. PWD_EUNSUPPORTED if RESIDENT is asked for
+ * a configuration outside its range, PWD_EINVAL for an unknown value. Host only. */
+int decoder_schedule(pwd_decoder* dec, int schedule);
 
 typedef struct {
     double ms[PWD_NUM_STAGES];       /* summed kernel time per stage, milliseconds */

@@ -9,7 +9,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libpwdec.so")
-SOURCES = ["tok.hip", "attn.hip", "readout.hip", "f32_window.hip", "stream.hip", "pwdec.cpp"]
+SOURCES = ["tok.hip", "attn.hip", "resident.hip", "readout.hip", "f32_window.hip", "stream.hip", "pwdec.cpp"]
 # Per-source extra flags. The attention kernel keeps its MFMA accumulators in VGPRs (it needs
 # far fewer than 256), so no copies between accumulation and arithmetic registers; the token
 # kernel needs the AGPRs as accumulators.

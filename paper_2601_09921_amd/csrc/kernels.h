@@ -104,6 +104,26 @@ struct F32Params {
     float kappa, eps;
 };
 
+// The state-resident decoder (resident.hip): every round and layer of a batch of windows in
+// one launch, one wavefront per window, the state in registers. It writes the final state
+// D_W to X for the readout.
+struct ResidentParams {
+    SyndromeIn in;
+    int ntok;               // tokens per window
+    const int* tok_stab;    // [ntok] stabilizer of each token or -1; null: token s = stabilizer s
+    int nbw;                // 16-token blocks per window (1..4)
+    int L;                  // layers
+    float kappa, eps, qscale;
+    const uint16_t* stream; // weight fragments of every layer in consumption order (see resident.hip)
+    const float* vecs;      // [L][9 D + F]: b_q b_k b_v b_o g1 be1 b2 g2 be2 b1
+    const float* S0;        // b_e + PE, fp32 C fragments [nbw][D/16][64][4]
+    const float* we;        // [D]
+    float* X;               // out: the final state, fp32 C fragments [nwin * nbw][D/16][64][4]
+};
+bool resident_supported(int D, int nbw, int L, int mr, int dh);
+int resident_chunk_fragments();
+hipError_t launch_resident(int mr, int dh, const ResidentParams& p, hipStream_t s);
+
 hipError_t launch_events(const EventsParams& p, hipStream_t s);
 int64_t tok_block_granule();
 int tok_mlp_chunk(int D);

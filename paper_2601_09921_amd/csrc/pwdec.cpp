@@ -122,6 +122,37 @@ void append_qkv_stream(std::vector<uint16_t>& out, const float* Wqkv, int D) {
             }
 }
 
+// The resident kernel's stream of one layer (d_model D, feed-forward width F): per 32-feature
+// group og, the Q, K and V fragments of the group (part, k-step, row tile 2 og + hh), then the
+// out-projection's fragments at k-step og (row tile); per feed-forward chunk of 64 hidden units,
+// W1 (k-step, hidden row tile) and W2 (hidden k-step, output row tile).
+void append_resident_stream(std::vector<uint16_t>& out, const float* Wq, const float* Wk, const float* Wv,
+                            const float* Wo, const float* W1, const float* W2, int D, int F) {
+    const int RT = D / 16, KS = D / 32, FKS = F / 32, CH = 64;
+    std::vector<uint16_t> fq, fk, fv, fo, f1, f2;
+    append_frags(fq, Wq, D, D);
+    append_frags(fk, Wk, D, D);
+    append_frags(fv, Wv, D, D);
+    append_frags(fo, Wo, D, D);
+    append_frags(f1, W1, D, F);
+    append_frags(f2, W2, F, D);
+    auto frag = [&](const std::vector<uint16_t>& v, int ro, int ks, int nks) {
+        out.insert(out.end(), v.begin() + ((size_t)ro * nks + ks) * 512, v.begin() + ((size_t)ro * nks + ks + 1) * 512);
+    };
+    for (int og = 0; og < KS; ++og) {
+        for (const auto* f : {&fq, &fk, &fv})
+            for (int ks = 0; ks < KS; ++ks)
+                for (int hh = 0; hh < 2; ++hh) frag(*f, 2 * og + hh, ks, KS);
+        for (int rt = 0; rt < RT; ++rt) frag(fo, rt, og, KS);
+    }
+    for (int c = 0; c < F / CH; ++c) {
+        for (int ks = 0; ks < KS; ++ks)
+            for (int rh = 0; rh < CH / 16; ++rh) frag(f1, c * (CH / 16) + rh, ks, KS);
+        for (int kh = 0; kh < CH / 32; ++kh)
+            for (int rt = 0; rt < RT; ++rt) frag(f2, rt, c * (CH / 32) + kh, FKS);
+    }
+}
+
 size_t layer_floats(int D, int F) { return (size_t)4 * D * D + 2 * (size_t)D * F + F + 9 * (size_t)D; }
 
 bool has_conv(const pwd_model_dims* m) {
@@ -263,6 +294,12 @@ struct pwd_decoder {
     const int* emb_nb = nullptr;   // embedder residual block (PWD_EMBED_RESNET): see emb_tables
     const float* emb_tab = nullptr;
     const float* f32w = nullptr;   // fp32 path: the blob tensors as given
+    // the state-resident schedule (PWD_SCHEDULE_RESIDENT), when the configuration allows it
+    bool resident_ok = false;
+    int schedule = PWD_SCHEDULE_AUTO;
+    int mlp_ratio = 4;
+    const uint16_t* res_stream = nullptr;
+    const float* res_vecs = nullptr;
     float bo_out = 0.f, beta[3] = {0.f, 0.f, 0.f};
     // per-stage timing (decoder_profile)
     bool profiling = false;
@@ -478,6 +515,11 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
     struct LayerOff { size_t post, qkv, post_vecs, bqkv, conv[3], conv_b[3]; };
     std::vector<LayerOff> loff(L);
     size_t off_S0 = 0, off_we = 0, off_Wc = 0, off_bc = 0, off_wo = 0, off_f32 = 0, off_zero = 0;
+    size_t off_res_stream = 0, off_res_vecs = 0;
+    const bool resident_ok = dims->dtype == PWD_DTYPE_BF16 && !has_conv(dims) && dims->embedder == PWD_EMBED_LINEAR &&
+                             resident_supported(D, (dec->ntok + 15) / 16, L, dims->mlp_ratio, D / H);
+    dec->resident_ok = resident_ok;
+    dec->mlp_ratio = dims->mlp_ratio;
     const size_t lf = layer_floats(D, F);
     const float* tail = w.data() + 2 * D + (size_t)L * lf;   // Wc, bc, w_o, b_o, beta
     if (dims->dtype == PWD_DTYPE_BF16) {
@@ -534,6 +576,21 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
                 }
             }
         }
+        if (resident_ok) {
+            std::vector<uint16_t> rs;
+            std::vector<float> rv;
+            for (int l = 0; l < L; ++l) {
+                const float* p = w.data() + 2 * D + (size_t)l * lf;
+                const float *Wq = p, *bq = Wq + D * D, *Wk = bq + D, *bk = Wk + D * D, *Wv = bk + D, *bv = Wv + D * D;
+                const float *Wo = bv + D, *bo = Wo + D * D, *g1 = bo + D, *be1 = g1 + D, *W1 = be1 + D;
+                const float *b1 = W1 + (size_t)D * F, *W2 = b1 + F, *b2 = W2 + (size_t)F * D, *g2 = b2 + D, *be2 = g2 + D;
+                append_resident_stream(rs, Wq, Wk, Wv, Wo, W1, W2, D, F);
+                for (const float* v : {bq, bk, bv, bo, g1, be1, b2, g2, be2}) rv.insert(rv.end(), v, v + D);
+                rv.insert(rv.end(), b1, b1 + F);
+            }
+            off_res_stream = put(rs.data(), rs.size() * 2);
+            off_res_vecs = put(rv.data(), rv.size() * 4);
+        }
         {
             std::vector<uint16_t> fr;
             append_frags(fr, tail, 4 * D, D);   // Wc[2][2][D][D] read as [4D][D]
@@ -587,6 +644,10 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
         dec->bc = fptr(off_bc);
         if (has_conv(dims)) dec->zero = hptr(off_zero);
         dec->wo = fptr(off_wo);
+        if (resident_ok) {
+            dec->res_stream = hptr(off_res_stream);
+            dec->res_vecs = fptr(off_res_vecs);
+        }
         for (int l = 0; l < L; ++l) {
             pwd_decoder::Layer ly;
             ly.post = hptr(loff[l].post); ly.qkv = hptr(loff[l].qkv);
@@ -736,6 +797,51 @@ static int decode_impl(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* 
     }
 
     const int64_t n_tb = n * dec->nbw;
+    ReadoutParams rp;
+    rp.X = act.X;
+    rp.Xb = nullptr;
+    rp.types = d_types;
+    rp.err = dec->err;
+    rp.Wc = dec->Wc;
+    rp.bc = dec->bc;
+    rp.wo = dec->wo;
+    rp.bo = dec->bo_out;
+    for (int i = 0; i < 3; ++i) rp.beta[i] = dec->beta[i];
+    rp.cell_token = dec->cell_token;
+    rp.nwin = (int)n;
+    rp.d = dec->d;
+    rp.D = dec->D;
+    rp.nbw = dec->nbw;
+    rp.stride = readouts;
+    // readout of D_t into output slot k; `state` is null for the fp32 final state in X, else
+    // the bf16 copy of D_t
+    auto readout = [&](int k, const uint16_t* state) {
+        rp.Xb = state;
+        rp.logits = d_logits + k;
+        rp.bits = d_bits + k;
+        return timed(dec, PWD_STAGE_READOUT, s, [&] { return launch_readout(rp, s); });
+    };
+
+    if (readouts == 1 && dec->resident_ok && dec->schedule != PWD_SCHEDULE_LAYERS) {
+        ResidentParams rs;
+        rs.in = in;
+        rs.ntok = dec->ntok;
+        rs.tok_stab = dec->tok_stab;
+        rs.nbw = dec->nbw;
+        rs.L = dec->L;
+        rs.kappa = dec->kappa;
+        rs.eps = dec->eps;
+        rs.qscale = (float)(1.4426950408889634 / std::sqrt((double)dec->dh));
+        rs.stream = dec->res_stream;
+        rs.vecs = dec->res_vecs;
+        rs.S0 = dec->S0;
+        rs.we = dec->we;
+        rs.X = act.X;
+        HIP_OK(timed(dec, PWD_STAGE_RESIDENT, s, [&] { return launch_resident(dec->mlp_ratio, dec->dh, rs, s); }));
+        HIP_OK(readout(0, nullptr));
+        return PWD_OK;
+    }
+
     TokParams tp;
     std::memset(&tp, 0, sizeof tp);
     tp.in = in;
@@ -770,31 +876,6 @@ static int decode_impl(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* 
     ap.Npad = dec->Npad;
     ap.nbw = dec->nbw;
     ap.H = dec->H;
-
-    ReadoutParams rp;
-    rp.X = act.X;
-    rp.Xb = nullptr;
-    rp.types = d_types;
-    rp.err = dec->err;
-    rp.Wc = dec->Wc;
-    rp.bc = dec->bc;
-    rp.wo = dec->wo;
-    rp.bo = dec->bo_out;
-    for (int i = 0; i < 3; ++i) rp.beta[i] = dec->beta[i];
-    rp.cell_token = dec->cell_token;
-    rp.nwin = (int)n;
-    rp.d = dec->d;
-    rp.D = dec->D;
-    rp.nbw = dec->nbw;
-    rp.stride = readouts;
-    // readout of D_t into output slot k; `state` is null for the fp32 final state in X, else
-    // the bf16 copy of D_t
-    auto readout = [&](int k, const uint16_t* state) {
-        rp.Xb = state;
-        rp.logits = d_logits + k;
-        rp.bits = d_bits + k;
-        return timed(dec, PWD_STAGE_READOUT, s, [&] { return launch_readout(rp, s); });
-    };
 
     // POST of layer l followed by `flags` (QKV, EMBED, RESNET). With the dilated convolutions:
     // out-projection + LN1 (writing the first unit's input G), the three residual units
@@ -943,6 +1024,17 @@ int decode_stream(pwd_decoder* dec, const uint32_t* d_stream, int64_t T, float* 
     cp.bit = d_bit;
     cp.prob = d_prob;
     HIP_OK(timed(dec, PWD_STAGE_STREAM_COMBINE, s, [&] { return launch_stream_combine(cp, s); }));
+    return PWD_OK;
+}
+
+int decoder_schedule(pwd_decoder* dec, int schedule) {
+    if (!dec) return fail(PWD_EINVAL, "null decoder");
+    if (schedule != PWD_SCHEDULE_AUTO && schedule != PWD_SCHEDULE_LAYERS && schedule != PWD_SCHEDULE_RESIDENT)
+        return fail(PWD_EINVAL, "schedule %d: need 0 (auto), 1 (layers) or 2 (resident)", schedule);
+    if (schedule == PWD_SCHEDULE_RESIDENT && !dec->resident_ok)
+        return fail(PWD_EUNSUPPORTED, "the resident schedule needs bf16, d_model 128, at most 64 tokens and 4 layers, "
+                                      "heads of 16 or 32, feed-forward 4 d_model, no dilated convolutions or embedder block");
+    dec->schedule = schedule;
     return PWD_OK;
 }
 

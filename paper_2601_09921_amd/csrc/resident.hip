@@ -1,0 +1,436 @@
+// The recurrent decoder with each window's state resident on chip for all rounds and layers
+// (Algorithm 1: the state D_n is carried from round to round, D_0 = 0; App. A.2 fold and
+// Syndrome Transformer layers), bf16 MFMA with fp32 state, accumulation, softmax and LayerNorm.
+//
+// One wavefront owns one whole window of up to four 16-token blocks (the 48 stabilizers of
+// d = 7 are three). Its fp32 state stays in registers through every round and layer, and so
+// do the window's Q, K and V: the projections are computed transposed with tokens along MFMA
+// columns, so after a bf16 pack their accumulators are exactly the operands attention takes --
+// K as the A operand of S^T = K Q'^T, Q' = Q log2(e)/sqrt(dh) as its B operand, and V,
+// computed with the activations as the A operand (tokens as rows), as the A operand of
+// O^T = V^T P^T; the output O^T packs into the B operand of the out-projection. Attention is
+// local to the wavefront, with the exact row maximum (all 48 scores of a query are in
+// registers). Only the weights and the final state move through memory: one launch decodes
+// every round and layer, and the readout follows on the state it writes.
+//
+// Four wavefronts (four windows) share one weight stream. The host lays each layer's weights
+// out in the order the kernel consumes them, and the workgroup pulls the stream through a
+// double-buffered LDS ring in chunks of 32 one-kilobyte fragments with direct global->LDS
+// loads, spread between the current chunk's fragment reads. Per layer: for each 32-feature
+// group og of Q/K/V (one chunk at d_model 128), the Q, K and V fragments of the group, the
+// attention of the group's heads, and the out-projection's k-step og, whose input is exactly
+// that group's attention output (the projections read a bf16 copy of the layer input, so the
+// out-projection accumulates into the state in place); then LayerNorm 1, the feed-forward in
+// chunks of 64 hidden units, and LayerNorm 2. A round is L (KS + F/64) chunks and the stream
+// wraps from the last layer to the first, so the prefetch runs on across layers and rounds.
+// Every fragment read from LDS feeds one MFMA per token block of the wavefront (TB of them).
+#include "common.h"
+#include "kernels.h"
+#include "pipeline.h"
+
+namespace {
+
+constexpr int FRAG = 512;          // bf16 values per fragment (1 KB)
+constexpr int RWAVES = 4;          // wavefronts, i.e. windows, per workgroup
+constexpr int RCHUNK = 32;         // fragments per ring buffer
+constexpr int RD = 128;            // d_model of the resident path
+constexpr int RRT = RD / 16;       // 16-row C tiles of a d_model vector
+constexpr int RKS = RD / 32;       // 32-deep k-steps of a d_model vector
+constexpr int RLA = 4;             // fragment reads in flight ahead of their MFMAs
+constexpr int RMAXL = 4;           // layers whose vectors fit the LDS table
+
+template <int MR>
+struct RShape {
+    static constexpr int F = MR * RD;
+    static constexpr int CH = 64;                          // hidden units per feed-forward chunk
+    static constexpr int NMLP = F / CH;
+    static constexpr int QKV_FRAGS = 3 * 2 * RKS;          // Q, K, V of one 32-feature group
+    static constexpr int W1_FRAGS = (CH / 16) * RKS, W2_FRAGS = RRT * (CH / 32);
+    static constexpr int LAYER_CHUNKS = RKS + NMLP;
+    static_assert(QKV_FRAGS + RRT == RCHUNK, "a Q/K/V group and its out-projection k-step fill one chunk");
+    static_assert(W1_FRAGS + W2_FRAGS == RCHUNK, "a feed-forward chunk fills one ring buffer");
+    static_assert(RKS % 2 == 0 && LAYER_CHUNKS % 2 == 0, "ring parity repeats every layer");
+};
+
+// Per-layer vectors, in the order the host writes them: [b_q b_k b_v | b_o g1 be1 b2 g2 be2 | b1].
+template <int MR>
+struct RVec {
+    static constexpr int BQ = 0, BK = RD, BV = 2 * RD, BO = 3 * RD, G1 = 4 * RD, BE1 = 5 * RD, B2 = 6 * RD,
+                         G2 = 7 * RD, BE2 = 8 * RD, B1 = 9 * RD;
+    static constexpr int PER_LAYER = 9 * RD + MR * RD;
+};
+
+// The two ring buffers, separate objects so the compiler can tell they never alias.
+template <int PAR>
+PWD_DEV uint16_t* rbuf() {
+    __shared__ __align__(16) uint16_t buf[RCHUNK * FRAG];
+    return buf;
+}
+
+// The weight stream of a round: chunk i of L * LAYER_CHUNKS at stream + i * RCHUNK fragments.
+// While chunk i is in use, each wavefront loads its RCHUNK / RWAVES fragments of chunk i + 1
+// (wrapping to the first chunk after the last) into the other buffer, one load after each of
+// read RLA, RLA + 2, ... of the chunk's fragment reads.
+struct Ring {
+    const uint16_t* stream;
+    int nchunks, wave, lane;
+    static constexpr int PER_WAVE = RCHUNK / RWAVES;
+
+    __device__ const uint16_t* next(int i) const {
+        return stream + (size_t)(i + 1 < nchunks ? i + 1 : 0) * RCHUNK * FRAG;
+    }
+    template <int PAR>
+    __device__ void part(const uint16_t* src, int j) const {
+        const int f = wave * PER_WAVE + j;
+        lds_load_1k(uniform_ptr(src + f * FRAG), lds_addr(rbuf<PAR>() + f * FRAG), lane);
+    }
+    // after fragment read r of the chunk whose successor is `src`, going to buffer PAR
+    template <int PAR>
+    __device__ void after_read(const uint16_t* src, int r) const {
+        if (r >= RLA && (r - RLA) % 2 == 0 && (r - RLA) / 2 < PER_WAVE) part<PAR>(src, (r - RLA) / 2);
+    }
+    // Chunk in buffer PAR becomes visible to every wavefront: this wavefront's loads of it have
+    // landed (no other vector memory operation is outstanding at a chunk boundary that must
+    // not be waited for), then the barrier also frees the other buffer for the next chunk.
+    template <int PAR>
+    __device__ const uint16_t* sync() const {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        return rbuf<PAR>();
+    }
+};
+static_assert(RLA + 2 * (Ring::PER_WAVE - 1) < 3 * 2 * RKS, "the next chunk's loads go out during the Q/K/V reads");
+
+PWD_DEV bf16x4 to_b4(f32x4 v) {
+    bf16x4 r;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) r[i] = (__bf16)v[i];
+    return r;
+}
+PWD_DEV bf16x4 half_b8(bf16x8 v, int h) {   // elements 4h .. 4h+3
+    return bf16x4{v[4 * h], v[4 * h + 1], v[4 * h + 2], v[4 * h + 3]};
+}
+
+// Softmax over the window's keys for one query block: scores s[kb] (keys 4g+i of key block kb
+// as rows, this lane's query as the column), padding keys (index >= ntok) excluded, exact row
+// maximum; returns the probabilities in place (rounded to bf16 as the P^T operand) and 1/sum.
+template <int TB>
+PWD_DEV float softmax_cols(f32x4 (&s)[TB], bf16x4 (&pb)[TB], int ntok, int g) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < TB; ++kb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            if (kb * 16 + 4 * g + i >= ntok) s[kb][i] = -INFINITY;
+            mx = fmaxf(mx, s[kb][i]);
+        }
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    float sum = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < TB; ++kb) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) s[kb][i] = __builtin_amdgcn_exp2f(s[kb][i] - mx);
+        pb[kb] = to_b4(s[kb]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) sum += (float)pb[kb][i];   // the same bf16 values as P^T
+    }
+    sum += __shfl_xor(sum, 16);
+    sum += __shfl_xor(sum, 32);
+    return 1.0f / sum;
+}
+
+template <int TB, int MR, int DH>
+__global__ __launch_bounds__(RWAVES * 64, 1) void resident_kernel(ResidentParams p) {
+    using S = RShape<MR>;
+    using V = RVec<MR>;
+    static_assert(DH == 16 || DH == 32, "heads of 16 or 32");
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int g = lane >> 4, col = lane & 15;
+    // a wavefront past the batch decodes the last window again (the weight ring needs every
+    // wavefront at every barrier) and stores nothing
+    const int win_raw = (int)blockIdx.x * RWAVES + wave;
+    const bool live = win_raw < p.in.nwin;
+    const int win = live ? win_raw : p.in.nwin - 1;
+
+    Ring ring;
+    ring.stream = p.stream;
+    ring.nchunks = p.L * S::LAYER_CHUNKS;
+    ring.wave = __builtin_amdgcn_readfirstlane(wave);
+    ring.lane = lane;
+    ring.template part<0>(p.stream, 0);   // chunk 0 into buffer 0 ...
+#pragma unroll
+    for (int j = 1; j < Ring::PER_WAVE; ++j) ring.template part<0>(p.stream, j);
+
+    // ... while the per-layer vectors, b_e + PE of the window's blocks and w_e go to LDS
+    __shared__ __align__(16) float vec[RMAXL * V::PER_LAYER];
+    __shared__ __align__(16) float s0[TB * RRT * 256];
+    __shared__ __align__(16) float we[RD];
+    for (int i = threadIdx.x; i < p.L * V::PER_LAYER; i += RWAVES * 64) vec[i] = p.vecs[i];
+    for (int i = threadIdx.x; i < TB * RRT * 256; i += RWAVES * 64) s0[i] = p.S0[i];
+    for (int i = threadIdx.x; i < RD; i += RWAVES * 64) we[i] = p.we[i];
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // chunk 0 and the tables are in LDS ...
+    __syncthreads();                                    // ... and visible to every wavefront
+
+    const uint32_t* meas = p.in.meas + (int64_t)win * (p.in.W + 1) * p.in.words;
+    const int type = p.in.types[win];
+    int stab[TB];   // this lane's token's stabilizer in each block, or -1
+#pragma unroll
+    for (int b = 0; b < TB; ++b) {
+        const int s = b * 16 + col;
+        stab[b] = s < p.ntok ? (p.tok_stab ? p.tok_stab[s] : s) : -1;
+    }
+
+    f32x4 x[RRT][TB];
+#pragma unroll
+    for (int rt = 0; rt < RRT; ++rt)
+#pragma unroll
+        for (int b = 0; b < TB; ++b) x[rt][b] = f32x4{0.f, 0.f, 0.f, 0.f};   // D_0 = 0
+
+    for (int t = 0; t < p.in.W; ++t) {
+        // ---- embedding of round t folded into the state: X = kappa (E_t w_e + b_e + PE + X)
+        float ev[TB];
+#pragma unroll
+        for (int b = 0; b < TB; ++b) {
+            ev[b] = 0.f;
+            if (stab[b] >= 0) {
+                const uint32_t w = event_word(meas, p.in.words, t, stab[b] >> 5, type, p.in.b_left, p.in.d);
+                ev[b] = (float)((w >> (stab[b] & 31)) & 1u);
+            }
+        }
+#pragma unroll
+        for (int b = 0; b < TB; ++b) {
+            const bool real = b * 16 + col < p.ntok;
+#pragma unroll
+            for (int rt = 0; rt < RRT; ++rt) {
+                const f32x4 sv = ld4(s0 + ((b * RRT + rt) * 64 + lane) * 4);
+                const f32x4 wv = ld4(we + rt * 16 + 4 * g);
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    x[rt][b][i] = p.kappa * ((real ? ev[b] * wv[i] + sv[i] : 0.f) + x[rt][b][i]);
+            }
+        }
+
+        for (int l = 0; l < p.L; ++l) {
+            const float* vl = vec + l * V::PER_LAYER;
+            const int cbase = l * S::LAYER_CHUNKS;
+            bf16x8 xb[RKS][TB];   // the layer input as B fragments (the projections' operand)
+#pragma unroll
+            for (int ks = 0; ks < RKS; ++ks)
+#pragma unroll
+                for (int b = 0; b < TB; ++b) xb[ks][b] = pack_b(x[2 * ks][b], x[2 * ks + 1][b]);
+
+            // ---- per 32-feature group: Q, K, V, attention of its heads, out-projection k-step.
+            // Groups run in pairs (ring buffers 0 and 1) in a loop rather than fully unrolled,
+            // which keeps the code, and its compile time, small.
+            auto og_group = [&](auto parc, int og) {
+                constexpr int PAR = decltype(parc)::value;
+                const uint16_t* buf = ring.template sync<PAR>();
+                const uint16_t* nx = ring.next(cbase + og);
+                f32x4 q[2][TB], k[2][TB], v[2][TB];
+#pragma unroll
+                for (int hh = 0; hh < 2; ++hh) {
+                    const int f0 = og * 32 + hh * 16;
+                    const f32x4 bq = ld4(vl + V::BQ + f0 + 4 * g), bk = ld4(vl + V::BK + f0 + 4 * g);
+                    const float bvv = vl[V::BV + f0 + col];   // V tiles: features along columns
+#pragma unroll
+                    for (int b = 0; b < TB; ++b) {
+                        q[hh][b] = bq;
+                        k[hh][b] = bk;
+                        v[hh][b] = f32x4{bvv, bvv, bvv, bvv};
+                    }
+                }
+                // fragment r: part r / (2 KS) (Q, K, V), k-step (r / 2) % KS, row tile r % 2
+                pipelined<S::QKV_FRAGS, RLA>(
+                    [&](int r) { return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(buf + r * FRAG + lane * 8)); },
+                    [&](int r, const bf16x8& a) {
+                        const int part = r / (2 * RKS), ks = (r / 2) % RKS, hh = r % 2;
+#pragma unroll
+                        for (int b = 0; b < TB; ++b) {
+                            if (part == 0) q[hh][b] = mfma16x16x32(a, xb[ks][b], q[hh][b]);
+                            else if (part == 1) k[hh][b] = mfma16x16x32(a, xb[ks][b], k[hh][b]);
+                            else v[hh][b] = mfma16x16x32(xb[ks][b], a, v[hh][b]);
+                        }
+                    },
+                    [&](int r) { ring.template after_read<1 - PAR>(nx, r); });
+                sched_pipeline<S::QKV_FRAGS, TB, RLA>();
+
+                // attention of the group's heads: y[qb] = O^T of query block qb as a B fragment
+                bf16x8 y[TB];
+                bf16x4 vt[2][TB];   // V^T A operands per 16-feature tile and key block
+#pragma unroll
+                for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+                    for (int b = 0; b < TB; ++b) vt[hh][b] = to_b4(v[hh][b]);
+                bf16x8 qf[TB], kf[TB];
+#pragma unroll
+                for (int b = 0; b < TB; ++b) {
+                    qf[b] = pack_b(q[0][b] * p.qscale, q[1][b] * p.qscale);
+                    kf[b] = pack_b(k[0][b], k[1][b]);
+                }
+#pragma unroll
+                for (int qb = 0; qb < TB; ++qb) {
+                    f32x4 o[2];
+                    if constexpr (DH == 16) {   // two heads per group: features 16 hh .. 16 hh + 15
+#pragma unroll
+                        for (int hh = 0; hh < 2; ++hh) {
+                            f32x4 s[TB];
+                            bf16x4 pb[TB];
+#pragma unroll
+                            for (int kb = 0; kb < TB; ++kb)
+                                s[kb] = mfma16x16x16(half_b8(kf[kb], hh), half_b8(qf[qb], hh), f32x4{0.f, 0.f, 0.f, 0.f});
+                            const float inv = softmax_cols<TB>(s, pb, p.ntok, g);
+                            o[hh] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                            for (int kb = 0; kb < TB; ++kb) o[hh] = mfma16x16x16(vt[hh][kb], pb[kb], o[hh]);
+                            o[hh] *= inv;
+                        }
+                    } else {   // one head of 32 features
+                        f32x4 s[TB];
+                        bf16x4 pb[TB];
+#pragma unroll
+                        for (int kb = 0; kb < TB; ++kb) s[kb] = mfma16x16x32(kf[kb], qf[qb], f32x4{0.f, 0.f, 0.f, 0.f});
+                        const float inv = softmax_cols<TB>(s, pb, p.ntok, g);
+#pragma unroll
+                        for (int hh = 0; hh < 2; ++hh) {
+                            o[hh] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                            for (int kb = 0; kb < TB; ++kb) o[hh] = mfma16x16x16(vt[hh][kb], pb[kb], o[hh]);
+                            o[hh] *= inv;
+                        }
+                    }
+                    y[qb] = pack_b(o[0], o[1]);
+                }
+
+                // out-projection k-step og: X += Wo[:, og]^T y (the residual is the state itself)
+                pipelined<RRT, RLA>(
+                    [&](int r) { return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(buf + (S::QKV_FRAGS + r) * FRAG + lane * 8)); },
+                    [&](int r, const bf16x8& a) {
+#pragma unroll
+                        for (int b = 0; b < TB; ++b) x[r][b] = mfma16x16x32(a, y[b], x[r][b]);
+                    },
+                    [](int) {});
+                sched_pipeline<RRT, TB, RLA>();
+            };
+            for (int og = 0; og < RKS; og += 2) {
+                og_group(std::integral_constant<int, 0>{}, og);
+                og_group(std::integral_constant<int, 1>{}, og + 1);
+            }
+#pragma unroll
+            for (int rt = 0; rt < RRT; ++rt) {
+                const f32x4 bo = ld4(vl + V::BO + rt * 16 + 4 * g);
+#pragma unroll
+                for (int b = 0; b < TB; ++b) x[rt][b] += bo;
+            }
+            layer_norm<RRT, TB>(x, vl + V::G1, vl + V::BE1, p.eps, g);
+
+            // ---- feed-forward in chunks of 64 hidden units; accumulators start at X + b_2
+#pragma unroll
+            for (int ks = 0; ks < RKS; ++ks)
+#pragma unroll
+                for (int b = 0; b < TB; ++b) xb[ks][b] = pack_b(x[2 * ks][b], x[2 * ks + 1][b]);
+#pragma unroll
+            for (int rt = 0; rt < RRT; ++rt) {
+                const f32x4 b2 = ld4(vl + V::B2 + rt * 16 + 4 * g);
+#pragma unroll
+                for (int b = 0; b < TB; ++b) x[rt][b] += b2;
+            }
+            constexpr int NRH = S::CH / 16, NKH = S::CH / 32;
+            auto mlp_chunk = [&](auto parc, int c) {
+                constexpr int PAR = decltype(parc)::value;   // = (KS + c) & 1, KS even
+                const uint16_t* buf = ring.template sync<PAR>();
+                const uint16_t* nx = ring.next(cbase + RKS + c);
+                f32x4 h[NRH][TB];
+#pragma unroll
+                for (int rh = 0; rh < NRH; ++rh) {
+                    const f32x4 b1 = ld4(vl + V::B1 + c * S::CH + rh * 16 + 4 * g);
+#pragma unroll
+                    for (int b = 0; b < TB; ++b) h[rh][b] = b1;
+                }
+                bf16x8 hb[NKH][TB];
+                // W1 fragment r: k-step r / NRH, hidden row tile r % NRH; then W2 fragment
+                // r - W1_FRAGS: hidden k-step (r - W1) / RT, output row tile (r - W1) % RT
+                pipelined<RCHUNK, RLA>(
+                    [&](int r) { return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(buf + r * FRAG + lane * 8)); },
+                    [&](int r, const bf16x8& a) {
+                        if (r < S::W1_FRAGS) {
+                            const int ks = r / NRH, rh = r % NRH;
+#pragma unroll
+                            for (int b = 0; b < TB; ++b) h[rh][b] = mfma16x16x32(a, xb[ks][b], h[rh][b]);
+                            if (r == S::W1_FRAGS - 1) {
+#pragma unroll
+                                for (int kh = 0; kh < NKH; ++kh)
+#pragma unroll
+                                    for (int b = 0; b < TB; ++b) {
+                                        f32x4 lo = h[2 * kh][b], hi = h[2 * kh + 1][b];
+#pragma unroll
+                                        for (int i = 0; i < 4; ++i) {
+                                            lo[i] = fmaxf(lo[i], 0.f);
+                                            hi[i] = fmaxf(hi[i], 0.f);
+                                        }
+                                        hb[kh][b] = pack_b(lo, hi);
+                                    }
+                            }
+                        } else {
+                            const int kh = (r - S::W1_FRAGS) / RRT, rt = (r - S::W1_FRAGS) % RRT;
+#pragma unroll
+                            for (int b = 0; b < TB; ++b) x[rt][b] = mfma16x16x32(a, hb[kh][b], x[rt][b]);
+                        }
+                    },
+                    [&](int r) { ring.template after_read<1 - PAR>(nx, r); });
+                sched_pipeline<RCHUNK, TB, RLA>();
+            };
+            static_assert(S::NMLP % 2 == 0, "feed-forward chunks in pairs");
+            for (int c = 0; c < S::NMLP; c += 2) {
+                mlp_chunk(std::integral_constant<int, 0>{}, c);
+                mlp_chunk(std::integral_constant<int, 1>{}, c + 1);
+            }
+            layer_norm<RRT, TB>(x, vl + V::G2, vl + V::BE2, p.eps, g);
+        }
+    }
+
+    // the final state D_W for the readout
+    if (live) {
+#pragma unroll
+        for (int b = 0; b < TB; ++b)
+#pragma unroll
+            for (int rt = 0; rt < RRT; ++rt)
+                *reinterpret_cast<f32x4*>(p.X + ((((int64_t)win * p.nbw + b) * RRT + rt) * 64 + lane) * 4) = x[rt][b];
+    }
+    // the last chunk's prefetch (the first chunk again) lands before the LDS is freed
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
+template <int TB, int MR>
+hipError_t launch_tb_mr(int dh, const ResidentParams& p, hipStream_t s) {
+    const dim3 grid((unsigned)((p.in.nwin + RWAVES - 1) / RWAVES)), block(RWAVES * 64);
+    if (dh == 16) resident_kernel<TB, MR, 16><<<grid, block, 0, s>>>(p);
+    else if (dh == 32) resident_kernel<TB, MR, 32><<<grid, block, 0, s>>>(p);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+template <int TB>
+hipError_t launch_tb(int mr, int dh, const ResidentParams& p, hipStream_t s) {
+    if (mr == 4) return launch_tb_mr<TB, 4>(dh, p, s);
+    return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+bool resident_supported(int D, int nbw, int L, int mr, int dh) {
+    return D == RD && nbw >= 1 && nbw <= 4 && L >= 1 && L <= RMAXL && mr == 4 && (dh == 16 || dh == 32);
+}
+
+int resident_chunk_fragments() { return RCHUNK; }
+
+hipError_t launch_resident(int mr, int dh, const ResidentParams& p, hipStream_t s) {
+    if (p.in.nwin <= 0) return hipSuccess;
+    switch (p.nbw) {
+        case 1: return launch_tb<1>(mr, dh, p, s);
+        case 2: return launch_tb<2>(mr, dh, p, s);
+        case 3: return launch_tb<3>(mr, dh, p, s);
+        case 4: return launch_tb<4>(mr, dh, p, s);
+        default: return hipErrorInvalidValue;
+    }
+}

@@ -30,6 +30,7 @@
 // wavefront owns). Activations (X, Y, Q/K/V) are streamed with non-temporal accesses.
 #include "common.h"
 #include "kernels.h"
+#include "pipeline.h"
 
 #include <type_traits>
 #include <utility>
@@ -94,7 +95,6 @@ PWD_DEV void stfrag(uint16_t* __restrict__ base, int64_t frag, int lane, bf16x8 
     st_stream(reinterpret_cast<u16x8*>(base + (frag * 64 + lane) * 8), __builtin_bit_cast(u16x8, v));
 }
 
-PWD_DEV f32x4 ld4(const float* __restrict__ p) { return *reinterpret_cast<const f32x4*>(p); }
 
 PWD_DEV u16x4 to_bf16x4(f32x4 v) {
     u16x4 r;
@@ -125,43 +125,6 @@ PWD_DEV f32x4 relu4(f32x4 v) {
 #ifndef TOK_DMA_SP
 #define TOK_DMA_SP 2
 #endif
-
-// The fragment reads of one chunk, software-pipelined in program order: LA reads are in
-// flight ahead of the MFMAs; read r + LA is issued right after the MFMAs that consume read
-// r. read(r) loads fragment r of the chunk, use(r, a) issues the MFMAs of fragment r, and
-// after(r) runs right after read r is issued. Every loop is fully unrolled, so the ring
-// indices are compile-time constants and the ring lives in registers.
-template <int NREAD, int LA, typename Read, typename Use, typename After>
-PWD_DEV void pipelined(const Read& read, const Use& use, const After& after) {
-    static_assert(LA >= 1 && LA <= NREAD, "look-ahead");
-    bf16x8 ring[LA];
-#pragma unroll
-    for (int r = 0; r < LA; ++r) {
-        ring[r] = read(r);
-        after(r);
-    }
-#pragma unroll
-    for (int r = 0; r < NREAD; ++r) {
-        use(r, ring[r % LA]);
-        if (r + LA < NREAD) {
-            ring[r % LA] = read(r + LA);
-            after(r + LA);
-        }
-    }
-}
-
-// Keeps the scheduler on the program order above: LA reads, then (MPR MFMAs, one read)
-// pairs, then the MFMAs of the last LA fragments.
-template <int NREAD, int MPR, int LA>
-PWD_DEV void sched_pipeline() {
-    __builtin_amdgcn_sched_group_barrier(0x100, LA, 0);
-#pragma unroll
-    for (int k = 0; k < NREAD - LA; ++k) {
-        __builtin_amdgcn_sched_group_barrier(0x008, MPR, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, MPR * LA, 0);
-}
 
 // The two LDS buffers of the weight stream. They are separate objects so the compiler can
 // tell that the direct-to-LDS prefetch into one never aliases reads of the other.
@@ -235,40 +198,6 @@ struct WeightPipe {
     }
 };
 
-// LayerNorm over the D features of each token (biased variance, two passes); gamma and
-// beta are in LDS.
-template <int RT, int TB>
-PWD_DEV void layer_norm(f32x4 (&x)[RT][TB], const float* gamma, const float* beta, float eps, int g) {
-    constexpr float inv_d = 1.0f / (RT * 16);
-#pragma unroll
-    for (int b = 0; b < TB; ++b) {
-        float s = 0.f;
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt) s += (x[rt][b][0] + x[rt][b][1]) + (x[rt][b][2] + x[rt][b][3]);
-        s += __shfl_xor(s, 16);
-        s += __shfl_xor(s, 32);
-        const float mean = s * inv_d;
-        float v = 0.f;
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float c = x[rt][b][i] - mean;
-                v += c * c;
-            }
-        v += __shfl_xor(v, 16);
-        v += __shfl_xor(v, 32);
-        const float rstd = rsqrtf(v * inv_d + eps);
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt) {
-            const f32x4 gm = ld4(gamma + rt * 16 + 4 * g);
-            const f32x4 bt = ld4(beta + rt * 16 + 4 * g);
-#pragma unroll
-            for (int i = 0; i < 4; ++i) x[rt][b][i] = (x[rt][b][i] - mean) * rstd * gm[i] + bt[i];
-        }
-    }
-}
-
 // LDS of one workgroup (two per CU): the weight ring (two 32-fragment buffers) + vectors.
 constexpr int LDS_BUDGET = 80 * 1024, RING_BYTES = 2 * 32 * FRAG * 2;
 
@@ -297,14 +226,6 @@ constexpr int qkv_stores_after_last_load() {
         if ((o2 + 1) * 2 * KS - 1 + LA - 1 >= LAST) n += STORES_PER_GROUP;
     return n;
 }
-
-template <typename F, int... I>
-PWD_DEV void static_for_impl(const F& f, std::integer_sequence<int, I...>) {
-    (f(std::integral_constant<int, I>{}), ...);
-}
-// f(integral_constant<int, i>) for i = 0 .. N-1, unrolled at compile time
-template <int N, typename F>
-PWD_DEV void static_for(const F& f) { static_for_impl(f, std::make_integer_sequence<int, N>{}); }
 
 template <int D, int MR, int FLAGS>
 __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(TokParams p) {

@@ -40,9 +40,10 @@ class ModelDims(ctypes.Structure):
                 ("embedder", ctypes.c_int32), ("conv_dilation", ctypes.c_int32 * 3)]
 
 
-NUM_STAGES = 11
+NUM_STAGES = 12
 STAGE_NAMES = ["embed_qkv", "attention", "post_qkv", "post_embed_qkv", "post", "readout", "fp32_window",
-               "stream_split", "stream_combine", "out_proj", "dilated_conv"]
+               "stream_split", "stream_combine", "out_proj", "dilated_conv", "resident"]
+SCHEDULE_AUTO, SCHEDULE_LAYERS, SCHEDULE_RESIDENT = 0, 1, 2
 
 
 class StageTimes(ctypes.Structure):
@@ -79,6 +80,7 @@ def bind(lib: ctypes.CDLL) -> ctypes.CDLL:
         "decoder_last_error": (ctypes.c_char_p, []),
         "decoder_destroy": (ctypes.c_int, [VP]),
         "decoder_profile": (ctypes.c_int, [VP, ctypes.c_int]),
+        "decoder_schedule": (ctypes.c_int, [VP, ctypes.c_int]),
         "decoder_profile_read": (ctypes.c_int, [VP, P(StageTimes)]),
     }
     for name, (res, args) in sig.items():
@@ -276,6 +278,10 @@ class Decoder:
 
     def sync_status(self, stream=None) -> int:
         return self._lib.decoder_sync_status(self._h, _stream_ptr(stream))
+
+    def schedule(self, which: int):
+        """SCHEDULE_AUTO, SCHEDULE_LAYERS or SCHEDULE_RESIDENT for the following decodes."""
+        _check(self._lib.decoder_schedule(self._h, which))
 
     def profile(self, enable: bool):
         """Per-stage kernel timing with HIP events on the decode stream (on/off)."""
