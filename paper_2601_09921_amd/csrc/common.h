@@ -78,14 +78,48 @@ PWD_DEV bf16x8 pack_b(f32x4 lo, f32x4 hi) {
     return r;
 }
 
-// Detection-event bit of stabilizer s at window round t (Sec. 2.2: a detector is the parity
-// of two consecutive measurements of one stabilizer; App. A.1.1: zero padding replaces the
-// missing buffer of the initial and final windows; the initial window's first core round
-// is compared with the all-zero state). meas points at the window's rows [W+1][words].
-PWD_DEV uint32_t event_word(const uint32_t* __restrict__ meas, int words, int t, int w,
-                            int type, int b_left, int d) {
-    uint32_t cur = meas[(t + 1) * words + w];
-    uint32_t prev = meas[t * words + w];
+// Reductions across the four 16-lane groups of a wavefront (lanes l, l^16, l^32, l^48 -- the
+// four row groups of an MFMA C fragment's column) with the gfx950 lane-swap instructions, in the
+// vector ALU rather than through LDS: v_permlane32_swap exchanges the upper half of one register
+// with the lower half of another, so with both holding v each lane sees v of lane l^32; then
+// v_permlane16_swap does the same for lane l^16. Every lane gets the same result.
+PWD_DEV float swap32(float v, float& other) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    other = __uint_as_float(r[1]);
+    return __uint_as_float(r[0]);
+}
+PWD_DEV float swap16(float v, float& other) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    other = __uint_as_float(r[1]);
+    return __uint_as_float(r[0]);
+}
+PWD_DEV float group_sum(float v) {
+    float o;
+    const float a = swap32(v, o);
+    v = a + o;
+    const float b = swap16(v, o);
+    return b + o;
+}
+PWD_DEV float group_max(float v) {
+    float o;
+    const float a = swap32(v, o);
+    v = fmaxf(a, o);
+    const float b = swap16(v, o);
+    return fmaxf(b, o);
+}
+// the value of lane l % 16 (row 0 of a C fragment's column) in every lane
+PWD_DEV float row0_broadcast(float v) {
+    float o;
+    const float a = swap16(v, o);   // lanes of rows 0 and 1 now hold row 0's value
+    return swap32(a, o);            // and the upper half receives the lower half
+}
+
+// Detection events at window round t, one 32-stabilizer word (Sec. 2.2: a detector is the
+// parity of two consecutive measurements of one stabilizer; App. A.1.1: zero padding replaces
+// the missing buffer of the initial and final windows; the initial window's first core round
+// is compared with the all-zero state): event_from takes the words of rows t (prev) and t + 1
+// (cur), event_word reads them from the window's rows meas [W+1][words].
+PWD_DEV uint32_t event_from(uint32_t prev, uint32_t cur, int t, int type, int b_left, int d) {
     if (type == WIN_INITIAL) {
         if (t < b_left) return 0u;
         if (t == b_left) prev = 0u;
@@ -93,4 +127,8 @@ PWD_DEV uint32_t event_word(const uint32_t* __restrict__ meas, int words, int t,
         if (t >= b_left + d) return 0u;
     }
     return cur ^ prev;
+}
+PWD_DEV uint32_t event_word(const uint32_t* __restrict__ meas, int words, int t, int w,
+                            int type, int b_left, int d) {
+    return event_from(meas[t * words + w], meas[(t + 1) * words + w], t, type, b_left, d);
 }

@@ -36,7 +36,7 @@ constexpr int RCHUNK = 32;         // fragments per ring buffer
 constexpr int RD = 128;            // d_model of the resident path
 constexpr int RRT = RD / 16;       // 16-row C tiles of a d_model vector
 constexpr int RKS = RD / 32;       // 32-deep k-steps of a d_model vector
-constexpr int RLA = 4;             // fragment reads in flight ahead of their MFMAs
+constexpr int RLA = 8;             // fragment reads in flight ahead of their MFMAs (8: 8% faster than 4 at d7)
 constexpr int RMAXL = 4;           // layers whose vectors fit the LDS table
 
 template <int MR>
@@ -107,37 +107,90 @@ PWD_DEV bf16x4 to_b4(f32x4 v) {
     for (int i = 0; i < 4; ++i) r[i] = (__bf16)v[i];
     return r;
 }
-PWD_DEV bf16x4 half_b8(bf16x8 v, int h) {   // elements 4h .. 4h+3
-    return bf16x4{v[4 * h], v[4 * h + 1], v[4 * h + 2], v[4 * h + 3]};
+
+// Softmax over the window's keys for NP independent (query block, head) pairs at once, so that
+// their latencies overlap: scores s[p][kb] (keys 4g+i of key block kb as rows, this lane's
+// query as the column), exact row maximum, padding keys (index >= ntok, only ever in the last
+// block) excluded. The probabilities, rounded to bf16, go to pb (the P^T operand); inv gets 1 /
+// their column sum, taken on the matrix core from the same bf16 values (an A operand whose row 0
+// is all ones turns P^T into its column sums, in row 0 of the result).
+template <int NP, int TB>
+PWD_DEV void softmax_cols(f32x4 (&s)[NP][TB], bf16x4 (&pb)[NP][TB], float (&inv)[NP], int ntok, int g,
+                          bf16x4 ones) {
+    if (ntok < TB * 16) {   // wavefront-uniform: the last block holds padding keys
+#pragma unroll
+        for (int p = 0; p < NP; ++p)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if ((TB - 1) * 16 + 4 * g + i >= ntok) s[p][TB - 1][i] = -INFINITY;
+    }
+    float mx[NP];
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+        mx[p] = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < TB; ++kb)
+            mx[p] = fmaxf(mx[p], fmaxf(fmaxf(s[p][kb][0], s[p][kb][1]), fmaxf(s[p][kb][2], s[p][kb][3])));
+    }
+#pragma unroll
+    for (int p = 0; p < NP; ++p) mx[p] = group_max(mx[p]);
+    f32x4 ls[NP];
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+        ls[p] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kb = 0; kb < TB; ++kb) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) s[p][kb][i] = __builtin_amdgcn_exp2f(s[p][kb][i] - mx[p]);
+            pb[p][kb] = to_b4(s[p][kb]);
+            ls[p] = mfma16x16x16(ones, pb[p][kb], ls[p]);
+        }
+    }
+#pragma unroll
+    for (int p = 0; p < NP; ++p) inv[p] = __builtin_amdgcn_rcpf(row0_broadcast(ls[p][0]));
 }
 
-// Softmax over the window's keys for one query block: scores s[kb] (keys 4g+i of key block kb
-// as rows, this lane's query as the column), padding keys (index >= ntok) excluded, exact row
-// maximum; returns the probabilities in place (rounded to bf16 as the P^T operand) and 1/sum.
+// LayerNorm over the d_model features of each token (biased variance, two passes) of the state
+// plus `bias_in` (per feature, or null), in one pass over the state: the result, plus
+// `bias_out` (or null), goes back to the state, and the result itself (without bias_out) as bf16
+// B fragments to xb when `pack` is set -- the next matrix product's operand.
 template <int TB>
-PWD_DEV float softmax_cols(f32x4 (&s)[TB], bf16x4 (&pb)[TB], int ntok, int g) {
-    float mx = -INFINITY;
+PWD_DEV void ln_pack(f32x4 (&x)[RRT][TB], const float* bias_in, const float* gamma, const float* beta,
+                     const float* bias_out, bf16x8 (&xb)[RKS][TB], bool pack, float eps, int g) {
+    constexpr float inv_d = 1.0f / RD;
 #pragma unroll
-    for (int kb = 0; kb < TB; ++kb)
+    for (int b = 0; b < TB; ++b) {
+        f32x4 y[RRT];
+        float s = 0.f;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            if (kb * 16 + 4 * g + i >= ntok) s[kb][i] = -INFINITY;
-            mx = fmaxf(mx, s[kb][i]);
+        for (int rt = 0; rt < RRT; ++rt) {
+            y[rt] = x[rt][b];
+            if (bias_in) y[rt] += ld4(bias_in + rt * 16 + 4 * g);
+            s += (y[rt][0] + y[rt][1]) + (y[rt][2] + y[rt][3]);
         }
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    float sum = 0.f;
+        const float mean = group_sum(s) * inv_d;
+        float v = 0.f;
 #pragma unroll
-    for (int kb = 0; kb < TB; ++kb) {
+        for (int rt = 0; rt < RRT; ++rt)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) s[kb][i] = __builtin_amdgcn_exp2f(s[kb][i] - mx);
-        pb[kb] = to_b4(s[kb]);
+            for (int i = 0; i < 4; ++i) {
+                y[rt][i] -= mean;
+                v = fmaf(y[rt][i], y[rt][i], v);
+            }
+        const float rstd = rsqrtf(group_sum(v) * inv_d + eps);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) sum += (float)pb[kb][i];   // the same bf16 values as P^T
+        for (int rt = 0; rt < RRT; ++rt) {
+            const f32x4 gm = ld4(gamma + rt * 16 + 4 * g);
+            const f32x4 bt = ld4(beta + rt * 16 + 4 * g);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) y[rt][i] = fmaf(y[rt][i] * rstd, gm[i], bt[i]);
+        }
+        if (pack)
+#pragma unroll
+            for (int ks = 0; ks < RKS; ++ks) xb[ks][b] = pack_b(y[2 * ks], y[2 * ks + 1]);
+#pragma unroll
+        for (int rt = 0; rt < RRT; ++rt) x[rt][b] = bias_out ? y[rt] + ld4(bias_out + rt * 16 + 4 * g) : y[rt];
     }
-    sum += __shfl_xor(sum, 16);
-    sum += __shfl_xor(sum, 32);
-    return 1.0f / sum;
 }
 
 template <int TB, int MR, int DH>
@@ -174,14 +227,23 @@ __global__ __launch_bounds__(RWAVES * 64, 1) void resident_kernel(ResidentParams
 
     const uint32_t* meas = p.in.meas + (int64_t)win * (p.in.W + 1) * p.in.words;
     const int type = p.in.types[win];
-    int stab[TB];   // this lane's token's stabilizer in each block, or -1
+    int stab[TB];   // this lane's token's stabilizer in each block, or -1 (reads word 0)
+    uint32_t m_prev[TB], m_cur[TB];   // its measurement words of rows t and t + 1
 #pragma unroll
     for (int b = 0; b < TB; ++b) {
         const int s = b * 16 + col;
         stab[b] = s < p.ntok ? (p.tok_stab ? p.tok_stab[s] : s) : -1;
+        const int wd = stab[b] >= 0 ? stab[b] >> 5 : 0;
+        m_prev[b] = meas[wd];
+        m_cur[b] = meas[p.in.words + wd];
     }
 
+    bf16x4 ones;   // A operand with row 0 all ones: column sums on the matrix core
+#pragma unroll
+    for (int i = 0; i < 4; ++i) ones[i] = (__bf16)(col == 0 ? 1.0f : 0.0f);
+
     f32x4 x[RRT][TB];
+    bf16x8 xb[RKS][TB];   // the current matrix product's operand: a bf16 copy of the state
 #pragma unroll
     for (int rt = 0; rt < RRT; ++rt)
 #pragma unroll
@@ -192,11 +254,9 @@ __global__ __launch_bounds__(RWAVES * 64, 1) void resident_kernel(ResidentParams
         float ev[TB];
 #pragma unroll
         for (int b = 0; b < TB; ++b) {
-            ev[b] = 0.f;
-            if (stab[b] >= 0) {
-                const uint32_t w = event_word(meas, p.in.words, t, stab[b] >> 5, type, p.in.b_left, p.in.d);
-                ev[b] = (float)((w >> (stab[b] & 31)) & 1u);
-            }
+            const uint32_t w = event_from(m_prev[b], m_cur[b], t, type, p.in.b_left, p.in.d);
+            ev[b] = stab[b] >= 0 ? (float)((w >> (stab[b] & 31)) & 1u) : 0.f;
+            m_prev[b] = m_cur[b];
         }
 #pragma unroll
         for (int b = 0; b < TB; ++b) {
@@ -211,14 +271,15 @@ __global__ __launch_bounds__(RWAVES * 64, 1) void resident_kernel(ResidentParams
             }
         }
 
+        // the layer input as B fragments, the projections' operand (layers after the first get
+        // it from the previous layer's LayerNorm 2)
+#pragma unroll
+        for (int ks = 0; ks < RKS; ++ks)
+#pragma unroll
+            for (int b = 0; b < TB; ++b) xb[ks][b] = pack_b(x[2 * ks][b], x[2 * ks + 1][b]);
         for (int l = 0; l < p.L; ++l) {
             const float* vl = vec + l * V::PER_LAYER;
             const int cbase = l * S::LAYER_CHUNKS;
-            bf16x8 xb[RKS][TB];   // the layer input as B fragments (the projections' operand)
-#pragma unroll
-            for (int ks = 0; ks < RKS; ++ks)
-#pragma unroll
-                for (int b = 0; b < TB; ++b) xb[ks][b] = pack_b(x[2 * ks][b], x[2 * ks + 1][b]);
 
             // ---- per 32-feature group: Q, K, V, attention of its heads, out-projection k-step.
             // Groups run in pairs (ring buffers 0 and 1) in a loop rather than fully unrolled,
@@ -226,6 +287,13 @@ __global__ __launch_bounds__(RWAVES * 64, 1) void resident_kernel(ResidentParams
             auto og_group = [&](auto parc, int og) {
                 constexpr int PAR = decltype(parc)::value;
                 const uint16_t* buf = ring.template sync<PAR>();
+                if (PAR == 0 && og == 0 && l == 0 && t + 2 <= p.in.W) {
+                    // the next round's measurement words, issued ahead of this chunk's weight
+                    // loads so they have landed by the next chunk's wait
+#pragma unroll
+                    for (int b = 0; b < TB; ++b)
+                        m_cur[b] = meas[(t + 2) * p.in.words + (stab[b] >= 0 ? stab[b] >> 5 : 0)];
+                }
                 const uint16_t* nx = ring.next(cbase + og);
                 f32x4 q[2][TB], k[2][TB], v[2][TB];
 #pragma unroll
@@ -262,44 +330,60 @@ __global__ __launch_bounds__(RWAVES * 64, 1) void resident_kernel(ResidentParams
                 for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
                     for (int b = 0; b < TB; ++b) vt[hh][b] = to_b4(v[hh][b]);
-                bf16x8 qf[TB], kf[TB];
+                const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+                if constexpr (DH == 16) {   // two heads per group: features 16 hh .. 16 hh + 15
+                    constexpr int NP = 2 * TB;   // pair p = query block p / 2, head p % 2
+                    bf16x4 q4[2][TB], k4[2][TB];
 #pragma unroll
-                for (int b = 0; b < TB; ++b) {
-                    qf[b] = pack_b(q[0][b] * p.qscale, q[1][b] * p.qscale);
-                    kf[b] = pack_b(k[0][b], k[1][b]);
-                }
+                    for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
-                for (int qb = 0; qb < TB; ++qb) {
-                    f32x4 o[2];
-                    if constexpr (DH == 16) {   // two heads per group: features 16 hh .. 16 hh + 15
-#pragma unroll
-                        for (int hh = 0; hh < 2; ++hh) {
-                            f32x4 s[TB];
-                            bf16x4 pb[TB];
-#pragma unroll
-                            for (int kb = 0; kb < TB; ++kb)
-                                s[kb] = mfma16x16x16(half_b8(kf[kb], hh), half_b8(qf[qb], hh), f32x4{0.f, 0.f, 0.f, 0.f});
-                            const float inv = softmax_cols<TB>(s, pb, p.ntok, g);
-                            o[hh] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                            for (int kb = 0; kb < TB; ++kb) o[hh] = mfma16x16x16(vt[hh][kb], pb[kb], o[hh]);
-                            o[hh] *= inv;
+                        for (int b = 0; b < TB; ++b) {
+                            q4[hh][b] = to_b4(q[hh][b] * p.qscale);
+                            k4[hh][b] = to_b4(k[hh][b]);
                         }
-                    } else {   // one head of 32 features
-                        f32x4 s[TB];
-                        bf16x4 pb[TB];
+                    f32x4 s[NP][TB];
+                    bf16x4 pb[NP][TB];
+                    float inv[NP];
 #pragma unroll
-                        for (int kb = 0; kb < TB; ++kb) s[kb] = mfma16x16x32(kf[kb], qf[qb], f32x4{0.f, 0.f, 0.f, 0.f});
-                        const float inv = softmax_cols<TB>(s, pb, p.ntok, g);
+                    for (int pp = 0; pp < NP; ++pp)
 #pragma unroll
-                        for (int hh = 0; hh < 2; ++hh) {
-                            o[hh] = f32x4{0.f, 0.f, 0.f, 0.f};
+                        for (int kb = 0; kb < TB; ++kb) s[pp][kb] = mfma16x16x16(k4[pp % 2][kb], q4[pp % 2][pp / 2], zero);
+                    softmax_cols<NP, TB>(s, pb, inv, p.ntok, g, ones);
+                    f32x4 o[NP];
 #pragma unroll
-                            for (int kb = 0; kb < TB; ++kb) o[hh] = mfma16x16x16(vt[hh][kb], pb[kb], o[hh]);
-                            o[hh] *= inv;
-                        }
+                    for (int pp = 0; pp < NP; ++pp) {
+                        o[pp] = zero;
+#pragma unroll
+                        for (int kb = 0; kb < TB; ++kb) o[pp] = mfma16x16x16(vt[pp % 2][kb], pb[pp][kb], o[pp]);
                     }
-                    y[qb] = pack_b(o[0], o[1]);
+#pragma unroll
+                    for (int qb = 0; qb < TB; ++qb) y[qb] = pack_b(o[2 * qb] * inv[2 * qb], o[2 * qb + 1] * inv[2 * qb + 1]);
+                } else {   // one head of 32 features
+                    bf16x8 qf[TB], kf[TB];
+#pragma unroll
+                    for (int b = 0; b < TB; ++b) {
+                        qf[b] = pack_b(q[0][b] * p.qscale, q[1][b] * p.qscale);
+                        kf[b] = pack_b(k[0][b], k[1][b]);
+                    }
+                    f32x4 s[TB][TB];
+                    bf16x4 pb[TB][TB];
+                    float inv[TB];
+#pragma unroll
+                    for (int qb = 0; qb < TB; ++qb)
+#pragma unroll
+                        for (int kb = 0; kb < TB; ++kb) s[qb][kb] = mfma16x16x32(kf[kb], qf[qb], zero);
+                    softmax_cols<TB, TB>(s, pb, inv, p.ntok, g, ones);
+#pragma unroll
+                    for (int qb = 0; qb < TB; ++qb) {
+                        f32x4 o[2];
+#pragma unroll
+                        for (int hh = 0; hh < 2; ++hh) {
+                            o[hh] = zero;
+#pragma unroll
+                            for (int kb = 0; kb < TB; ++kb) o[hh] = mfma16x16x16(vt[hh][kb], pb[qb][kb], o[hh]);
+                        }
+                        y[qb] = pack_b(o[0] * inv[qb], o[1] * inv[qb]);
+                    }
                 }
 
                 // out-projection k-step og: X += Wo[:, og]^T y (the residual is the state itself)
@@ -316,25 +400,11 @@ __global__ __launch_bounds__(RWAVES * 64, 1) void resident_kernel(ResidentParams
                 og_group(std::integral_constant<int, 0>{}, og);
                 og_group(std::integral_constant<int, 1>{}, og + 1);
             }
-#pragma unroll
-            for (int rt = 0; rt < RRT; ++rt) {
-                const f32x4 bo = ld4(vl + V::BO + rt * 16 + 4 * g);
-#pragma unroll
-                for (int b = 0; b < TB; ++b) x[rt][b] += bo;
-            }
-            layer_norm<RRT, TB>(x, vl + V::G1, vl + V::BE1, p.eps, g);
+            // LayerNorm 1 of X + b_o; its output is the feed-forward's operand, and the
+            // feed-forward accumulators start at that output + b_2
+            ln_pack<TB>(x, vl + V::BO, vl + V::G1, vl + V::BE1, vl + V::B2, xb, true, p.eps, g);
 
-            // ---- feed-forward in chunks of 64 hidden units; accumulators start at X + b_2
-#pragma unroll
-            for (int ks = 0; ks < RKS; ++ks)
-#pragma unroll
-                for (int b = 0; b < TB; ++b) xb[ks][b] = pack_b(x[2 * ks][b], x[2 * ks + 1][b]);
-#pragma unroll
-            for (int rt = 0; rt < RRT; ++rt) {
-                const f32x4 b2 = ld4(vl + V::B2 + rt * 16 + 4 * g);
-#pragma unroll
-                for (int b = 0; b < TB; ++b) x[rt][b] += b2;
-            }
+            // ---- feed-forward in chunks of 64 hidden units
             constexpr int NRH = S::CH / 16, NKH = S::CH / 32;
             auto mlp_chunk = [&](auto parc, int c) {
                 constexpr int PAR = decltype(parc)::value;   // = (KS + c) & 1, KS even
@@ -385,7 +455,9 @@ __global__ __launch_bounds__(RWAVES * 64, 1) void resident_kernel(ResidentParams
                 mlp_chunk(std::integral_constant<int, 0>{}, c);
                 mlp_chunk(std::integral_constant<int, 1>{}, c + 1);
             }
-            layer_norm<RRT, TB>(x, vl + V::G2, vl + V::BE2, p.eps, g);
+            // LayerNorm 2; its output is the next layer's operand (the last layer's is the state
+            // D_t, which the next round's embedding changes first)
+            ln_pack<TB>(x, nullptr, vl + V::G2, vl + V::BE2, nullptr, xb, l + 1 < p.L, p.eps, g);
         }
     }
 

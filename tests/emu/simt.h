@@ -217,6 +217,8 @@ inline std::common_type_t<A, B> min(A a, B b) { return a < b ? a : b; }
 template <class A, class B>
 inline std::common_type_t<A, B> max(A a, B b) { return a < b ? b : a; }
 inline float rsqrtf(float x) { return 1.0f / std::sqrt(x); }
+inline unsigned __float_as_uint(float f) { unsigned u; std::memcpy(&u, &f, 4); return u; }
+inline float __uint_as_float(unsigned u) { float f; std::memcpy(&f, &u, 4); return f; }
 
 template <class T>
 inline T atomicOr(T* p, T v) {
@@ -238,6 +240,24 @@ inline uint64_t emu_amdgcn_ballot_w64(bool b) {
     return m;
 }
 inline float emu_amdgcn_exp2f(float x) { return std::exp2(x); }
+inline float emu_amdgcn_rcpf(float x) { return 1.0f / x; }
+typedef unsigned int emu_u32x2 __attribute__((ext_vector_type(2)));
+// v_permlane32_swap / v_permlane16_swap: the upper half (odd 16-lane rows) of the first operand
+// swaps with the lower half (even rows) of the second; returns (first, second) after the swap.
+inline emu_u32x2 emu_permlane_swap(unsigned v, unsigned s, int span) {
+    struct P { unsigned v, s; };
+    emu::xput(P{v, s}, 100 + span);
+    emu::wave_sync();
+    const int lane = emu::g_cur->lane;
+    const bool upper = (lane / span) & 1;
+    const P mine = emu::xget<P>(lane), peer = emu::xget<P>(upper ? lane - span : lane + span);
+    emu::xdone();
+    // upper lanes of the first operand take the second operand of the lower peer; lower lanes of
+    // the second operand take the first operand of the upper peer
+    return upper ? emu_u32x2{peer.s, mine.s} : emu_u32x2{mine.v, peer.v};
+}
+inline emu_u32x2 emu_amdgcn_permlane32_swap(unsigned v, unsigned s, bool, bool) { return emu_permlane_swap(v, s, 32); }
+inline emu_u32x2 emu_amdgcn_permlane16_swap(unsigned v, unsigned s, bool, bool) { return emu_permlane_swap(v, s, 16); }
 inline void emu_amdgcn_sched_group_barrier(int, int, int) {}
 inline void emu_amdgcn_sched_barrier(int) {}
 
