@@ -44,3 +44,15 @@ def test_more_than_one_gpu_is_refused():
                        capture_output=True, text=True, timeout=120, cwd=ROOT)
     assert "one GPU" in (r.stdout + r.stderr)
     assert not r.stdout.strip().startswith("{")
+
+
+def test_transformer_block_fraction():
+    """The transformer-block MFMA fraction sums the FLOPs of every launch of those stages over
+    their summed time; the readout is not part of it."""
+    import bench
+    flops = {"attention": 2e12, "post_qkv": 3e12, "readout": 1e12}
+    stages = {"attention": (4.0, 2), "post_qkv": (6.0, 2), "readout": (5.0, 1)}   # ms total, launches
+    tb = bench.transformer_blocks(stages, flops, steps=1)
+    assert tb["stages"] == ["attention", "post_qkv"]
+    want = (2 * 2e12 + 2 * 3e12) / 10e-3 / 1e12
+    assert abs(tb["tflops"] - want) < 0.1 and abs(tb["frac_of_bf16_peak"] - want / 2500) < 1e-4
