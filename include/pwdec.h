@@ -232,15 +232,17 @@ int decoder_detection_events(pwd_decoder* dec, const uint32_t* d_meas, const uin
  * decoded as by decode_windows and their results combined:
  *   d_stream:        uint32 [T][words] packed rounds, as the rows of decode_windows.
  *   d_window_logits: float [m] out, or NULL; d_window_bits: uint8 [m] out, or NULL.
+ *   d_window_probs:  float [m] out, or NULL: each window's probability of a logical flip in its
+ *                    core, y_k = 1 / (1 + exp(-logit_k)) (the sigmoid output the model is trained
+ *                    on, Sec. 3.3; the inputs of eq. soft_xor), computed in double, rounded once.
  *   d_bit:           uint8 [1] out: XOR of the window bits, the global logical correction.
  *   d_prob:          float [1] out, or NULL: soft-XOR (1 - prod_k (1 - 2 y_k)) / 2 of the
- *                    window probabilities y_k = 1 / (1 + exp(-logit_k)), accumulated in
- *                    double in a fixed order.
+ *                    window probabilities y_k, accumulated in double in a fixed order.
  * PWD_EINVAL if dec, d_stream or d_bit is NULL or T <= 0; PWD_EBATCH unless
  * 2 <= m <= max_windows. The window scratch (allocated by decoder_create) belongs to the
  * handle, so calls on one handle must not overlap. */
 int decode_stream(pwd_decoder* dec, const uint32_t* d_stream, int64_t T, float* d_window_logits,
-                  uint8_t* d_window_bits, uint8_t* d_bit, float* d_prob, void* hip_stream);
+                  uint8_t* d_window_bits, float* d_window_probs, uint8_t* d_bit, float* d_prob, void* hip_stream);
 
 /* Synchronises hip_stream, then reports PWD_EDEVICE if a device-side check fired since
  * the previous call (and clears it), PWD_EHIP on a stream error, else PWD_OK. */

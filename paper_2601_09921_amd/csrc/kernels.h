@@ -150,6 +150,7 @@ struct StreamCombineParams {
     int m;
     uint8_t* bit;             // [1] out
     float* prob;              // [1] out, or null
+    float* probs;             // [m] out, or null: sigmoid of each window's logit
 };
 hipError_t launch_stream_split(const StreamSplitParams& p, hipStream_t s);
 hipError_t launch_stream_combine(const StreamCombineParams& p, hipStream_t s);

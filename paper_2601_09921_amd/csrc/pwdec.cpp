@@ -991,7 +991,7 @@ int decoder_detection_events(pwd_decoder* dec, const uint32_t* d_meas, const uin
 }
 
 int decode_stream(pwd_decoder* dec, const uint32_t* d_stream, int64_t T, float* d_window_logits,
-                  uint8_t* d_window_bits, uint8_t* d_bit, float* d_prob, void* hip_stream) {
+                  uint8_t* d_window_bits, float* d_window_probs, uint8_t* d_bit, float* d_prob, void* hip_stream) {
     if (!dec) return fail(PWD_EINVAL, "null decoder");
     if (!d_stream || !d_bit) return fail(PWD_EINVAL, "null buffer");
     if (T <= 0) return fail(PWD_EINVAL, "stream of %lld rounds", (long long)T);
@@ -1023,6 +1023,7 @@ int decode_stream(pwd_decoder* dec, const uint32_t* d_stream, int64_t T, float* 
     cp.m = (int)m;
     cp.bit = d_bit;
     cp.prob = d_prob;
+    cp.probs = d_window_probs;
     HIP_OK(timed(dec, PWD_STAGE_STREAM_COMBINE, s, [&] { return launch_stream_combine(cp, s); }));
     return PWD_OK;
 }

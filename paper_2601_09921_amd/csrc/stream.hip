@@ -27,7 +27,8 @@ __global__ __launch_bounds__(SPLIT_THREADS) void stream_split_kernel(StreamSplit
     if (idx < (IDX)p.m) p.types[idx] = idx == 0 ? WIN_INITIAL : (idx == (IDX)p.m - 1 ? WIN_FINAL : WIN_BULK);
 }
 
-// One workgroup: XOR of the window bits and prod_k (1 - 2 sigmoid(logit_k)) in double. Each
+// One workgroup: XOR of the window bits and prod_k (1 - 2 sigmoid(logit_k)) in double (and,
+// when asked for, each window's probability sigmoid(logit_k) rounded to float). Each
 // thread takes a fixed stride of windows and the partial results are combined by a fixed
 // tree, so the result does not depend on timing.
 __global__ __launch_bounds__(COMBINE_THREADS) void stream_combine_kernel(StreamCombineParams p) {
@@ -37,6 +38,7 @@ __global__ __launch_bounds__(COMBINE_THREADS) void stream_combine_kernel(StreamC
     int x = 0;
     for (int i = threadIdx.x; i < p.m; i += COMBINE_THREADS) {
         const double y = 1.0 / (1.0 + exp(-(double)p.logits[i]));
+        if (p.probs) p.probs[i] = (float)y;
         pr *= 1.0 - 2.0 * y;
         x ^= p.bits[i] & 1;
     }

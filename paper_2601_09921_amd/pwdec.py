@@ -75,7 +75,7 @@ def bind(lib: ctypes.CDLL) -> ctypes.CDLL:
         "decode_windows_recurrent": (ctypes.c_int, [VP, VP, VP, I64, VP, VP, VP]),
         "decode_windows_noalloc": (ctypes.c_int, [VP, VP, VP, I64, VP, VP, VP]),
         "decoder_detection_events": (ctypes.c_int, [VP, VP, VP, I64, VP, VP]),
-        "decode_stream": (ctypes.c_int, [VP, VP, I64, VP, VP, VP, VP, VP]),
+        "decode_stream": (ctypes.c_int, [VP, VP, I64, VP, VP, VP, VP, VP, VP]),
         "decoder_sync_status": (ctypes.c_int, [VP, VP]),
         "decoder_last_error": (ctypes.c_char_p, []),
         "decoder_destroy": (ctypes.c_int, [VP]),
@@ -249,10 +249,11 @@ class Decoder:
                                                   ctypes.c_void_p(logits.data_ptr()),
                                                   ctypes.c_void_p(bits.data_ptr()), _stream_ptr(stream)))
 
-    def decode_stream(self, rounds, bit, prob=None, window_logits=None, window_bits=None, stream=None):
+    def decode_stream(self, rounds, bit, prob=None, window_logits=None, window_bits=None, stream=None,
+                      window_probs=None):
         """rounds: int32/uint32 [T][words] cuda tensor of packed measurement rounds; bit: uint8 [1]
-        out; prob: float32 [1] out or None; window_logits / window_bits: float32 / uint8
-        [ceil(T/d)] out or None."""
+        out; prob: float32 [1] out or None; window_logits / window_bits / window_probs: float32 /
+        uint8 / float32 [ceil(T/d)] out or None (window_probs: sigmoid of each logit)."""
         ptr = lambda t: ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
         require(rounds, "rounds", WORDS, self.device)
         if rounds.dim() != 2 or rounds.shape[1] != self.words:
@@ -265,8 +266,11 @@ class Decoder:
             require(window_logits, "window_logits", ("float32",), self.device, min_numel=m)
         if window_bits is not None:
             require(window_bits, "window_bits", ("uint8",), self.device, min_numel=m)
+        if window_probs is not None:
+            require(window_probs, "window_probs", ("float32",), self.device, min_numel=m)
         _check(self._lib.decode_stream(self._h, ptr(rounds), rounds.shape[0], ptr(window_logits),
-                                       ptr(window_bits), ptr(bit), ptr(prob), _stream_ptr(stream)))
+                                       ptr(window_bits), ptr(window_probs), ptr(bit), ptr(prob),
+                                       _stream_ptr(stream)))
 
     def detection_events(self, meas, types, events, stream=None):
         """events: int32/uint32 [n][W][words] out."""

@@ -71,7 +71,7 @@ def test_null_arguments(lib):
     g, m = pwdec.geometry(3, 6, 4), pwdec.dims(64, 2, 4, 4, 0)
     assert lib.decoder_create(ctypes.byref(g), ctypes.byref(m), None, 0, ctypes.byref(h)) == pwdec.PWD_EINVAL
     assert lib.decode_windows(None, None, None, 0, None, None, None) == pwdec.PWD_EINVAL
-    assert lib.decode_stream(None, None, 0, None, None, None, None, None) == pwdec.PWD_EINVAL
+    assert lib.decode_stream(None, None, 0, None, None, None, None, None, None) == pwdec.PWD_EINVAL
     assert lib.decode_windows_recurrent(None, None, None, 0, None, None, None) == pwdec.PWD_EINVAL
     assert lib.decoder_destroy(None) == pwdec.PWD_OK
 

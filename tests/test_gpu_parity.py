@@ -55,6 +55,26 @@ def test_logits_match_oracle(name):
     assert np.array_equal(bits, (logits > 0).astype(np.uint8))
 
 
+def test_d7_layer_phased_schedule():
+    """The d7 network decodes with the state-resident schedule by default; the layer-phased one
+    (one launch per layer and round) stays selectable and matches the oracle too, with the
+    same batch invariance."""
+    wl = synth.WORKLOADS["d7"]
+    B = SMALL["d7"]
+    meas, types = inputs("d7", B)
+    dec = pwdec.Decoder.from_workload(wl, weights("d7"), max_windows=B)
+    dec.schedule(pwdec.SCHEDULE_LAYERS)
+    say(f"decode d7 B={B} layer-phased")
+    logits, bits, rc = gpu_decode(dec, meas, types)
+    assert rc == pwdec.PWD_OK
+    o_logits, _, _ = oracle("d7", B)
+    check_logits("d7", logits, o_logits)
+    check_bits(bits, o_logits)
+    one, _, _ = gpu_decode(dec, meas[B - 1:], types[B - 1:])
+    assert one.view(np.uint32)[0] == logits.view(np.uint32)[B - 1]
+    dec.close()
+
+
 @pytest.mark.parametrize("name", ["d3", "d7", "d11"])
 def test_masks_reach_the_network(name):
     """Windows whose padded rows hold random measurements decode like the oracle, which
@@ -133,10 +153,28 @@ def test_invalid_type_and_batch_limits(name):
     assert rc == pwdec.PWD_EBATCH
 
 
+def spread_sample(B, k):
+    """Windows spread over a batch of B beyond its first k: one per residue mod 8 at evenly
+    spaced positions (the readout runs one workgroup per window and workgroups go round-robin
+    over the 8 XCDs, so each XCD's share is represented; so are distant token-kernel tiles), and
+    the last two windows (the final, partly padded workgroup tiles of every kernel)."""
+    base = (k + 7) // 8 * 8
+    picks = {base + x * ((B - base) // 8) // 8 * 8 + x for x in range(8)} | {B - 2, B - 1}
+    return sorted(w for w in picks if k <= w < B)
+
+
+def test_spread_sample_covers_xcds_and_the_tail():
+    for B, k in ((8192, 3), (4096, 4), (4096, 13), (1024, 97)):
+        sample = spread_sample(B, k)
+        assert {w % 8 for w in sample} == set(range(8)) and sample[-2:] == [B - 2, B - 1]
+        assert min(sample) >= k and max(np.diff(sample)) > B // 16
+
+
 @pytest.mark.parametrize("name", ["d7", "d11", "d17", "d25"])
 def test_full_batch_sampled(name):
-    """The full batch of the workload, in the launch configuration the benchmark times:
-    the leading windows against the oracle, sampled windows against a batch of one."""
+    """The full batch of the workload, in the launch configuration the benchmark times: the
+    leading windows and windows spread across the batch -- one per XCD residue, the last two
+    (the final partial tiles) -- against the oracle; two more against a batch of one."""
     wl = synth.WORKLOADS[name]
     B = wl.B
     meas, types = inputs(name, B)
@@ -150,6 +188,11 @@ def test_full_batch_sampled(name):
     o_logits, _, _ = oracle(name, k)
     check_logits(name, logits[:k], o_logits)
     check_bits(bits[:k], o_logits)
+    spread = spread_sample(B, k)
+    say(f"  oracle on {len(spread)} spread windows")
+    o_spread, _ = O.forward_windows(meas[spread], types[spread], weights(name), wl.d, wl.H)
+    check_logits(name, logits[spread], o_spread)
+    check_bits(bits[spread], o_spread)
     for w in (B // 3 + 1, B - 1):
         one, _, _ = gpu_decode(dec, meas[w:w + 1], types[w:w + 1])
         assert one.view(np.uint32)[0] == logits.view(np.uint32)[w], f"window {w}"

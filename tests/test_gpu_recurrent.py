@@ -44,7 +44,13 @@ def test_recurrent_parity(name, B):
     say(f"  max |gpu - oracle| = {err.max():.3e}")
     assert (err <= bound).all(), (gl, ol)
     assert np.array_equal(gb, (gl > 0).astype(np.uint8))
-    # the last readout is the inference branch, computed by the same kernels
+    # the last readout is the inference branch: bit for bit the layer-phased decode (the
+    # recurrent branch's schedule), and within the tolerance of the default schedule (the
+    # state-resident one where the network allows it)
+    fl, _, rc = gpu_decode(dec, meas, types)
+    assert rc == pwdec.PWD_OK
+    assert (np.abs(gl[:, -1] - fl) <= (bound[:, -1] if bound.ndim == 2 else bound)).all()
+    dec.schedule(pwdec.SCHEDULE_LAYERS)
     fl, _, rc = gpu_decode(dec, meas, types)
     assert rc == pwdec.PWD_OK
     assert np.array_equal(gl[:, -1].view(np.uint32), fl.view(np.uint32))

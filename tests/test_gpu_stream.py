@@ -29,11 +29,12 @@ def run_stream(dec, R, m, with_windows=True):
     prob = torch.full((1,), float("nan"), dtype=torch.float32, device="cuda")
     wl = torch.full((m,), float("nan"), dtype=torch.float32, device="cuda") if with_windows else None
     wb = torch.full((m,), 7, dtype=torch.uint8, device="cuda") if with_windows else None
-    dec.decode_stream(rounds, bit, prob, wl, wb)
+    wp = torch.full((m,), float("nan"), dtype=torch.float32, device="cuda") if with_windows else None
+    dec.decode_stream(rounds, bit, prob, wl, wb, window_probs=wp)
     torch.cuda.synchronize()
     out = [int(bit.item()), float(prob.item())]
     if with_windows:
-        out += [wl.cpu().numpy(), wb.cpu().numpy()]
+        out += [wl.cpu().numpy(), wb.cpu().numpy(), wp.cpu().numpy()]
     return out
 
 
@@ -55,7 +56,7 @@ def test_stream_parity(name, T, zero):
     m = -(-T // wl.d)
     say(f"stream {name} T={T} m={m} zero={zero}")
     dec = pwdec.Decoder.from_workload(wl, w, max_windows=m)
-    bit, prob, glog, gbits = run_stream(dec, R, m)
+    bit, prob, glog, gbits, gprob = run_stream(dec, R, m)
     assert dec.sync_status() == pwdec.PWD_OK
     meas, types = O.split_stream(R, wl.d, wl.W)
     olog, _ = O.forward_windows(meas, types, w, wl.d, wl.H)
@@ -72,6 +73,10 @@ def test_stream_parity(name, T, zero):
     # window moves the soft-XOR by at most |d sigmoid| <= |d logit| / 4
     assert prob == pytest.approx(O.soft_xor(sigmoid(glog)), rel=1e-5, abs=1e-6)
     assert abs(prob - O.soft_xor(sigmoid(olog))) <= float(np.sum(bound)) / 4 + 1e-6
+    # per-window probabilities: the sigmoid of the device's own logits (computed in double,
+    # rounded once), and within |d logit| / 4 of the oracle's
+    assert np.array_equal(gprob, sigmoid(glog).astype(np.float32))
+    assert (np.abs(gprob - sigmoid(olog)) <= bound / 4 + 1e-7).all()
     # the same stream without the per-window outputs gives the same combined results
     bit2, prob2 = run_stream(dec, R, m, with_windows=False)
     assert bit2 == bit and np.float32(prob2) == np.float32(prob)
@@ -104,9 +109,10 @@ def test_stream_full_size_sampled():
     R = synth.make_stream(wl.N, T, wl.p, seed=2025)
     say(f"stream d25 T={T} m={m}")
     dec = pwdec.Decoder.from_workload(wl, w, max_windows=m)
-    bit, prob, glog, gbits = run_stream(dec, R, m)
+    bit, prob, glog, gbits, gprob = run_stream(dec, R, m)
     assert dec.sync_status() == pwdec.PWD_OK
     assert np.isfinite(glog).all() and bit == O.combine_bits(gbits)
+    assert np.array_equal(gprob, sigmoid(glog).astype(np.float32))
     assert prob == pytest.approx(O.soft_xor(sigmoid(glog)), rel=1e-5, abs=1e-6)
     dec.close()
     meas, types = O.split_stream(R, wl.d, wl.W)
