@@ -55,9 +55,17 @@ typedef struct {
 
 /* Network dimensions (App. A model table): d_model, layers, heads, MLP expansion (the
  * feed-forward width is mlp_ratio * d_model; the model table gives 5), the arithmetic type,
- * the token set, the embedder and the dilated convolutions (see the enums below). PWD_DTYPE_BF16: bf16 weights and matrix operands, fp32
- * accumulation, softmax, LayerNorm, residual stream and recurrent state. PWD_DTYPE_F32: fp32
- * throughout. PWD_TOKENS_STABILIZERS: one token per stabilizer (d*d-1); PWD_TOKENS_GRID: one
+ * the token set, the embedder and the dilated convolutions (see the enums below).
+ * PWD_DTYPE_BF16: bf16 weights and matrix operands, fp32 accumulation, softmax, LayerNorm,
+ * residual stream and recurrent state. PWD_DTYPE_F32: fp32 throughout. PWD_DTYPE_MXFP8: as
+ * bf16, except that the Q, K and V projections and the feed-forward's first matrix (d_model ->
+ * F) of every layer take MXFP8 operands (quantization, named in Sec. 1 and Sec. 5 as the route
+ * toward the real-time budget): OCP Microscaling v1.0 FP8 E4M3 elements with one E8M0 scale
+ * 2^(floor(log2 amax) - 8) per block of 32 input features (each 128-feature slice splits into
+ * four blocks; feature f is in block 4 (f/128) + 2 ((f/64) % 2) + (f/8) % 2), elements rounded
+ * to nearest even and clamped to +-448; one scale per token and block for the activations
+ * (quantized on the fly), one per output feature and block for the weights (quantized once,
+ * by decoder_create); fp32 accumulation. PWD_TOKENS_STABILIZERS: one token per stabilizer (d*d-1); PWD_TOKENS_GRID: one
  * token per cell of the (d+1)x(d+1) stabilizer array (App. A.1.2 and the (d+1)^2 x d_model
  * state of Algorithm 1), the cells without a stabilizer carrying state but no detection
  * events. Syndrome inputs and detection events stay one bit per stabilizer either way. */
@@ -72,7 +80,7 @@ typedef struct {
     int32_t conv_dilation[3];
 } pwd_model_dims;
 
-enum { PWD_DTYPE_F32 = 0, PWD_DTYPE_BF16 = 1 };
+enum { PWD_DTYPE_F32 = 0, PWD_DTYPE_BF16 = 1, PWD_DTYPE_MXFP8 = 2 };
 enum { PWD_TOKENS_STABILIZERS = 0, PWD_TOKENS_GRID = 1 };
 /* PWD_EMBED_LINEAR: the embedding is Linear(1 -> d_model) of each event bit plus PE.
  * PWD_EMBED_RESNET: the model table's StabilizerEmbedder, Linear(1 -> d_model) followed by a
@@ -124,7 +132,8 @@ typedef enum {
  *     dilated convolutions only, per layer: Wd[3][3][3][D][D] bd[3][D]   ([j][a][e][in][out]:
  *                                                       unit j, tap (a, e) reading the cell
  *                                                       at dil_j (a - 1, e - 1))
- * For PWD_DTYPE_BF16 the values are used rounded to bf16 (they should already be
+ * For PWD_DTYPE_BF16 and PWD_DTYPE_MXFP8 the values are used rounded to bf16, those of Wq, Wk,
+ * Wv and W1 under MXFP8 quantized from the given float32 values instead (they should already be
  * bf16-representable). The positional encoding is not stored: the library computes it. */
 #define PWD_BLOB_MAGIC 0x31445750u
 #define PWD_BLOB_VERSION 1
@@ -140,6 +149,7 @@ size_t decoder_blob_floats(const pwd_geometry* geom, const pwd_model_dims* dims)
  * token_set PWD_TOKENS_STABILIZERS or PWD_TOKENS_GRID (n_tokens = d*d-1 or (d+1)^2);
  * embedder PWD_EMBED_LINEAR or PWD_EMBED_RESNET; conv_dilation all 0, or all in 1..distance
  * with PWD_TOKENS_GRID (bf16: d_model 128 only for now);
+ * PWD_DTYPE_MXFP8: as PWD_DTYPE_BF16, without the dilated convolutions;
  * PWD_DTYPE_BF16: d_model in {128, 256}, head size d_model/n_heads in {16, 32, 64}, and the
  * attention tile (K and V of one head: (2 ceil(n_tokens/16) + 1) KB, twice that for head size
  * 64) within 160 KB of LDS;
@@ -275,7 +285,7 @@ enum {
  *   PWD_SCHEDULE_LAYERS: one launch per layer and round for attention and one for the token-local
  *     stages, the state and activations of the whole batch in HBM between launches;
  *   PWD_SCHEDULE_RESIDENT: one launch for every round and layer, each window owned by one
- *     wavefront with its state, Q, K and V kept in registers throughout (bf16, d_model 128, at
+ *     wavefront with its state, Q, K and V kept in registers throughout (PWD_DTYPE_BF16, d_model 128, at
  *     most 64 tokens and 4 layers, heads of 16 or 32, feed-forward 4 d_model, no dilated
  *     convolutions or embedder block), then the readout;
  *   PWD_SCHEDULE_AUTO (the default): RESIDENT where the configuration allows it, else LAYERS.

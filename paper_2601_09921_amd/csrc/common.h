@@ -56,8 +56,15 @@ PWD_DEV uint32_t lds_addr(T* p) {
 // wait-count pass treats a pending direct-to-LDS builtin as outstanding LDS traffic and then
 // waits for every LDS read before each use; callers await completion with s_waitcnt vmcnt.
 // The memory clobber keeps the load in program order relative to other memory accesses.
+// The compiler cannot see the operands of inline assembly when it inserts the wait states the
+// hardware requires, and a vector instruction that writes an SGPR (v_readfirstlane, which
+// uniform_ptr becomes when the address was computed in VGPRs) must be followed by 5 of them
+// before a vector memory instruction reads that SGPR as its address; otherwise the load uses
+// the register's previous contents. LDS_DMA_GUARD provides them (and the one an SALU write of
+// M0 needs before the load reads it).
+#define LDS_DMA_GUARD "s_nop 4\n\t"
 PWD_DEV void lds_load_1k(const void* src, uint32_t lds, int lane) {
-    asm volatile("global_load_lds_dwordx4 %0, %1" :: "v"((uint32_t)lane * 16), "s"(src), "{m0}"(lds)
+    asm volatile(LDS_DMA_GUARD "global_load_lds_dwordx4 %0, %1" :: "v"((uint32_t)lane * 16), "s"(src), "{m0}"(lds)
                  : "memory");
 }
 

@@ -15,7 +15,10 @@ struct SyndromeIn {
 // POST = out-projection + LN1 + feed-forward + LN2. With the dilated convolutions between LN1
 // and the feed-forward, POST splits into WO (out-projection + LN1, alone; also writes the
 // convolutions' bf16 input G) and FFN (feed-forward + LN2, then EMBED / QKV as after POST).
-enum { TOK_POST = 1, TOK_EMBED = 2, TOK_QKV = 4, TOK_RESNET = 8, TOK_WO = 16, TOK_FFN = 32 };
+// MX: the Q/K/V projections and the feed-forward's first matrix take MXFP8 operands (E4M3
+// elements, one E8M0 scale per 32-feature block; see tok.hip); their weight streams are laid
+// out for it.
+enum { TOK_POST = 1, TOK_EMBED = 2, TOK_QKV = 4, TOK_RESNET = 8, TOK_WO = 16, TOK_FFN = 32, TOK_MX = 64 };
 
 struct TokParams {
     SyndromeIn in;          // in.N: stabilizers (bits per measurement round)
@@ -128,6 +131,8 @@ hipError_t launch_events(const EventsParams& p, hipStream_t s);
 int64_t tok_block_granule();
 int tok_mlp_chunk(int D);
 int tok_bv_rep(int D, int F);
+int tok_mx_qkv_frags();     // MXFP8 fragments per Q/K/V chunk
+int tok_mx_scale_slot();    // 1 KB slot of a chunk that holds its MXFP8 weight scales
 hipError_t launch_tok(int D, int F, int flags, const TokParams& p, int64_t n_tb, hipStream_t s);
 hipError_t launch_conv(int D, bool gout, const ConvParams& p, int64_t n_tb, hipStream_t s);
 hipError_t launch_attn(int dh, const AttnParams& p, int nwin, hipStream_t s);

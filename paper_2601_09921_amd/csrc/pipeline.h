@@ -56,6 +56,26 @@ PWD_DEV void static_for_impl(const F& f, std::integer_sequence<int, I...>) {
 template <int N, typename F>
 PWD_DEV void static_for(const F& f) { static_for_impl(f, std::make_integer_sequence<int, N>{}); }
 
+// As sched_pipeline, for chunks whose first NPAIRED reads come in pairs (the two halves of one
+// 8-bit fragment): the MFMAs of a pair follow its second read.
+template <int NREAD, int MPR, int LA, int NPAIRED>
+PWD_DEV void sched_pipeline_pairs() {
+    static_assert(NPAIRED % 2 == 0 && NPAIRED <= NREAD, "whole pairs");
+    constexpr auto mfmas = [](int r) { return r < NPAIRED ? (r & 1 ? MPR : 0) : MPR; };
+    __builtin_amdgcn_sched_group_barrier(0x100, LA, 0);
+    static_for<NREAD - LA>([&](auto kc) {
+        constexpr int M = mfmas(decltype(kc)::value);
+        if constexpr (M > 0) __builtin_amdgcn_sched_group_barrier(0x008, M, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    });
+    constexpr int TAIL = [=] {
+        int n = 0;
+        for (int k = NREAD - LA; k < NREAD; ++k) n += mfmas(k);
+        return n;
+    }();
+    __builtin_amdgcn_sched_group_barrier(0x008, TAIL, 0);
+}
+
 // LayerNorm over the D features of each token (biased variance, two passes); gamma and
 // beta are in LDS.
 template <int RT, int TB>

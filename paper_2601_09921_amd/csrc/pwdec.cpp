@@ -122,6 +122,126 @@ void append_qkv_stream(std::vector<uint16_t>& out, const float* Wqkv, int D) {
             }
 }
 
+// ---- MXFP8 weight streams (PWD_DTYPE_MXFP8; OCP Microscaling v1.0: E4M3 elements, one E8M0
+// scale per block of 32 input features)
+
+// Block of input feature f: each 128-feature slice splits into four blocks of 32, the runs of 8
+// features of a 64-feature half alternating between two of them -- the blocks whose scales the
+// token kernel's matrix-core operands take from lane groups 0..3 (see tok.hip).
+int mx_block(int f) { return 4 * (f / 128) + 2 * ((f / 64) % 2) + (f / 8) % 2; }
+
+// Shared exponent of a block with largest magnitude amax: floor(log2 amax) - 8 (8: the exponent
+// of E4M3's largest power of two), within E8M0's [-127, 127]; -127 for amax = 0.
+int mx_exponent(double amax) {
+    if (!(amax > 0.0)) return -127;
+    int e;
+    std::frexp(amax, &e);   // amax = m 2^e, m in [0.5, 1): floor(log2 amax) = e - 1
+    return std::min(127, std::max(-127, e - 1 - 8));
+}
+
+// E4M3 code of v: nearest value, ties to even mantissa; magnitudes from 448 (the largest finite
+// value) up clamp to 448. Codes are monotone in the magnitude, subnormals (2^-9 steps below
+// 2^-6) included.
+uint8_t e4m3_code(double v) {
+    const uint8_t sign = std::signbit(v) ? 0x80 : 0x00;
+    const double a = std::fabs(v);
+    if (!(a < 448.0)) return sign | 0x7e;
+    if (a < std::ldexp(1.0, -6)) return sign | (uint8_t)std::nearbyint(std::ldexp(a, 9));   // 8 -> 2^-6
+    int e;
+    std::frexp(a, &e);
+    int E = e - 1;                                              // a in [2^E, 2^(E+1)), E in [-6, 8]
+    int q = (int)std::nearbyint((std::ldexp(a, -E) - 1.0) * 8.0);   // 3 mantissa bits
+    if (q == 8) {
+        q = 0;
+        ++E;
+    }
+    return sign | (uint8_t)(((E + 7) << 3) | q);
+}
+
+// Exponents [O][K/32] of W [K][O] (y = x W), one per output feature and input block.
+std::vector<int> mx_exponents(const float* W, int K, int O) {
+    std::vector<double> amax((size_t)O * (K / 32), 0.0);
+    for (int k = 0; k < K; ++k)
+        for (int o = 0; o < O; ++o) {
+            double& m = amax[(size_t)o * (K / 32) + mx_block(k)];
+            m = std::max(m, std::fabs((double)W[(size_t)k * O + o]));
+        }
+    std::vector<int> ex(amax.size());
+    for (size_t i = 0; i < amax.size(); ++i) ex[i] = mx_exponent(amax[i]);
+    return ex;
+}
+
+// The 8-bit A fragment (row tile ro, 128-deep k-step ks8) of W^T: 2 KB at `frag`, half h of lane
+// l at frag + 1024 h + 16 l; lane (m = l % 16, g = l / 16) byte e holds input feature
+// 128 ks8 + 16 (e / 4) + 4 g + e % 4 of output feature 16 ro + m, divided by its block's scale.
+// scale[16 l]: the E8M0 byte (exponent + 127) of output 16 ro + m, block 4 ks8 + g -- the
+// block lane group g stands for.
+void mx_fragment(const float* W, int K, int O, const std::vector<int>& ex, int ro, int ks8, uint8_t* frag,
+                 uint8_t* scale) {
+    for (int l = 0; l < 64; ++l) {
+        const int m = l & 15, g = l >> 4, o = 16 * ro + m;
+        for (int e = 0; e < 32; ++e) {
+            const int k = 128 * ks8 + 16 * (e / 4) + 4 * g + e % 4;
+            const double v = std::ldexp((double)W[(size_t)k * O + o], -ex[(size_t)o * (K / 32) + mx_block(k)]);
+            frag[1024 * (e / 16) + 16 * l + e % 16] = e4m3_code(v);
+        }
+        scale[16 * l] = (uint8_t)(ex[(size_t)o * (K / 32) + 4 * ks8 + g] + 127);
+    }
+}
+
+// MXFP8 Q/K/V stream of one layer (Wqkv [D][3D]): chunks of 32 KB, each holding `per_chunk`
+// 8-bit fragments (output group og of 32 features, k-step ks8, row tile 2 og + hh), then, in
+// 1 KB slot `scale_slot`, byte j of each lane's 16 the scale of fragment j; unused bytes zero.
+void append_qkv_stream_mx(std::vector<uint16_t>& out, const float* Wqkv, int D, int per_chunk, int scale_slot) {
+    const int KS8 = D / 128, O = 3 * D, opc = per_chunk / (2 * KS8), nchunks = (O / 32) / opc;
+    const std::vector<int> ex = mx_exponents(Wqkv, D, O);
+    for (int qc = 0; qc < nchunks; ++qc) {
+        std::vector<uint8_t> chunk(32 * 1024, 0);
+        for (int j = 0; j < per_chunk; ++j) {
+            const int hh = j & 1, ks8 = (j >> 1) % KS8, o2 = (j >> 1) / KS8;
+            mx_fragment(Wqkv, D, O, ex, 2 * (qc * opc + o2) + hh, ks8, chunk.data() + 2048 * j,
+                        chunk.data() + 1024 * scale_slot + j);
+        }
+        const size_t at = out.size();
+        out.resize(at + chunk.size() / 2);
+        std::memcpy(out.data() + at, chunk.data(), chunk.size());
+    }
+}
+
+// MXFP8 post stream of one layer: the out-projection's bf16 fragments as in append_post_stream,
+// then per feed-forward chunk of CH hidden units a 32 KB chunk: the 8-bit W1 fragments (hidden
+// row tile, k-step), the bf16 W2 fragments (row tile, hidden k-step) right after them, and the
+// W1 scales in slot `scale_slot`.
+// Returns false if a chunk's data would reach the scale slot.
+bool append_post_stream_mx(std::vector<uint16_t>& out, const float* Wo, const float* W1, const float* W2, int D, int F,
+                           int CH, int scale_slot) {
+    const int RT = D / 16, KS = D / 32, FKS = F / 32, KS8 = D / 128, nw1 = (CH / 16) * KS8;
+    std::vector<uint16_t> fo, f2;
+    append_frags(fo, Wo, D, D);
+    append_frags(f2, W2, F, D);
+    for (int rt = 0; rt < RT; ++rt)
+        for (int ks = 0; ks < KS; ++ks)
+            out.insert(out.end(), fo.begin() + ((size_t)rt * KS + ks) * 512, fo.begin() + ((size_t)rt * KS + ks + 1) * 512);
+    const std::vector<int> ex = mx_exponents(W1, D, F);
+    for (int c = 0; c < F / CH; ++c) {
+        std::vector<uint8_t> chunk(32 * 1024, 0);
+        for (int j = 0; j < nw1; ++j)
+            mx_fragment(W1, D, F, ex, c * (CH / 16) + j / KS8, j % KS8, chunk.data() + 2048 * j,
+                        chunk.data() + 1024 * scale_slot + j);
+        int slot = 2 * nw1;
+        for (int rt = 0; rt < RT; ++rt)
+            for (int kh = 0; kh < CH / 32; ++kh, ++slot) {
+                const size_t fr = (size_t)rt * FKS + c * (CH / 32) + kh;
+                std::memcpy(chunk.data() + 1024 * slot, f2.data() + fr * 512, 1024);
+            }
+        if (slot > scale_slot) return false;
+        const size_t at = out.size();
+        out.resize(at + chunk.size() / 2);
+        std::memcpy(out.data() + at, chunk.data(), chunk.size());
+    }
+    return true;
+}
+
 // The resident kernel's stream of one layer (d_model D, feed-forward width F): per 32-feature
 // group og, the Q, K and V fragments of the group (part, k-step, row tile 2 og + hh), then the
 // out-projection's fragments at k-step og (row tile); per feed-forward chunk of 64 hidden units,
@@ -380,9 +500,11 @@ int decoder_validate_config(const pwd_geometry* g, const pwd_model_dims* m) {
         if (m->dtype == PWD_DTYPE_BF16 && m->d_model == 256)
             return fail(PWD_EUNSUPPORTED, "dilated convolutions at bf16 d_model 256 are switched off "
                                           "(GPU fault without a shown cause); use d_model 128");
+        if (m->dtype == PWD_DTYPE_MXFP8)
+            return fail(PWD_EUNSUPPORTED, "MXFP8 networks without the dilated convolutions only");
     }
     const int N = m->token_set == PWD_TOKENS_GRID ? (d + 1) * (d + 1) : d * d - 1;   // tokens
-    if (m->dtype == PWD_DTYPE_BF16) {
+    if (m->dtype == PWD_DTYPE_BF16 || m->dtype == PWD_DTYPE_MXFP8) {
         if (m->d_model != 128 && m->d_model != 256)
             return fail(PWD_EUNSUPPORTED, "bf16 d_model %d: need 128 or 256", m->d_model);
         if (dh != 16 && dh != 32 && dh != 64)
@@ -398,7 +520,7 @@ int decoder_validate_config(const pwd_geometry* g, const pwd_model_dims* m) {
         if (smem > 64 * 1024)
             return fail(PWD_EUNSUPPORTED, "fp32 window of %d tokens needs %zu bytes of LDS (max 65536)", N, smem);
     } else {
-        return fail(PWD_EUNSUPPORTED, "dtype %d: need 0 (fp32) or 1 (bf16)", m->dtype);
+        return fail(PWD_EUNSUPPORTED, "dtype %d: need 0 (fp32), 1 (bf16) or 2 (MXFP8)", m->dtype);
     }
     return PWD_OK;
 }
@@ -522,7 +644,8 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
     dec->mlp_ratio = dims->mlp_ratio;
     const size_t lf = layer_floats(D, F);
     const float* tail = w.data() + 2 * D + (size_t)L * lf;   // Wc, bc, w_o, b_o, beta
-    if (dims->dtype == PWD_DTYPE_BF16) {
+    const bool mx = dims->dtype == PWD_DTYPE_MXFP8;
+    if (dims->dtype != PWD_DTYPE_F32) {
         const int RT = D / 16;
         std::vector<float> s0((size_t)dec->nbw * RT * 64 * 4, 0.f);
         for (int s = 0; s < dec->ntok; ++s) {
@@ -554,10 +677,18 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
                 for (int r = 0; r < rep; ++r) bqkv[2 * D + rep * o + r] = bv[o];
             }
             std::vector<uint16_t> fr;
-            append_post_stream(fr, Wo, W1, W2, D, F, tok_mlp_chunk(D));
+            if (mx) {
+                if (!append_post_stream_mx(fr, Wo, W1, W2, D, F, tok_mlp_chunk(D), tok_mx_scale_slot())) {
+                    delete dec;
+                    return fail(PWD_EUNSUPPORTED, "MXFP8 feed-forward chunk layout does not fit");
+                }
+            } else {
+                append_post_stream(fr, Wo, W1, W2, D, F, tok_mlp_chunk(D));
+            }
             loff[l].post = put(fr.data(), fr.size() * 2);
             fr.clear();
-            append_qkv_stream(fr, wqkv.data(), D);
+            if (mx) append_qkv_stream_mx(fr, wqkv.data(), D, tok_mx_qkv_frags(), tok_mx_scale_slot());
+            else append_qkv_stream(fr, wqkv.data(), D);
             loff[l].qkv = put(fr.data(), fr.size() * 2);
             std::vector<float> pv;   // the token kernel's LDS vector table order
             for (const float* v : {bo, g1, be1, b2, g2, be2}) pv.insert(pv.end(), v, v + D);
@@ -638,7 +769,7 @@ int decoder_create(const pwd_geometry* geom, const pwd_model_dims* dims, const v
         dec->emb_tab = fptr(off_emb_tab);
     }
     dec->S0 = fptr(off_S0);
-    if (dims->dtype == PWD_DTYPE_BF16) {
+    if (dims->dtype != PWD_DTYPE_F32) {
         dec->we = fptr(off_we);
         dec->Wc = hptr(off_Wc);
         dec->bc = fptr(off_bc);
@@ -859,6 +990,7 @@ static int decode_impl(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* 
     tp.emb_nb = dec->emb_nb;
     tp.emb_tab = dec->emb_tab;
     const int RES = dec->emb_tab ? TOK_RESNET : 0;
+    const int MXF = dec->dtype == PWD_DTYPE_MXFP8 ? TOK_MX : 0;   // MXFP8 Q/K/V and W1
     tp.we = dec->we;
     auto set_post = [&](int l) {
         const auto& ly = dec->layers[l];
@@ -890,7 +1022,7 @@ static int decode_impl(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* 
     cp.nwin = (int)n;
     cp.zero = dec->zero;
     auto post = [&](int l, int flags, int stage) -> hipError_t {
-        if (!dec->dil[0]) return timed(dec, stage, s, [&] { return launch_tok(dec->D, dec->F, TOK_POST | flags, tp, n_tb, s); });
+        if (!dec->dil[0]) return timed(dec, stage, s, [&] { return launch_tok(dec->D, dec->F, TOK_POST | MXF | flags, tp, n_tb, s); });
         tp.G = act.G[0];
         hipError_t e = timed(dec, PWD_STAGE_OUT_PROJ, s, [&] { return launch_tok(dec->D, dec->F, TOK_WO, tp, n_tb, s); });
         for (int j = 0; j < 3 && e == hipSuccess; ++j) {
@@ -908,7 +1040,7 @@ static int decode_impl(pwd_decoder* dec, const uint32_t* d_meas, const uint8_t* 
     // round 0: embed (state D_0 = 0) and project layer 0
     tp.t = 0;
     set_qkv(0);
-    HIP_OK(timed(dec, PWD_STAGE_EMBED_QKV, s, [&] { return launch_tok(dec->D, dec->F, TOK_EMBED | TOK_QKV | RES, tp, n_tb, s); }));
+    HIP_OK(timed(dec, PWD_STAGE_EMBED_QKV, s, [&] { return launch_tok(dec->D, dec->F, TOK_EMBED | TOK_QKV | RES | MXF, tp, n_tb, s); }));
     for (int t = 0; t < dec->W; ++t) {
         const bool read_t = t >= dec->W - readouts;
         for (int l = 0; l < dec->L; ++l) {
@@ -952,7 +1084,7 @@ int decode_windows_noalloc(pwd_decoder* dec, const uint32_t* d_meas, const uint8
     const int rc = check_batch(dec, d_meas, d_types, n, d_logits, d_bits);
     if (rc != PWD_OK || n == 0) return rc;
     Activations act{nullptr, nullptr, nullptr, {nullptr, nullptr}};
-    if (dec->dtype == PWD_DTYPE_BF16) {
+    if (dec->dtype != PWD_DTYPE_F32) {
         // the same token-block rounding as the handle's buffers: every launch's grid fits
         const int64_t gran = tok_block_granule();
         const int64_t n_tb = (n * dec->nbw + gran - 1) / gran * gran;

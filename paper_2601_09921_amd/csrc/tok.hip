@@ -28,6 +28,19 @@
 // are software-pipelined in program order (a ring of fragments in flight ahead of the MFMAs).
 // Every fragment read from LDS feeds 2 MFMAs of each wavefront (one per 16-token block the
 // wavefront owns). Activations (X, Y, Q/K/V) are streamed with non-temporal accesses.
+//
+// With TOK_MX the Q/K/V projections and the feed-forward's first matrix run on MXFP8 operands
+// with v_mfma_scale_f32_16x16x128_f8f6f4 (OCP Microscaling: E4M3 elements, one E8M0 scale per
+// block of 32 reduction elements). That instruction pairs byte e of lane group g of A with
+// byte e of lane group g of B, and lane group kb supplies the scale of K block kb, which is made
+// of the first 16 bytes of lane groups 2 kb, 2 kb + 1 (kb < 2) or the last 16 bytes of lane
+// groups 2 (kb - 2), 2 (kb - 2) + 1. A token's activations are quantized where they sit, in the
+// C-fragment layout: lane (column n, group g) packs the 32 features 128 s + 16 r + 4 g + i
+// (r = 0..7, i = 0..3) of 128-feature slice s as bytes 4 r + i, so the blocks of a slice are
+// {16 r + 4 g + i : g in {2 p, 2 p + 1}, r in [4 h, 4 h + 4)} for block 2 h + p. A block's
+// largest magnitude takes one lane-pair exchange; its owner lane gets it with one more. The
+// weights are quantized by the host to the same blocks, one scale per output feature and
+// block, and each 32 KB chunk carries its fragments' scales in one 1 KB slot.
 #include "common.h"
 #include "kernels.h"
 #include "pipeline.h"
@@ -62,6 +75,21 @@ struct Shape {
     static constexpr int OG_PER_CHUNK = CHUNK / (2 * KS);
     static constexpr int POST_CHUNKS = WO_CHUNKS + MLP_CHUNKS;
     static_assert((CH / 16) * KS + RT * (CH / 32) == 32, "32 fragments per feed-forward sub-chunk");
+    // MXFP8 (TOK_MX): 8-bit fragments of 16 rows x 128 k (2 KB, two 1 KB halves = two reads).
+    // A feed-forward chunk holds the CH hidden units' W1 fragments (hidden row tile, k-step)
+    // followed by their bf16 W2 fragments, a Q/K/V chunk 12 fragments (output group, k-step,
+    // row tile); slot MX_SCALE_SLOT holds the chunk's weight scales, lane-major, byte j of a
+    // lane for 8-bit fragment j; the other slots are unused.
+    static constexpr int KS8 = D / 128;
+    static constexpr int MX_SCALE_SLOT = 24;
+    static constexpr int MX_NW1 = (CH / 16) * KS8;
+    static constexpr int MX_FFN_READS = 2 * MX_NW1 + RT * (CH / 32);
+    static constexpr int MX_QKV_FRAGS = 12;
+    static constexpr int MX_OPC = MX_QKV_FRAGS / (2 * KS8);   // output groups per Q/K/V chunk
+    static constexpr int MX_QKV_READS = 2 * MX_QKV_FRAGS;
+    static constexpr int MX_QKV_CHUNKS = (3 * D / 32) / MX_OPC;
+    static_assert(MX_FFN_READS == MX_SCALE_SLOT && MX_QKV_READS == MX_SCALE_SLOT, "data ahead of the scales");
+    static_assert((3 * D / 32) % MX_OPC == 0 && MX_NW1 <= 4 && MLP_PER == 1, "MXFP8 chunk layout");
     static_assert(NMLP % MLP_PER == 0, "whole feed-forward chunks");
     static_assert(RT * KS % CHUNK == 0 && (3 * D / 16) * KS % CHUNK == 0, "whole chunks");
 };
@@ -108,6 +136,98 @@ PWD_DEV f32x4 relu4(f32x4 v) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) r[i] = v[i] > 0.f ? v[i] : 0.f;
     return r;
+}
+
+typedef int i32x8 __attribute__((ext_vector_type(8)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// ---- MXFP8 (TOK_MX)
+// E8M0 scale of a block whose largest magnitude is m >= 0: 2^(floor(log2 m) - 8), 8 being the
+// exponent of E4M3's largest power of two, as a biased byte (floor(log2 m) + 127 is m's own
+// exponent field); 0 (2^-127) for m below 2^-119, zero included.
+PWD_DEV uint32_t mx_scale_byte(float m) {
+    const int e = (int)(__float_as_uint(m) >> 23) - 8;
+    return e > 0 ? (uint32_t)e : 0u;
+}
+// 1 / scale, exactly: 2^(127 - byte) for byte in [0, 247]
+PWD_DEV float mx_inv_scale(uint32_t byte) { return __uint_as_float((254u - byte) << 23); }
+// Four values to E4M3 bytes (round to nearest, ties to even). The conversion does not
+// saturate, so magnitudes are clamped to 448, E4M3's largest finite value, first.
+PWD_DEV uint32_t e4m3x4(float a, float b, float c, float d) {
+    const float lim = 448.f;
+    const int w = __builtin_amdgcn_cvt_pk_fp8_f32(__builtin_amdgcn_fmed3f(a, -lim, lim),
+                                                  __builtin_amdgcn_fmed3f(b, -lim, lim), 0, false);
+    return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(__builtin_amdgcn_fmed3f(c, -lim, lim),
+                                                     __builtin_amdgcn_fmed3f(d, -lim, lim), w, true);
+}
+
+// MXFP8 B (or A) operands of each token from its fp32 C fragments: q[s][b] holds slice s of
+// block b's token (bytes 4 r + i = feature 128 s + 16 r + 4 g + i), and byte b * KS8 + s of
+// `scales` the E8M0 scale of K block g of that slice (the block this lane's scale stands for).
+template <int RT, int TB>
+PWD_DEV void quantize_mx(const f32x4 (&x)[RT][TB], i32x8 (&q)[RT / 8][TB], uint32_t& scales, int g) {
+    constexpr int KS8 = RT / 8;
+    static_assert(KS8 * TB <= 4, "scale bytes fit one register");
+    scales = 0u;
+#pragma unroll
+    for (int b = 0; b < TB; ++b)
+#pragma unroll
+        for (int s = 0; s < KS8; ++s) {
+            // largest magnitudes of this lane's two halves (r < 4, r >= 4), then of the lane pair
+            // (groups 2 p, 2 p + 1) that forms each block
+            float mlo = 0.f, mhi = 0.f;
+#pragma unroll
+            for (int r = 0; r < 8; ++r)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float a = fabsf(x[8 * s + r][b][i]);
+                    if (r < 4) mlo = fmaxf(mlo, a);
+                    else mhi = fmaxf(mhi, a);
+                }
+            float o;
+            float t = swap16(mlo, o);
+            mlo = fmaxf(t, o);
+            t = swap16(mhi, o);
+            mhi = fmaxf(t, o);
+            // blocks of both pairs: *0 from groups {0, 1}, *1 from groups {2, 3}
+            float lo1, hi1;
+            const float lo0 = swap32(mlo, lo1);
+            const float hi0 = swap32(mhi, hi1);
+            const float owned = g == 0 ? lo0 : g == 1 ? lo1 : g == 2 ? hi0 : hi1;
+            scales |= mx_scale_byte(owned) << (8 * (b * KS8 + s));
+            const float ilo = mx_inv_scale(mx_scale_byte(mlo)), ihi = mx_inv_scale(mx_scale_byte(mhi));
+#pragma unroll
+            for (int r = 0; r < 8; ++r) {
+                const float inv = r < 4 ? ilo : ihi;
+                const f32x4 v = x[8 * s + r][b];
+                q[s][b][r] = (int)e4m3x4(v[0] * inv, v[1] * inv, v[2] * inv, v[3] * inv);
+            }
+        }
+}
+
+// An 8-bit fragment from its two 1 KB halves (bytes 0-15 and 16-31 of each lane).
+PWD_DEV i32x8 join_halves(const bf16x8& lo, const bf16x8& hi) {
+    const i32x4 a = __builtin_bit_cast(i32x4, lo), b = __builtin_bit_cast(i32x4, hi);
+    return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// D = scale_a scale_b (A B) + C on MXFP8 operands; byte ia of sa and byte ib of sb are the
+// E8M0 scales of this lane's A row / B column block. ia and ib fold to constants in the
+// unrolled callers (the instruction takes the byte selectors as immediates).
+template <int IA, int IB>
+PWD_DEV f32x4 mfma_mx_sel(const i32x8& a, const i32x8& b, f32x4 c, uint32_t sa, uint32_t sb) {
+    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, IA, (int)sa, IB, (int)sb);
+}
+PWD_DEV f32x4 mfma_mx(const i32x8& a, const i32x8& b, f32x4 c, uint32_t sa, int ia, uint32_t sb, int ib) {
+    switch (ia * 4 + ib) {
+#define PWD_MX_CASE(k) case k: return mfma_mx_sel<k / 4, k % 4>(a, b, c, sa, sb);
+        PWD_MX_CASE(0) PWD_MX_CASE(1) PWD_MX_CASE(2) PWD_MX_CASE(3) PWD_MX_CASE(4) PWD_MX_CASE(5)
+        PWD_MX_CASE(6) PWD_MX_CASE(7) PWD_MX_CASE(8) PWD_MX_CASE(9) PWD_MX_CASE(10) PWD_MX_CASE(11)
+        PWD_MX_CASE(12) PWD_MX_CASE(13) PWD_MX_CASE(14)
+#undef PWD_MX_CASE
+        default: return mfma_mx_sel<3, 3>(a, b, c, sa, sb);
+    }
 }
 
 // Look-ahead of the fragment reads (fragments in flight ahead of the MFMAs that use them);
@@ -227,6 +347,19 @@ constexpr int qkv_stores_after_last_load() {
     return n;
 }
 
+// The same for a Q/K/V chunk of the MXFP8 layout: its output group o2 is stored after read
+// (o2 + 1) * 4 KS8 - 1; groups of Q and K store TB fragments, groups of V 2 TB half-fragments
+// (one chunk may hold both kinds).
+template <int D, int NW, int LA>
+constexpr int mx_qkv_stores_after_last_load(int qc) {
+    using S = Shape<D, NW, 4>;
+    constexpr int LAST = WeightPipe<S::CHUNK, NW>::template last_load_read<S::MX_QKV_READS, LA>();
+    int n = 0;
+    for (int o2 = 0; o2 < S::MX_OPC; ++o2)
+        if ((o2 + 1) * 4 * S::KS8 - 1 + LA - 1 >= LAST) n += qc * S::MX_OPC + o2 >= 2 * S::KS ? 2 * TB : TB;
+    return n;
+}
+
 template <int D, int MR, int FLAGS>
 __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(TokParams p) {
     constexpr int WAVES = tok_waves<D, FLAGS>();
@@ -239,6 +372,9 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(To
     static_assert(!WO_ONLY || FLAGS == TOK_WO, "the out-projection-only launch stands alone");
     constexpr bool DO_WO = (FLAGS & TOK_POST) != 0 || WO_ONLY, DO_FFN = (FLAGS & TOK_POST) != 0 || FFN_ONLY;
     constexpr bool POST = DO_WO || DO_FFN, QKV = (FLAGS & TOK_QKV) != 0;
+    constexpr bool MX = (FLAGS & TOK_MX) != 0;
+    static_assert(!MX || (!WO_ONLY && !FFN_ONLY), "MXFP8 runs without the dilated convolutions");
+    constexpr int KS8 = S::KS8;
     constexpr int WO_CH = DO_WO ? S::WO_CHUNKS : 0, N_POST = WO_CH + (DO_FFN ? S::MLP_CHUNKS : 0);
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
@@ -251,7 +387,7 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(To
     pipe.post = DO_WO ? p.post_stream : p.post_stream + (size_t)S::WO_CHUNKS * CHUNK * FRAG;
     pipe.qkv = p.qkv_stream;
     pipe.n_post = N_POST;
-    pipe.total = pipe.n_post + (QKV ? S::QKV_CHUNKS : 0);
+    pipe.total = pipe.n_post + (QKV ? (MX ? S::MX_QKV_CHUNKS : S::QKV_CHUNKS) : 0);
     pipe.wave = __builtin_amdgcn_readfirstlane(wave);
     pipe.lane = lane;
 
@@ -325,7 +461,7 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(To
             const float* src = k < NP_V ? p.post_vecs + k * 64 : p.bqkv + (k - NP_V) * 64;
             const int dst = k < NP_V ? k * 64 : V::BQKV + (k - NP_V) * 64;
             // (inline assembly for the reason given at lds_load_1k)
-            asm volatile("global_load_lds_dword %0, %1" :: "v"((uint32_t)lane * 4), "s"(uniform_ptr(src)),
+            asm volatile(LDS_DMA_GUARD "global_load_lds_dword %0, %1" :: "v"((uint32_t)lane * 4), "s"(uniform_ptr(src)),
                          "{m0}"(lds_addr(vec + dst)) : "memory");
         }
     }
@@ -383,11 +519,17 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(To
             __syncthreads();
         }
         // ---- feed-forward, hidden units in chunks of CH; accumulators start at X + b_2
-        bf16x8 xb[KS][TB];
+        bf16x8 xb[MX ? 1 : KS][TB];
+        i32x8 xq[MX ? KS8 : 1][TB];   // MX: the LayerNorm output in MXFP8 ...
+        uint32_t sx = 0u;             // ... and its scales
+        if constexpr (MX) {
+            quantize_mx<RT, TB>(x, xq, sx, g);
+        } else {
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
+            for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-            for (int b = 0; b < TB; ++b) xb[ks][b] = pack_b(x[2 * ks][b], x[2 * ks + 1][b]);
+                for (int b = 0; b < TB; ++b) xb[ks][b] = pack_b(x[2 * ks][b], x[2 * ks + 1][b]);
+        }
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt) {
             const f32x4 bias = ld4(vec + V::B2 + rt * 16 + 4 * g);
@@ -440,11 +582,63 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(To
                 [&](int r) { pipe.template after_read<1 - PAR, MP * 32, LA>(nx, r); });
             sched_pipeline<MP * 32, TB, LA>();
         };
+        // MX: the chunk's MX_NW1 8-bit W1 fragments (hidden row tile, k-step; two reads each)
+        // against the quantized LayerNorm output, then its bf16 W2 fragments as above
+        auto mlp_chunk_mx = [&](auto par, int c) {
+            constexpr int PAR = decltype(par)::value;
+            constexpr int NR = S::MX_FFN_READS, NP1 = 2 * S::MX_NW1;
+            const int ci = WO_CH + c;
+            const uint16_t* buf = pipe.template sync<PAR, 0>(ci);
+            f32x4 h[CH / 16][TB];
+#pragma unroll
+            for (int rh = 0; rh < CH / 16; ++rh) {
+                const f32x4 bias = ld4(vec + V::B1 + c * CH + rh * 16 + 4 * g);
+#pragma unroll
+                for (int b = 0; b < TB; ++b) h[rh][b] = bias;
+            }
+            const uint32_t wsc = *reinterpret_cast<const uint32_t*>(buf + S::MX_SCALE_SLOT * FRAG + lane * 8);
+            const uint16_t* nx = pipe.next(ci);
+            __builtin_amdgcn_sched_barrier(0);
+            bf16x8 hb[CH / 32][TB];
+            bf16x8 half0;
+            pipelined<NR, LA>(
+                [&](int r) { return lds_frag(buf, r, lane); },
+                [&](int r, const bf16x8& a) {
+                    if (r < NP1) {
+                        if ((r & 1) == 0) {
+                            half0 = a;
+                            return;
+                        }
+                        const int j = r >> 1, rh = j / KS8, ks8 = j % KS8;
+                        const i32x8 w = join_halves(half0, a);
+#pragma unroll
+                        for (int b = 0; b < TB; ++b) h[rh][b] = mfma_mx(w, xq[ks8][b], h[rh][b], wsc, j, sx, b * KS8 + ks8);
+                        if (j == S::MX_NW1 - 1) {
+#pragma unroll
+                            for (int kh = 0; kh < CH / 32; ++kh)
+#pragma unroll
+                                for (int b = 0; b < TB; ++b)
+                                    hb[kh][b] = pack_b(relu4(h[2 * kh][b]), relu4(h[2 * kh + 1][b]));
+                        }
+                    } else {
+                        const int k = r - NP1, rt = k / (CH / 32), kh = k % (CH / 32);
+#pragma unroll
+                        for (int b = 0; b < TB; ++b) x[rt][b] = mfma16x16x32(a, hb[kh][b], x[rt][b]);
+                    }
+                },
+                [&](int r) { pipe.template after_read<1 - PAR, NR, LA>(nx, r); });
+            sched_pipeline_pairs<NR, TB, LA, NP1>();
+        };
         static_assert(S::MLP_CHUNKS % 2 == 0, "feed-forward chunks come in pairs");
         constexpr int P0 = WO_CH & 1;
         for (int c = 0; c < S::MLP_CHUNKS; c += 2) {
-            mlp_chunk(std::integral_constant<int, P0>{}, c);
-            mlp_chunk(std::integral_constant<int, 1 - P0>{}, c + 1);
+            if constexpr (MX) {
+                mlp_chunk_mx(std::integral_constant<int, P0>{}, c);
+                mlp_chunk_mx(std::integral_constant<int, 1 - P0>{}, c + 1);
+            } else {
+                mlp_chunk(std::integral_constant<int, P0>{}, c);
+                mlp_chunk(std::integral_constant<int, 1 - P0>{}, c + 1);
+            }
         }
         layer_norm<RT, TB>(x, vec + V::G2, vec + V::BE2, p.eps, g);
     }
@@ -492,7 +686,7 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(To
     };
 
     store_x();
-    if constexpr (QKV) {
+    if constexpr (QKV && !MX) {
         bf16x8 xb[KS][TB];
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
@@ -575,10 +769,91 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(To
         };
         static_for<S::QKV_CHUNKS>(qkv_chunk);
     }
+    if constexpr (QKV && MX) {
+        // MXFP8: the residual stream quantized per token, then per chunk MX_OPC output groups of
+        // 32 features, each KS8 k-steps x 2 row tiles of 8-bit fragments (two reads each);
+        // Q and K as in the bf16 path, V with the activations as the A operand. A chunk may
+        // hold groups of both kinds.
+        i32x8 xq[KS8][TB];
+        uint32_t sx;
+        quantize_mx<RT, TB>(x, xq, sx, g);
+        constexpr int NP = N_POST;
+        constexpr int OPC = S::MX_OPC;
+        constexpr int LA = LA_QKV;
+        constexpr int NR = S::MX_QKV_READS;
+        auto qkv_chunk = [&](auto qcc) {
+            constexpr int qc = decltype(qcc)::value;
+            constexpr int PAR = (NP + qc) & 1;
+            constexpr int YOUNGER = qc == 0 ? RT * TB : mx_qkv_stores_after_last_load<D, WAVES, LA>(qc - 1);
+            const uint16_t* buf = pipe.template sync<PAR, YOUNGER>(NP + qc);
+            f32x4 q[OPC][2][TB];
+#pragma unroll
+            for (int o2 = 0; o2 < OPC; ++o2)
+#pragma unroll
+                for (int hh = 0; hh < 2; ++hh) {
+                    const int og = qc * OPC + o2;
+                    f32x4 bias;
+                    if (og >= 2 * KS) {   // V: bias along the tile's columns
+                        const int o = (og - 2 * KS) * 32 + hh * 16 + col;
+                        if constexpr (V::REP == 4) {
+                            bias = ld4(vec + V::BV + o * 4);
+                        } else {
+                            const float bv = vec[V::BV + o];
+                            bias = f32x4{bv, bv, bv, bv};
+                        }
+                    } else {
+                        bias = ld4(vec + V::BQKV + og * 32 + hh * 16 + 4 * g);
+                    }
+#pragma unroll
+                    for (int b = 0; b < TB; ++b) q[o2][hh][b] = bias;
+                }
+            const u32x4 wsc = *reinterpret_cast<const u32x4*>(buf + S::MX_SCALE_SLOT * FRAG + lane * 8);
+            const uint16_t* nx = pipe.next(NP + qc);
+            __builtin_amdgcn_sched_barrier(0);
+            bf16x8 half0;
+            pipelined<NR, LA>(
+                [&](int r) { return lds_frag(buf, r, lane); },
+                [&](int r, const bf16x8& a) {
+                    if ((r & 1) == 0) {
+                        half0 = a;
+                        return;
+                    }
+                    // 8-bit fragment j = (o2 * KS8 + ks8) * 2 + hh
+                    const int j = r >> 1, hh = j & 1, ks8 = (j >> 1) % KS8, o2 = (j >> 1) / KS8;
+                    const int og = qc * OPC + o2;
+                    const bool vout = og >= 2 * KS;
+                    const i32x8 w = join_halves(half0, a);
+#pragma unroll
+                    for (int b = 0; b < TB; ++b) {
+                        if (vout) q[o2][hh][b] = mfma_mx(xq[ks8][b], w, q[o2][hh][b], sx, b * KS8 + ks8, wsc[j >> 2], j & 3);
+                        else q[o2][hh][b] = mfma_mx(w, xq[ks8][b], q[o2][hh][b], wsc[j >> 2], j & 3, sx, b * KS8 + ks8);
+                    }
+                    if (hh == 1 && ks8 == KS8 - 1) {
+#pragma unroll
+                        for (int b = 0; b < TB; ++b) {
+                            if (vout) {
+                                uint16_t* t = p.QKV + ((tb0 + b) * (3 * KS) + og) * FRAG + lane * 4;
+#pragma unroll
+                                for (int h2 = 0; h2 < 2; ++h2)
+                                    st_stream(reinterpret_cast<u16x4*>(t + h2 * (FRAG / 2)), to_bf16x4(q[o2][h2][b]));
+                            } else {
+                                const float sc = og < KS ? p.qscale : 1.0f;   // Q: log2(e)/sqrt(dh)
+                                stfrag(p.QKV, (tb0 + b) * (3 * KS) + og, lane,
+                                       pack_b(q[o2][0][b] * sc, q[o2][1][b] * sc));
+                            }
+                        }
+                    }
+                },
+                [&](int r) { pipe.template after_read<1 - PAR, NR, LA>(nx, r); });
+            sched_pipeline_pairs<NR, TB, LA, NR>();
+        };
+        static_for<S::MX_QKV_CHUNKS>(qkv_chunk);
+    }
     // The last chunk's reload into the idle buffer must land before the workgroup's LDS is
     // freed; the global stores issued after it need not.
-    constexpr int END_YOUNGER = QKV ? qkv_stores_after_last_load<CHUNK, WAVES, KS, LA_QKV, 2 * TB>()
-                                    : RT * TB + (WO_ONLY ? KS * TB : 0);
+    constexpr int END_YOUNGER = !QKV ? RT * TB + (WO_ONLY ? KS * TB : 0)
+                              : MX   ? mx_qkv_stores_after_last_load<D, WAVES, LA_QKV>(S::MX_QKV_CHUNKS - 1)
+                                     : qkv_stores_after_last_load<CHUNK, WAVES, KS, LA_QKV, 2 * TB>();
     asm volatile("s_waitcnt vmcnt(%0)" :: "n"(END_YOUNGER) : "memory");
 }
 
@@ -593,6 +868,19 @@ void launch_variant(const TokParams& p, int64_t n_tb, hipStream_t s) {
 template <int D, int MR>
 hipError_t launch_tok_d(int flags, const TokParams& p, int64_t n_tb, hipStream_t s) {
     switch (flags) {
+        // MXFP8 (no dilated convolutions)
+        case TOK_MX | TOK_EMBED | TOK_QKV: launch_variant<D, MR, TOK_MX | TOK_EMBED | TOK_QKV>(p, n_tb, s); break;
+        case TOK_MX | TOK_POST | TOK_QKV: launch_variant<D, MR, TOK_MX | TOK_POST | TOK_QKV>(p, n_tb, s); break;
+        case TOK_MX | TOK_POST | TOK_EMBED | TOK_QKV:
+            launch_variant<D, MR, TOK_MX | TOK_POST | TOK_EMBED | TOK_QKV>(p, n_tb, s);
+            break;
+        case TOK_MX | TOK_POST: launch_variant<D, MR, TOK_MX | TOK_POST>(p, n_tb, s); break;
+        case TOK_MX | TOK_EMBED | TOK_QKV | TOK_RESNET:
+            launch_variant<D, MR, TOK_MX | TOK_EMBED | TOK_QKV | TOK_RESNET>(p, n_tb, s);
+            break;
+        case TOK_MX | TOK_POST | TOK_EMBED | TOK_QKV | TOK_RESNET:
+            launch_variant<D, MR, TOK_MX | TOK_POST | TOK_EMBED | TOK_QKV | TOK_RESNET>(p, n_tb, s);
+            break;
         case TOK_EMBED | TOK_QKV: launch_variant<D, MR, TOK_EMBED | TOK_QKV>(p, n_tb, s); break;
         case TOK_POST | TOK_QKV: launch_variant<D, MR, TOK_POST | TOK_QKV>(p, n_tb, s); break;
         case TOK_POST | TOK_EMBED | TOK_QKV: launch_variant<D, MR, TOK_POST | TOK_EMBED | TOK_QKV>(p, n_tb, s); break;
@@ -793,6 +1081,9 @@ int tok_mlp_chunk(int D) { return 8192 / D; }
 
 // Copies of each V bias value in the Q/K/V bias table: [b_q b_k] then b_v, each value rep times.
 int tok_bv_rep(int D, int F) { return bv_rep(D, F); }
+
+int tok_mx_qkv_frags() { return Shape<256, 4, 4>::MX_QKV_FRAGS; }
+int tok_mx_scale_slot() { return Shape<256, 4, 4>::MX_SCALE_SLOT; }
 
 hipError_t launch_tok(int D, int F, int flags, const TokParams& p, int64_t n_tb, hipStream_t s) {
     if (n_tb <= 0) return hipSuccess;

@@ -18,7 +18,7 @@ HEADER = os.path.join(os.path.dirname(HERE), "include", "pwdec.h")
 
 PWD_OK, PWD_EINVAL, PWD_EUNSUPPORTED, PWD_EBLOB, PWD_ENOMEM, PWD_EHIP, PWD_EBATCH, PWD_EDEVICE = (
     0, -1, -2, -3, -4, -5, -6, -7)
-DTYPE_F32, DTYPE_BF16 = 0, 1
+DTYPE_F32, DTYPE_BF16, DTYPE_MXFP8 = 0, 1, 2
 BLOB_MAGIC = 0x31445750
 BLOB_VERSION = 1
 
@@ -186,6 +186,10 @@ class Decoder:
     def __init__(self, d: int, W: int, max_windows: int, D: int, L: int, H: int, mlp_ratio: int,
                  dtype: int, blob: bytes, token_set: int = TOKENS_STABILIZERS, embedder: int = EMBED_LINEAR,
                  dilations=(0, 0, 0)):
+        import torch
+        # torch's HIP runtime starts first: created the other way round (the library's HIP calls
+        # before torch initialises its device), torch then finds no GPU in this process
+        self.device = torch.cuda.current_device()   # decoder_create uses the current HIP device
         lib = load_library()
         self._lib = lib
         self.d, self.W, self.max_windows = d, W, max_windows
@@ -196,8 +200,6 @@ class Decoder:
         buf = ctypes.create_string_buffer(blob, len(blob))
         _check(lib.decoder_create(ctypes.byref(g), ctypes.byref(m), buf, len(blob), ctypes.byref(h)))
         self._h = h
-        import torch
-        self.device = torch.cuda.current_device()   # decoder_create uses the current HIP device
 
     @classmethod
     def from_workload(cls, wl, weights: dict, max_windows: int | None = None) -> "Decoder":

@@ -18,7 +18,7 @@ import numpy as np
 # Window types (Sec. 3.1 and App. A.1.1: initial, bulk and final decoding windows).
 WIN_INITIAL, WIN_BULK, WIN_FINAL = 0, 1, 2
 
-DTYPE_F32, DTYPE_BF16 = 0, 1
+DTYPE_F32, DTYPE_BF16, DTYPE_MXFP8 = 0, 1, 2
 
 
 @dataclasses.dataclass(frozen=True)
@@ -32,7 +32,9 @@ class Workload:
     p: Bernoulli probability of a detection event per (round, stabilizer).
     pair_p: probability per round of one extra correlated flip of a diagonal stabilizer pair.
     D, L, H, mlp_ratio: model width, layers, heads and MLP expansion.
-    dtype: DTYPE_F32 or DTYPE_BF16 (bf16 weights/activations, fp32 accumulation).
+    dtype: DTYPE_F32, DTYPE_BF16 (bf16 weights/activations, fp32 accumulation) or DTYPE_MXFP8
+       (as bf16, with the Q/K/V projections and the first feed-forward matrix on MXFP8
+       operands; the weights are drawn exactly as for bf16).
     grid: run the network over all (d+1)^2 cells of the stabilizer array instead of the
        d*d-1 stabilizers (inputs stay one bit per stabilizer).
     resnet: add the embedder's residual block of two Conv1d(D, D, kernel 3) over the
@@ -91,6 +93,11 @@ def input_seed(d: int) -> int:
 
 def with_batch(wl: Workload, B: int, **kw) -> Workload:
     return dataclasses.replace(wl, B=B, **kw)
+
+
+def mxfp8(wl: Workload) -> Workload:
+    """The same network and inputs with the MXFP8 projections."""
+    return dataclasses.replace(wl, name=wl.name + "_mxfp8", dtype=DTYPE_MXFP8)
 
 
 # ----------------------------------------------------------------------------- weights
@@ -154,7 +161,7 @@ def make_weights(wl: Workload, seed: int = WEIGHT_SEED, gain: float = 1.0) -> di
             lw["Wd"], lw["bd"] = mat(9 * D, (3, 3, 3, D, D)), bias((3, D))
     w["kappa"] = 0.707
     w["eps"] = 1e-5
-    if wl.dtype == DTYPE_BF16:
+    if wl.dtype in (DTYPE_BF16, DTYPE_MXFP8):
         w = map_tensors(w, round_bf16)
     else:
         w = map_tensors(w, lambda a: np.asarray(a, np.float32).astype(np.float64))

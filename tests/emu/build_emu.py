@@ -72,6 +72,8 @@ def rewrite_asm(text: str) -> str:
         open_i = m.end() - 1
         close_i = _matching(text, open_i)
         body = text[open_i + 1:close_i]
+        # the wait-state guard ahead of a direct-to-LDS load has no host meaning
+        body = re.sub(r'^\s*LDS_DMA_GUARD\s*', "", body)
         tmpl = re.match(r'\s*"([^"]*)"', body).group(1)
         if tmpl.startswith("s_waitcnt vmcnt"):
             call = "emu_waitcnt_vm(0)"

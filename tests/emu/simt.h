@@ -294,6 +294,76 @@ inline emu_f32x4 emu_amdgcn_mfma_f32_16x16x16bf16_1k(emu_bf16x4 a, emu_bf16x4 b,
     return emu_mfma_16x16<emu_bf16x4, 4>(a, b, c);
 }
 
+// ---- 8-bit floating point (MXFP8 path)
+typedef int emu_i32x8 __attribute__((ext_vector_type(8)));
+inline float emu_amdgcn_fmed3f(float a, float b, float c) { return std::fmax(std::fmin(a, b), std::fmin(std::fmax(a, b), c)); }
+// E4M3 (OCP FP8): value of a code, NaN for S.1111.111
+inline double emu_e4m3_value(unsigned code) {
+    const double sign = (code & 0x80) ? -1.0 : 1.0;
+    const int e = (code >> 3) & 15, m = code & 7;
+    if (e == 15 && m == 7) return NAN;
+    return e == 0 ? sign * std::ldexp((double)m, -9) : sign * std::ldexp(1.0 + m / 8.0, e - 7);
+}
+// v_cvt_pk_fp8_f32 as measured on gfx950: round to nearest, ties to even, on the E4M3 grid
+// extended by 480; results past 448 (480 and beyond) give the NaN code, no saturation.
+inline unsigned emu_e4m3_code(float f) {
+    const unsigned sign = std::signbit(f) ? 0x80u : 0u;
+    const double a = std::fabs((double)f);
+    if (std::isnan(a)) return sign | 0x7fu;
+    if (a < std::ldexp(1.0, -6)) return sign | (unsigned)std::nearbyint(std::ldexp(a, 9));
+    int e;
+    std::frexp(a, &e);
+    int E = e - 1;
+    if (E > 8) return sign | 0x7fu;
+    int q = (int)std::nearbyint((std::ldexp(a, -E) - 1.0) * 8.0);
+    if (q == 8) { q = 0; ++E; }
+    if (E > 8 || (E == 8 && q == 7)) return sign | 0x7fu;
+    return sign | (unsigned)(((E + 7) << 3) | q);
+}
+inline int emu_amdgcn_cvt_pk_fp8_f32(float a, float b, int old, bool hi) {
+    const unsigned w = emu_e4m3_code(a) | (emu_e4m3_code(b) << 8);
+    return hi ? (int)(((unsigned)old & 0xffffu) | (w << 16)) : (int)(((unsigned)old & 0xffff0000u) | w);
+}
+// v_mfma_scale_f32_16x16x128_f8f6f4 with E4M3 operands, as measured on gfx950: byte e of lane
+// group g of A (row l % 16) pairs with byte e of lane group g of B (column l % 16); those bytes
+// form K block kb = 2 (e / 16) + g / 2, whose E8M0 scales (byte opsel of the scale operand)
+// come from lane row + 16 kb of A and lane col + 16 kb of B.
+inline emu_f32x4 emu_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(emu_i32x8 a, emu_i32x8 b, emu_f32x4 c, int cbsz,
+                                                             int blgp, int opsel_a, int sa, int opsel_b, int sb) {
+    if (cbsz != 0 || blgp != 0) emu::report("mfma_scale: only E4M3 operands are emulated");
+    struct Op { emu_i32x8 v; unsigned s; };
+    // two exchanges (a slot holds 64 bytes): every lane's A operand and scale, then B's
+    const int lane = emu::g_cur->lane, col = lane & 15, g = lane >> 4;
+    Op A[64], Bv[64];
+    emu::xput(Op{a, ((unsigned)sa >> (8 * opsel_a)) & 0xffu});
+    emu::wave_sync();
+    for (int l = 0; l < 64; ++l) A[l] = emu::xget<Op>(l);
+    emu::xdone();
+    emu::xput(Op{b, ((unsigned)sb >> (8 * opsel_b)) & 0xffu}, 1);
+    emu::wave_sync();
+    for (int l = 0; l < 64; ++l) Bv[l] = emu::xget<Op>(l);
+    emu::xdone();
+    emu_f32x4 d;
+    for (int i = 0; i < 4; ++i) {
+        const int row = 4 * g + i;
+        double s = 0.0;
+        for (int gg = 0; gg < 4; ++gg) {
+            const Op& ar = A[row + 16 * gg];
+            const Op& bc = Bv[col + 16 * gg];
+            for (int e = 0; e < 32; ++e) {
+                const int kb = 2 * (e / 16) + gg / 2;
+                const unsigned ca = ((unsigned)ar.v[e / 4] >> (8 * (e % 4))) & 0xffu;
+                const unsigned cb = ((unsigned)bc.v[e / 4] >> (8 * (e % 4))) & 0xffu;
+                const double xa = std::ldexp(1.0, (int)A[row + 16 * kb].s - 127);
+                const double xb = std::ldexp(1.0, (int)Bv[col + 16 * kb].s - 127);
+                s += emu_e4m3_value(ca) * emu_e4m3_value(cb) * xa * xb;
+            }
+        }
+        d[i] = c[i] + (float)s;
+    }
+    return d;
+}
+
 // ---- the kernels' inline assembly, as rewritten by the source transformation
 inline uint32_t emu_lds_off(const void* p) {
     const char* c = static_cast<const char*>(p);

@@ -83,6 +83,16 @@ def check_logits(name, g, o):
     assert (err <= bound).all(), f"window {worst}: gpu {g[worst]!r} oracle {o[worst]!r}"
 
 
+def spread_sample(B, k):
+    """Windows spread over a batch of B beyond its first k: one per residue mod 8 at evenly
+    spaced positions (the readout runs one workgroup per window and workgroups go round-robin
+    over the 8 XCDs, so each XCD's share is represented; so are distant token-kernel tiles), and
+    the last two windows (the final, partly padded workgroup tiles of every kernel)."""
+    base = (k + 7) // 8 * 8
+    picks = {base + x * ((B - base) // 8) // 8 * 8 + x for x in range(8)} | {B - 2, B - 1}
+    return sorted(w for w in picks if k <= w < B)
+
+
 def check_bits(g_bits, o_logits):
     sel = np.abs(o_logits) > BIT_MARGIN
     if sel.sum() == 0:

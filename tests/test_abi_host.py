@@ -35,7 +35,8 @@ def test_workloads_are_supported(lib, wl):
 @pytest.mark.parametrize("kw", [
     dict(d=4), dict(d=1), dict(d=65), dict(d=37, W=37), dict(d=27, W=27, D=256, H=4),
     dict(W=6), dict(W=22), dict(B=0), dict(r=3), dict(r=6), dict(L=0),
-    dict(H=3), dict(D=96, H=6), dict(D=128, H=1), dict(D=256, H=2), dict(dt=2), dict(dt=0, D=256, H=8),
+    dict(H=3), dict(D=96, H=6), dict(D=128, H=1), dict(D=256, H=2), dict(dt=3), dict(dt=0, D=256, H=8),
+    dict(dt=2, D=64, H=4), dict(dt=2, ts=1, dil=(1, 2, 4)),
     dict(ts=2), dict(ts=-1), dict(ts=1, d=35, W=35), dict(emb=2), dict(emb=-1),
     dict(dil=(1, 2, 4)), dict(ts=1, dil=(1, 0, 2)), dict(ts=1, dil=(1, 2, 8)), dict(ts=1, dil=(-1, 1, 1)),
     dict(ts=1, D=256, H=8, dil=(1, 2, 4)),
@@ -54,6 +55,7 @@ def test_rejects_unsupported(lib, kw):
     dict(r=5), dict(r=5, d=25, W=50, D=256, H=8), dict(r=5, dt=0, d=3, W=6, D=64, H=4),
     dict(emb=1), dict(emb=1, ts=1, d=25, W=50, D=256, H=8), dict(emb=1, dt=0, d=3, W=6, D=64, H=4),
     dict(ts=1, dil=(1, 2, 4)), dict(ts=1, dil=(7, 7, 7)), dict(ts=1, dt=0, d=3, W=6, D=32, H=2, dil=(1, 2, 3)),
+    dict(dt=2), dict(dt=2, d=25, W=50, D=256, H=8), dict(dt=2, r=5), dict(dt=2, emb=1, ts=1, d=11, W=22, D=256, H=8),
 ])
 def test_supported_head_sizes(lib, kw):
     """Head sizes 16, 32 and 64 on the bf16 path (LDS for K and V of one head of 64 at
@@ -61,7 +63,7 @@ def test_supported_head_sizes(lib, kw):
     fits (d = 35, heads of 16 or 32: 155 KB; d = 37 and d = 27 with heads of 64 do not),
     the (d+1)^2 token set, whose tile is counted in grid tokens (d = 33: 1156 tokens fit,
     d = 35: 1296 do not), and feed-forward widths of 4 and 5 times d_model (3 and 6 are
-    rejected)."""
+    rejected), and the MXFP8 option (dt=2) on such networks without dilated convolutions."""
     assert validate(lib, **kw) == pwdec.PWD_OK
 
 

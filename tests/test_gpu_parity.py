@@ -6,11 +6,12 @@ the rest are checked through batch invariance and output consistency."""
 import copy
 import ctypes
 import math
+import os
 
 import numpy as np
 import pytest
 
-from gpu_helpers import (BF16_ATOL, check_bits, check_logits, decoder, gpu_decode, gpu_events,
+from gpu_helpers import (BF16_ATOL, spread_sample, check_bits, check_logits, decoder, gpu_decode, gpu_events,
                          inputs, oracle, say, weights)
 from oracle import decoder as O
 from paper_2601_09921_amd import pwdec, synth
@@ -153,16 +154,6 @@ def test_invalid_type_and_batch_limits(name):
     assert rc == pwdec.PWD_EBATCH
 
 
-def spread_sample(B, k):
-    """Windows spread over a batch of B beyond its first k: one per residue mod 8 at evenly
-    spaced positions (the readout runs one workgroup per window and workgroups go round-robin
-    over the 8 XCDs, so each XCD's share is represented; so are distant token-kernel tiles), and
-    the last two windows (the final, partly padded workgroup tiles of every kernel)."""
-    base = (k + 7) // 8 * 8
-    picks = {base + x * ((B - base) // 8) // 8 * 8 + x for x in range(8)} | {B - 2, B - 1}
-    return sorted(w for w in picks if k <= w < B)
-
-
 def test_spread_sample_covers_xcds_and_the_tail():
     for B, k in ((8192, 3), (4096, 4), (4096, 13), (1024, 97)):
         sample = spread_sample(B, k)
@@ -260,3 +251,25 @@ def test_attention_shift_underflow(name):
     say(f"  max |gpu - oracle| = {err.max():.3e}")
     assert (err <= BF16_ATOL).all(), (logits, o_logits)
     check_bits(bits, o_logits)
+
+
+def test_decoder_first_in_a_fresh_process():
+    """A process whose first GPU work is creating a decoder (before any torch.cuda call) can
+    decode: the binding starts torch's HIP runtime before the library's own calls."""
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    code = ("import numpy as np\n"
+            "from paper_2601_09921_amd import pwdec, synth\n"
+            "wl = synth.with_batch(synth.WORKLOADS['d7'], 4)\n"
+            "dec = pwdec.Decoder.from_workload(wl, synth.make_weights(wl))\n"
+            "import torch\n"
+            "meas, types = synth.make_windows(wl)\n"
+            "m = torch.from_numpy(np.ascontiguousarray(synth.pack_bits(meas)).view(np.int32)).cuda()\n"
+            "t = torch.from_numpy(types).cuda()\n"
+            "lg = torch.empty(4, device='cuda'); bt = torch.empty(4, dtype=torch.uint8, device='cuda')\n"
+            "dec.decode(m, t, lg, bt); torch.cuda.synchronize()\n"
+            "assert torch.isfinite(lg).all()\n"
+            "print('ok')\n")
+    r = subprocess.run([sys.executable, "-c", code], cwd=root, capture_output=True, text=True, timeout=110)
+    assert r.returncode == 0 and r.stdout.strip().endswith("ok"), r.stderr[-2000:]

@@ -1,4 +1,5 @@
-"""The hand-counted vector-memory waits of the kernels, checked on their compiled gfx950 code.
+"""The hand-counted vector-memory waits of the kernels, checked on their compiled gfx950 code,
+and the wait states ahead of their direct-to-LDS loads.
 
 The token, convolution and attention kernels stage weights and K/V with direct global->LDS
 loads and await them with `s_waitcnt vmcnt(N)`, where N counts the vector memory operations
@@ -10,6 +11,12 @@ runs a dataflow over every kernel's control-flow graph: per program point, the f
 memory operations issued since the newest direct-to-LDS load on any path into it. A wait
 vmcnt(k) completes that load iff the count is >= k. At every s_barrier and s_endpgm no direct
 load may remain possibly pending.
+
+The direct loads are inline assembly, so the compiler inserts no wait states for their operands.
+A vector instruction that writes an SGPR must be followed by 5 wait states before a vector
+memory instruction reads that SGPR (the load address), or the load reads the register's old
+value -- a load from the wrong address. Every direct load must therefore sit at least 5 wait
+states after the last vector write of its address registers on the straight-line path before it.
 """
 import os
 import re
@@ -99,6 +106,44 @@ def check(insts) -> list[str]:
     return problems
 
 
+SREG = re.compile(r"^s\[(\d+):(\d+)\]$|^s(\d+)$")
+
+
+def sregs(tok: str) -> set:
+    m = SREG.match(tok.strip().rstrip(","))
+    if not m:
+        return set()
+    if m.group(3) is not None:
+        return {int(m.group(3))}
+    return set(range(int(m.group(1)), int(m.group(2)) + 1))
+
+
+def sgpr_hazards(insts, need_states: int = 5) -> list[str]:
+    """Direct-to-LDS loads closer than need_states wait states to a vector write of one of
+    their SGPR operands (scanning back along the instruction stream)."""
+    problems = []
+    for i, (a, mn, ops, _) in enumerate(insts):
+        if not DMA.match(mn):
+            continue
+        need = set()
+        for t in ops.split(",")[1:]:
+            if t.strip():
+                need |= sregs(t.split()[0])
+        states = 0
+        for j in range(i - 1, max(i - 16, -1), -1):
+            _, pm, pops, _ = insts[j]
+            if pm == "s_nop":
+                states += int(pops.split()[0]) + 1
+                continue
+            if states >= need_states:
+                break
+            if pm.startswith("v_") and pops and sregs(pops.split(",")[0]) & need:
+                problems.append(f"{pm} {pops} at {states} wait states before {mn} {ops} at 0x{a:x}")
+                break
+            states += 1
+    return problems
+
+
 def objects():
     if not os.path.isdir(OBJDIR):
         return []
@@ -115,6 +160,24 @@ def test_direct_lds_loads_complete_before_barriers(obj, tmp_path):
         assert any(DMA.match(mn) for insts in funcs.values() for _, mn, _, _ in insts)
     bad = {name: p for name, insts in funcs.items() if (p := check(insts))}
     assert not bad, bad
+
+
+@pytest.mark.parametrize("obj", objects(), ids=[os.path.basename(o) for o in objects()])
+def test_direct_lds_load_addresses_are_settled(obj, tmp_path):
+    if not os.path.exists(f"{LLVM}/llvm-objdump"):
+        pytest.skip("ROCm LLVM tools not found")
+    funcs = functions(disassemble(obj, tmp_path))
+    bad = {name: p for name, insts in funcs.items() if (p := sgpr_hazards(insts))}
+    assert not bad, bad
+
+
+def test_the_address_check_catches_a_fresh_sgpr():
+    """A planted mistake: the load's address register written by v_readfirstlane just before."""
+    insts = [(0, "v_readfirstlane_b32", "s20, v144", None), (4, "v_readfirstlane_b32", "s21, v145", None),
+             (8, "global_load_lds_dwordx4", "v98, s[20:21]", None)]
+    assert sgpr_hazards(insts)
+    insts.insert(2, (6, "s_nop", "4", None))
+    assert not sgpr_hazards(insts)
 
 
 def test_the_check_catches_a_missing_wait():
