@@ -148,7 +148,7 @@ size_t decoder_blob_floats(const pwd_geometry* geom, const pwd_model_dims* dims)
  * 1 <= max_windows <= 2^24; mlp_ratio 4 or 5; n_layers 1..8;
  * token_set PWD_TOKENS_STABILIZERS or PWD_TOKENS_GRID (n_tokens = d*d-1 or (d+1)^2);
  * embedder PWD_EMBED_LINEAR or PWD_EMBED_RESNET; conv_dilation all 0, or all in 1..distance
- * with PWD_TOKENS_GRID (bf16: d_model 128 only for now);
+ * with PWD_TOKENS_GRID;
  * PWD_DTYPE_MXFP8: as PWD_DTYPE_BF16, without the dilated convolutions;
  * PWD_DTYPE_BF16: d_model in {128, 256}, head size d_model/n_heads in {16, 32, 64}, and the
  * attention tile (K and V of one head: (2 ceil(n_tokens/16) + 1) KB, twice that for head size

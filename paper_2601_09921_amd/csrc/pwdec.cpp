@@ -494,12 +494,6 @@ int decoder_validate_config(const pwd_geometry* g, const pwd_model_dims* m) {
                             m->conv_dilation[j], d);
         if (m->token_set != PWD_TOKENS_GRID)
             return fail(PWD_EUNSUPPORTED, "dilated convolutions need the grid token set (every cell a token)");
-        // Switched off: the first run of this configuration ended in a GPU memory fault and no
-        // cause has been shown (a CPU replay of its launches stays inside every allocation and
-        // the waits check out; d_model 128 and the fp32 path pass their parity tests).
-        if (m->dtype == PWD_DTYPE_BF16 && m->d_model == 256)
-            return fail(PWD_EUNSUPPORTED, "dilated convolutions at bf16 d_model 256 are switched off "
-                                          "(GPU fault without a shown cause); use d_model 128");
         if (m->dtype == PWD_DTYPE_MXFP8)
             return fail(PWD_EUNSUPPORTED, "MXFP8 networks without the dilated convolutions only");
     }

@@ -32,16 +32,15 @@ SHAPES = [
     (13, 13, 3, 256, 1, 4, 5, BF16, True, (1, 3, 5)),
     (25, 25, 2, 256, 1, 8, 4, BF16, False, (1, 2, 4)),
 ]
-# d_model 256 is switched off in the library: its first GPU run ended in a memory fault and no
-# cause has been shown (the CPU replay of the case in tests/test_emu_host.py stays in bounds and
-# matches the oracle; the wait counts check out on the compiled code). These cases stay skipped
-# until a cause is shown and fixed.
-D256_OFF = "dilated convolutions at bf16 d_model 256 are switched off: GPU fault without a shown cause"
+# d_model 256: the first GPU run of these cases ended in a memory fault. The cause, shown on the
+# compiled code: conv_kernel<256> issued a direct-to-LDS load right after the v_readfirstlane
+# that wrote its address register, without the wait states the hardware requires, so the load
+# could use a stale address. The loads now carry those wait states and tests/test_wait_counts.py
+# checks every kernel for the pattern.
 
 
 def cases(shapes):
-    return [pytest.param(*s, id=i, marks=[pytest.mark.skip(reason=D256_OFF)] if s[3] == 256 else [])
-            for s, i in zip(shapes, ids(shapes))]
+    return [pytest.param(*s, id=i) for s, i in zip(shapes, ids(shapes))]
 
 
 @pytest.fixture(scope="module", autouse=True)
