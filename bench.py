@@ -129,6 +129,67 @@ def workload_line(name, torch, pwdec, synth, reps=3):
     return out
 
 
+def mxfp8_measurement(torch, pwdec, synth, names=("d7", "d11", "d25"), reps=3):
+    """The MXFP8 option (Q/K/V projections and the first feed-forward matrix on E4M3 operands with
+    E8M0 block scales, the rest as bf16) on the full batch of each workload, against the bf16
+    decoder of the same network and inputs on the same launch schedule (layer-phased; the only one
+    MXFP8 runs on) and on bf16's default schedule. Reported separately from the bf16 headline."""
+    out = {}
+    for name in names:
+        base = synth.WORKLOADS[name]
+        weights = synth.make_weights(base)
+        meas, types = synth.make_windows(base)
+        dev_meas = torch.from_numpy(synth.pack_bits(meas).view(np.int32)).cuda()
+        dev_types = torch.from_numpy(types).cuda()
+        del meas
+        logits = torch.empty(base.B, dtype=torch.float32, device="cuda")
+        bits = torch.empty(base.B, dtype=torch.uint8, device="cuda")
+        stream = torch.cuda.current_stream()
+        flops, step_flops = stage_flops(base, base.B)
+        N, D, F = base.N, base.D, base.F
+        fp8_share = (6 * N * D * D + 2 * N * D * F) / (6 * N * D * D + 4 * N * N * D + 2 * N * D * D + 4 * N * D * F)
+
+        def timed(dec, sched):
+            dec.schedule(sched)
+            dec.decode(dev_meas, dev_types, logits, bits, stream)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                dec.decode(dev_meas, dev_types, logits, bits, stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / reps
+            dec.profile(True)
+            dec.decode(dev_meas, dev_types, logits, bits, stream)
+            torch.cuda.synchronize()
+            stages = dec.profile_read()
+            dec.profile(False)
+            assert np.isfinite(logits.cpu().numpy()).all()
+            return ms, stages
+
+        mx = pwdec.Decoder.from_workload(synth.mxfp8(base), weights)
+        ms_mx, st_mx = timed(mx, pwdec.SCHEDULE_LAYERS)
+        mx.close()
+        bf = pwdec.Decoder.from_workload(base, weights)
+        ms_bf, _ = timed(bf, pwdec.SCHEDULE_LAYERS)
+        ms_auto, _ = timed(bf, pwdec.SCHEDULE_AUTO)
+        bf.close()
+        tb = transformer_blocks(st_mx, flops, 1)
+        out[name] = {
+            "workload": f"{base.name}: d={base.d}, {N} tokens, {base.W}-round windows, {base.B} windows, D={D}, "
+                        f"{base.L} layers, {base.H} heads, Q/K/V and W1 in MXFP8",
+            "ms_per_decode": round(ms_mx, 3), "us_per_round": ms_mx * 1e3 / (base.B * base.d),
+            "rounds_per_s": base.B * base.d / (ms_mx * 1e-3),
+            "fp8_flop_share": round(fp8_share, 3),
+            "transformer_blocks": tb,
+            "kernel_ms": {k: round(v[0], 3) for k, v in st_mx.items()},
+            "bf16_layers_ms_per_decode": round(ms_bf, 3), "speedup_vs_bf16_layers": round(ms_bf / ms_mx, 3),
+            "bf16_default_ms_per_decode": round(ms_auto, 3), "speedup_vs_bf16_default": round(ms_auto / ms_mx, 3),
+        }
+    return out
+
+
 def source_hash():
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2601_09921_amd", "csrc")
@@ -451,6 +512,7 @@ def main():
         out["paper_variant"] = paper_variant_measurement(wl, torch, pwdec, synth, dev_meas, dev_types)
     if not args.no_extra:
         out["workloads"] = {n: workload_line(n, torch, pwdec, synth) for n in EXTRA_WORKLOADS if n != wl.name}
+        out["mxfp8"] = mxfp8_measurement(torch, pwdec, synth)
     if args.cpu_sample > 0:
         out["cpu_baseline"] = cpu_baseline(wl, weights, args.cpu_sample)
     print(json.dumps(out), flush=True)
