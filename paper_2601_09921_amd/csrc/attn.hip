@@ -6,18 +6,20 @@
 // which serve as A fragments of K; V as 16x16 tiles with tokens as rows, whose per-lane
 // halves of two key blocks form an A fragment of V^T); the wavefronts then split the
 // 16-query blocks and stream the keys in steps of 32:
-//   S^T = K Q'^T - m      (16 keys x 16 queries per MFMA, lanes hold queries)
+//   S^T = K Q'^T          (16 keys x 16 queries per MFMA, lanes hold queries)
 //   P^T = exp2(S^T)       (P^T is the S^T accumulator rounded to bf16, no shuffle)
 //   O^T += V^T P^T,  l += 1^T P^T
 // Q' = Q log2(e)/sqrt(dh) comes pre-scaled from the Q/K/V projection, so S is in log2 units.
-// The shift m of a query is the Cauchy-Schwarz bound |q'| max_k |k| >= every score of the
-// row; softmax is shift-invariant, so this is the exact softmax without a running maximum
-// or rescaling, and m enters as the initial value of the MFMA accumulator. Should a row's
-// sum underflow (a bound far above the true maximum), that query block is recomputed with
-// the running-maximum form. Padding keys (index >= N) get probability 0. The row sums l come
-// from the matrix core too: an A fragment whose row 0 is all ones turns P^T into its column
-// sums, so numerator and denominator use the same bf16 probabilities and the VALU is left to
-// the exponentials. The output is written as the B fragments the out-projection consumes.
+// Softmax is shift-invariant, so the scores are exponentiated as they are: with fp32
+// exponentials, bf16 probabilities and fp32 sums this is the exact softmax (up to rounding)
+// whenever every probability and partial sum stays in the normal fp32 range, which a score
+// range of about +-100 log2 units guarantees. A query block whose row sum or output leaves
+// that range (inf, NaN, or a sum below 1e-30) is recomputed with the running-maximum form,
+// so no input is out of reach; the common case spends no VALU work on a shift. Padding keys
+// (index >= N) get probability 0. The row sums l come from the matrix core too: an A
+// fragment whose row 0 is all ones turns P^T into its column sums, so numerator and
+// denominator use the same bf16 probabilities and the VALU is left to the exponentials. The
+// output is written as the B fragments the out-projection consumes.
 //
 // One workgroup of 1, 2 or 4 wavefronts (by window size) per item, two workgroups per CU:
 // while one copies its K/V, the other keeps the SIMDs busy.
@@ -29,7 +31,6 @@ namespace {
 #ifndef ATTN_WIDE
 #define ATTN_WIDE 1
 #endif
-constexpr int KMAX_UNROLL = 8;        // key blocks per step of the max |k| scan
 
 PWD_DEV float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
@@ -94,7 +95,7 @@ struct AttnShape {
     int N, nbw, KSD;   // real tokens, 16-token blocks, Q/K/V fragments per token block
 };
 
-// One (window, head) item: its K/V in LDS, its Q, K and Y in HBM, and max |k|.
+// One (window, head) item: its K/V in LDS, its Q, K and Y in HBM.
 struct AttnItem {
     const uint16_t* ks;   // LDS [nbw][NF][512] K fragments
     const uint16_t* vs;   // LDS [nbw + 1][NF][512] V tiles (+ a zero block when nbw is odd)
@@ -102,7 +103,6 @@ struct AttnItem {
     const uint16_t* k0;   // first K fragment of token block 0 (V follows at + KSD fragments)
     uint16_t* y0;         // first Y fragment of token block 0; block stride KSD fragments
     int slot0, vhalf;     // this head's slots inside a fragment (dh = 16 packs two heads)
-    float kmax;
 };
 
 template <int DH>
@@ -117,7 +117,6 @@ PWD_DEV AttnItem make_item(const AttnParams& p, const AttnShape& sh, int item) {
     it.y0 = p.Y + (tb_base * sh.KSD + frag) * 512;
     it.slot0 = DH == 16 ? (h % 2) * 4 : 0;
     it.vhalf = DH == 16 ? h % 2 : 0;
-    it.kmax = 0.f;
     return it;
 }
 
@@ -144,49 +143,6 @@ PWD_DEV void stage_kv(const AttnShape& sh, const uint16_t* k0, uint16_t* ks, uin
             lds_load_1k(uniform_ptr(src), lds_addr(ks + (kb * NF + f) * 512), lane);
             lds_load_1k(uniform_ptr(src + (size_t)sh.KSD * 512), lds_addr(vs + (kb * NF + f) * 512), lane);
         }
-}
-
-// max |k|^2 over the real keys of blocks kb0, kb0 + stride, ..., reduced over the wavefront;
-// KMAX_UNROLL blocks at a time so their LDS reads and cross-lane sums are in flight together.
-// Blocks past the last are skipped (the tests are wavefront-uniform).
-template <int DH>
-PWD_DEV float kmax2_blocks(const AttnShape& sh, const uint16_t* ks, int slot0, int kb0, int stride, int lane) {
-    constexpr int NV = Frag<DH>::NV, NF = Frag<DH>::NF;
-    const int col = lane & 15;
-    float kmax2 = 0.f;
-    for (int kbs = kb0; kbs < sh.nbw; kbs += KMAX_UNROLL * stride) {
-        float n2[KMAX_UNROLL];
-#pragma unroll
-        for (int u = 0; u < KMAX_UNROLL; ++u) {
-            const int kb = kbs + u * stride;
-            n2[u] = 0.f;
-            if (kb < sh.nbw) {
-#pragma unroll
-                for (int fr = 0; fr < NF; ++fr) {
-                    const u16x8 kv = *reinterpret_cast<const u16x8*>(ks + ((kb * NF + fr) * 64 + lane) * 8);
-#pragma unroll
-                    for (int i = 0; i < NV; ++i) {
-                        const float f = (float)__builtin_bit_cast(__bf16, (uint16_t)kv[slot0 + i]);
-                        n2[u] = fmaf(f, f, n2[u]);
-                    }
-                }
-            }
-        }
-#pragma unroll
-        for (int u = 0; u < KMAX_UNROLL; ++u)
-            if (kbs + u * stride < sh.nbw) n2[u] += __shfl_xor(n2[u], 16);
-#pragma unroll
-        for (int u = 0; u < KMAX_UNROLL; ++u)
-            if (kbs + u * stride < sh.nbw) n2[u] += __shfl_xor(n2[u], 32);
-#pragma unroll
-        for (int u = 0; u < KMAX_UNROLL; ++u) {
-            const int kb = kbs + u * stride;
-            if (kb < sh.nbw && kb * 16 + col < sh.N) kmax2 = fmaxf(kmax2, n2[u]);
-        }
-    }
-#pragma unroll
-    for (int off = 1; off < 16; off <<= 1) kmax2 = fmaxf(kmax2, __shfl_xor(kmax2, off));
-    return kmax2;
 }
 
 // Scheduling request for one iteration of the key loop (two superblocks, NMFMA MFMAs): each
@@ -217,21 +173,13 @@ PWD_DEV void attn_pass(const AttnShape& sh, const AttnItem& it, int qb0, int qen
     const uint16_t* vs = it.vs;
 
     FT q[QB][NF];
-    f32x4 shift[QB];
 #pragma unroll
-    for (int j = 0; j < QB; ++j) {
-        float n2 = 0.f;
+    for (int j = 0; j < QB; ++j)
 #pragma unroll
         for (int f = 0; f < NF; ++f)
 #pragma unroll
-            for (int i = 0; i < NV; ++i) {
-                const float x = (float)__builtin_bit_cast(__bf16, (uint16_t)qv[j][f][slot0 + i]);
-                n2 = fmaf(x, x, n2);
-                q[j][f][i] = __builtin_bit_cast(__bf16, (uint16_t)qv[j][f][slot0 + i]);
-            }
-        const float m = sqrtf(sum4(n2)) * it.kmax;
-        shift[j] = f32x4{-m, -m, -m, -m};
-    }
+            for (int i = 0; i < NV; ++i) q[j][f][i] = __builtin_bit_cast(__bf16, (uint16_t)qv[j][f][slot0 + i]);
+    const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
 
     f32x4 o[QB][RT];
     f32x4 ls[QB];     // row 0 (lanes 0-15, element 0): sum of P over the keys
@@ -244,7 +192,7 @@ PWD_DEV void attn_pass(const AttnShape& sh, const AttnItem& it, int qb0, int qen
 
     // V^T tile rt: half rt % 2 of fragment rt / 2 (dh = 16: this head's half of fragment 0)
     auto vtile = [&](int rt, int sb) { return ld_vfrag<NF>(vs, DH == 16 ? 0 : rt / 2, DH == 16 ? it.vhalf : rt % 2, sb, lane); };
-    // S^T - m of key block kb for query block j: NF k-steps over the head's features
+    // S^T of key block kb for query block j: NF k-steps over the head's features
     auto score = [&](const FT (&kf)[NF], int j, f32x4 init) {
         f32x4 acc = Frag<DH>::mma(kf[0], q[j][0], init);
 #pragma unroll
@@ -264,12 +212,12 @@ PWD_DEV void attn_pass(const AttnShape& sh, const AttnItem& it, int qb0, int qen
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt) vf[rt] = vtile(rt, sb);
     };
-    // S^T - m of one superblock for every query block
+    // S^T of one superblock for every query block
     auto scores = [&](const FT (&kf)[2][NF], f32x4 (&s)[QB][2]) {
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-            for (int j = 0; j < QB; ++j) s[j][kk] = score(kf[kk], j, shift[j]);
+            for (int j = 0; j < QB; ++j) s[j][kk] = score(kf[kk], j, zero);
     };
     // P = exp2(S), row sums, and O^T += V^T P^T for one superblock
     auto accumulate = [&](const f32x4 (&s)[QB][2], const bf16x8 (&vf)[RT]) {
@@ -325,7 +273,7 @@ PWD_DEV void attn_pass(const AttnShape& sh, const AttnItem& it, int qb0, int qen
 #pragma unroll
                 for (int f = 0; f < NF; ++f) a[f] = ld_kfrag<DH>(ks, kb, f, lane, slot0);
 #pragma unroll
-                for (int j = 0; j < QB; ++j) s[j][kk] = score(a, j, shift[j]);
+                for (int j = 0; j < QB; ++j) s[j][kk] = score(a, j, zero);
             } else {
 #pragma unroll
                 for (int j = 0; j < QB; ++j) s[j][kk] = f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
@@ -346,12 +294,18 @@ PWD_DEV void attn_pass(const AttnShape& sh, const AttnItem& it, int qb0, int qen
     for (int j = 0; j < QB; ++j) {
         const int qb = qb0 + j;
         float lt = __shfl(ls[j][0], col);   // row 0 of the sums lives in lane col
-        // underflowed row sums: redo this block with a running maximum (wave-uniform)
-        if (__builtin_amdgcn_ballot_w64(lt < 1e-30f) != 0) {
+        // x * 0 is 0 for finite x and NaN for inf or NaN: chk is lt unless an output is not finite
+        float chk = lt;
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) chk = fmaf(o[j][rt][i], 0.f, chk);
+        // a row sum below 1e-30, above 2^126, or a non-finite output: redo this block with a
+        // running maximum (wave-uniform)
+        if (__builtin_amdgcn_ballot_w64(!(chk >= 1e-30f && chk <= 0x1p126f)) != 0) {
             float mm = -INFINITY, ll = 0.f;
 #pragma unroll
             for (int rt = 0; rt < RT; ++rt) o[j][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-            const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
             for (int sb = 0; sb < nsb; ++sb) {
                 f32x4 s2[2];
                 for (int kk = 0; kk < 2; ++kk) {
@@ -387,8 +341,9 @@ PWD_DEV void attn_pass(const AttnShape& sh, const AttnItem& it, int qb0, int qen
             lt = sum4(ll);
         }
         if (qb >= qend) continue;
-        const float inv = 1.0f / lt;
-        uint16_t* dst = it.y0 + (size_t)qb * sh.KSD * 512 + lane * 8;
+        // v_rcp_f32 (1 ulp) rather than a correctly rounded division: the outputs are bf16
+        const float inv = __builtin_amdgcn_rcpf(lt);
+        uint16_t* dst = it.y0 + (uint32_t)(qb * sh.KSD * 512 + lane * 8);   // 32-bit offset in the item
         if constexpr (DH == 16) {
             u16x4 out;
 #pragma unroll
@@ -458,7 +413,6 @@ __global__ __launch_bounds__(WAVES * 64, WAVES == 8 ? 1 : 2) void attn_kernel(At
     extern __shared__ __align__(16) unsigned char smem[];
     uint16_t* ks = reinterpret_cast<uint16_t*>(smem);   // [nbw][NF][512]: K fragments
     uint16_t* vs = ks + (size_t)nbw * NF * 512;          // [nbw + 1][NF][512]: V tiles, + a zero block
-    __shared__ float kmax_w[WAVES];
     constexpr int HPI = heads_per_item<DH>();
     AttnItem it = make_item<DH>(p, sh, blockIdx.x * HPI);   // the pair's first head
     it.ks = ks;
@@ -478,33 +432,13 @@ __global__ __launch_bounds__(WAVES * 64, WAVES == 8 ? 1 : 2) void attn_kernel(At
             reinterpret_cast<uint32_t*>(vs + (size_t)nbw * NF * 512)[i] = 0u;
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-    if constexpr (HPI == 1) {
-        const float kw = kmax2_blocks<DH>(sh, ks, it.slot0, wave, WAVES, lane);
-        if (lane == 0) kmax_w[wave] = kw;
-        __syncthreads();
-        float kmax2 = 0.f;
-#pragma unroll
-        for (int w = 0; w < WAVES; ++w) kmax2 = fmaxf(kmax2, kmax_w[w]);
-        it.kmax = sqrtf(kmax2);
-        if (qbeg < qend) attn_passes<DH>(sh, it, qbeg, qend, qnext, ones_row(lane), lane);
-    } else {
-        // both heads of the pair in turn: each its slots of the same fragments and its own
-        // max |k| (the second reloads its Q after a barrier that retires the first's kmax_w)
-        for (int hh = 0; hh < 2; ++hh) {
-            if (hh > 0) {
-                it.slot0 += 4;
-                it.vhalf += 1;
-                if (qbeg < qend) load_q<NF, QM>(sh, it.q0, qbeg, qend, lane, qnext);
-                __syncthreads();
-            }
-            const float kw = kmax2_blocks<DH>(sh, ks, it.slot0, wave, WAVES, lane);
-            if (lane == 0) kmax_w[wave] = kw;
-            __syncthreads();
-            float kmax2 = 0.f;
-#pragma unroll
-            for (int w = 0; w < WAVES; ++w) kmax2 = fmaxf(kmax2, kmax_w[w]);
-            it.kmax = sqrtf(kmax2);
-            if (qbeg < qend) attn_passes<DH>(sh, it, qbeg, qend, qnext, ones_row(lane), lane);
+    if (qbeg < qend) {
+        attn_passes<DH>(sh, it, qbeg, qend, qnext, ones_row(lane), lane);
+        if constexpr (HPI == 2) {   // the pair's second head: its slots of the same fragments
+            it.slot0 += 4;
+            it.vhalf += 1;
+            load_q<NF, QM>(sh, it.q0, qbeg, qend, lane, qnext);
+            attn_passes<DH>(sh, it, qbeg, qend, qnext, ones_row(lane), lane);
         }
     }
 }

@@ -189,44 +189,48 @@ def test_full_batch_sampled(name):
         assert one.view(np.uint32)[0] == logits.view(np.uint32)[w], f"window {w}"
 
 
-def orthogonal_qk_weights(wl, w, scale=12.0):
-    """Weights whose Q and K of every head live in disjoint halves of the head's features (Q
-    in the first, K in the second, biases included), scaled up: every attention score is
-    exactly 0 while |q'| max|k| is hundreds of log2 units."""
+def constant_score_weights(wl, w, sign, beta=32.0):
+    """Weights under which every attention score of every head is the same number, far outside
+    the range the kernel exponentiates directly: Q of a head is the bias beta on the head's
+    first feature (zero elsewhere), and K has exactly sign * beta on that feature (its column
+    of Wk zeroed), whatever it holds on the others. So q'.k = sign * beta^2 log2(e)/sqrt(dh)
+    for every pair (beta = 32: at least 184 log2 units for heads of 16 to 64 features), all
+    scores of a row are equal and the softmax is uniform."""
     w = copy.deepcopy(w)
     dh = wl.D // wl.H
     for lw in w["layers"]:
-        Wq, Wk, bq, bk = lw["Wq"] * scale, lw["Wk"] * scale, lw["bq"].copy(), lw["bk"].copy()
+        Wq, Wk, bq, bk = lw["Wq"].copy(), lw["Wk"].copy(), lw["bq"].copy(), lw["bk"].copy()
         for h in range(wl.H):
-            first, second = slice(h * dh, h * dh + dh // 2), slice(h * dh + dh // 2, (h + 1) * dh)
-            Wq[:, second], bq[second] = 0.0, 0.0
-            Wk[:, first], bk[first] = 0.0, 0.0
-        lw["Wq"], lw["Wk"] = synth.round_bf16(Wq), synth.round_bf16(Wk)
-        lw["bq"], lw["bk"] = synth.round_bf16(bq), synth.round_bf16(bk)
+            f0, head = h * dh, slice(h * dh, (h + 1) * dh)
+            Wq[:, head], bq[head] = 0.0, 0.0
+            bq[f0] = beta
+            Wk[:, f0], bk[f0] = 0.0, sign * beta
+        lw["Wq"], lw["Wk"], lw["bq"], lw["bk"] = Wq, Wk, bq, bk
     return w
 
 
 # (workload, B): heads of 16 (d7), 32 (d11) and 64 (d11 geometry, d_model 128, 2 heads)
-UNDERFLOW_CASES = {
+RANGE_CASES = {
     "d7": (synth.WORKLOADS["d7"], 5),
     "d11": (synth.WORKLOADS["d11"], 5),
     "d11_dh64": (synth.Workload("d11_dh64", 11, 22, 3, 0.005, 0.0, 128, 2, 2, 4, synth.DTYPE_BF16), 3),
 }
 
 
-@pytest.mark.parametrize("name", list(UNDERFLOW_CASES))
-def test_attention_shift_underflow(name):
-    """The attention kernel shifts each query's scores by the Cauchy-Schwarz bound
-    |q'| max_k |k| and recomputes a query block with a running maximum when a row sum
-    underflows. With Q and K in orthogonal feature halves every score is 0, so softmax is
-    uniform, while the bound is far above 100 log2 units: every row sum underflows in fp32
-    (checked below for round 0, layer 0) and the results can only match the oracle through
-    the running-maximum path (head sizes 16, 32 and 64)."""
-    wl, B = UNDERFLOW_CASES[name]
+@pytest.mark.parametrize("sign", [1.0, -1.0], ids=["overflow", "underflow"])
+@pytest.mark.parametrize("name", list(RANGE_CASES))
+def test_attention_score_range(name, sign):
+    """The attention kernel exponentiates the scores without a shift and recomputes a query
+    block with a running maximum when its row sum or output leaves the normal fp32 range.
+    With every score equal to +-(at least 184) log2 units, exp2 overflows to inf (sign +1) or
+    underflows to 0 (sign -1) for every key: the results can only match the oracle's uniform
+    softmax through the running-maximum path (head sizes 16, 32 and 64)."""
+    wl, B = RANGE_CASES[name]
     base = weights(name) if name in synth.WORKLOADS else synth.make_weights(wl, seed=5)
-    w = orthogonal_qk_weights(wl, base)
+    w = constant_score_weights(wl, base, sign)
     meas, types = synth.make_windows(wl, B=B, seed=6)
-    # the bound on round 0, layer 0: X = kappa * Embed(E_0)
+    # the scores on round 0, layer 0 (X = kappa * Embed(E_0)): one value per head, beyond the
+    # exponent range of fp32 (and of bf16) in the direction of sign
     ev = O.detection_events(meas, types, wl.d)
     pe = O.positional_encoding((wl.d + 1) ** 2, wl.D)[O.grid_positions(wl.d)]
     X = w["kappa"] * O.embed(ev[:, 0, :], w, pe)
@@ -235,22 +239,22 @@ def test_attention_shift_underflow(name):
     Q, K = X @ lw["Wq"] + lw["bq"], X @ lw["Wk"] + lw["bk"]
     for h in range(wl.H):
         sl = slice(h * dh, (h + 1) * dh)
-        qn = np.linalg.norm(Q[:, :, sl], axis=-1) * math.log2(math.e) / math.sqrt(dh)
-        kmax = np.linalg.norm(K[:, :, sl], axis=-1).max(axis=1, keepdims=True)
-        assert np.abs(np.einsum("bnd,bmd->bnm", Q[:, :, sl], K[:, :, sl])).max() == 0.0
-        # every row: N * 2^(-bound) < 1e-30, the kernel's underflow test
-        assert (qn * kmax).min() > 100 + math.log2(wl.N), (h, (qn * kmax).min())
-    say(f"shift underflow {name} B={B}")
-    dec = pwdec.Decoder.from_workload(wl, w, max_windows=B)
-    logits, bits, rc = gpu_decode(dec, meas, types)
-    dec.close()
-    assert rc == pwdec.PWD_OK
-    assert np.isfinite(logits).all()
+        S = np.einsum("bnd,bmd->bnm", Q[:, :, sl], K[:, :, sl]) * math.log2(math.e) / math.sqrt(dh)
+        assert np.all(S == S.flat[0]) and sign * S.flat[0] > 180, (h, S.flat[0])
     o_logits, _ = O.forward_windows(meas, types, w, wl.d, wl.H)
-    err = np.abs(logits - o_logits)
-    say(f"  max |gpu - oracle| = {err.max():.3e}")
-    assert (err <= BF16_ATOL).all(), (logits, o_logits)
-    check_bits(bits, o_logits)
+    dec = pwdec.Decoder.from_workload(wl, w, max_windows=B)
+    # the layer-phased kernels, and for d7 the state-resident kernel (its own attention) too
+    for schedule in [pwdec.SCHEDULE_LAYERS] + ([pwdec.SCHEDULE_RESIDENT] if name == "d7" else []):
+        say(f"score range {name} sign={sign:+.0f} B={B} schedule={schedule}")
+        dec.schedule(schedule)
+        logits, bits, rc = gpu_decode(dec, meas, types)
+        assert rc == pwdec.PWD_OK
+        assert np.isfinite(logits).all()
+        err = np.abs(logits - o_logits)
+        say(f"  max |gpu - oracle| = {err.max():.3e}")
+        assert (err <= BF16_ATOL).all(), (logits, o_logits)
+        check_bits(bits, o_logits)
+    dec.close()
 
 
 def test_decoder_first_in_a_fresh_process():
