@@ -9,9 +9,11 @@
 // K as the A operand of S^T = K Q'^T, Q' = Q log2(e)/sqrt(dh) as its B operand, and V,
 // computed with the activations as the A operand (tokens as rows), as the A operand of
 // O^T = V^T P^T; the output O^T packs into the B operand of the out-projection. Attention is
-// local to the wavefront, with the exact row maximum (all 48 scores of a query are in
-// registers). Only the weights and the final state move through memory: one launch decodes
-// every round and layer, and the readout follows on the state it writes.
+// local to the wavefront. Softmax is shift-invariant, so the scores are exponentiated as they
+// are; a head whose row sums or outputs leave the normal fp32 range (possible only for scores
+// beyond about +-100 log2 units) is recomputed with the exact row maximum (all 48 scores of a
+// query are in registers). Only the weights and the final state move through memory: one
+// launch decodes every round and layer, and the readout follows on the state it writes.
 //
 // Four wavefronts (four windows) share one weight stream. The host lays each layer's weights
 // out in the order the kernel consumes them, and the workgroup pulls the stream through a
@@ -27,6 +29,8 @@
 #include "common.h"
 #include "kernels.h"
 #include "pipeline.h"
+
+#include <type_traits>
 
 namespace {
 
@@ -110,13 +114,14 @@ PWD_DEV bf16x4 to_b4(f32x4 v) {
 
 // Softmax over the window's keys for NP independent (query block, head) pairs at once, so that
 // their latencies overlap: scores s[p][kb] (keys 4g+i of key block kb as rows, this lane's
-// query as the column), exact row maximum, padding keys (index >= ntok, only ever in the last
-// block) excluded. The probabilities, rounded to bf16, go to pb (the P^T operand); inv gets 1 /
-// their column sum, taken on the matrix core from the same bf16 values (an A operand whose row 0
-// is all ones turns P^T into its column sums, in row 0 of the result).
-template <int NP, int TB>
-PWD_DEV void softmax_cols(f32x4 (&s)[NP][TB], bf16x4 (&pb)[NP][TB], float (&inv)[NP], int ntok, int g,
-                          bf16x4 ones) {
+// query as the column), padding keys (index >= ntok, only ever in the last block) excluded.
+// SHIFT: with the exact row maximum subtracted; otherwise exponentiated as they are. The
+// probabilities, rounded to bf16, go to pb (the P^T operand); sum gets their column sum, taken
+// on the matrix core from the same bf16 values (an A operand whose row 0 is all ones turns P^T
+// into its column sums, in row 0 of the result), in every lane of the column, and inv 1 / sum.
+template <bool SHIFT, int NP, int TB>
+PWD_DEV void softmax_cols(f32x4 (&s)[NP][TB], bf16x4 (&pb)[NP][TB], float (&sum)[NP], float (&inv)[NP], int ntok,
+                          int g, bf16x4 ones) {
     if (ntok < TB * 16) {   // wavefront-uniform: the last block holds padding keys
 #pragma unroll
         for (int p = 0; p < NP; ++p)
@@ -126,28 +131,52 @@ PWD_DEV void softmax_cols(f32x4 (&s)[NP][TB], bf16x4 (&pb)[NP][TB], float (&inv)
     }
     float mx[NP];
 #pragma unroll
-    for (int p = 0; p < NP; ++p) {
-        mx[p] = -INFINITY;
+    for (int p = 0; p < NP; ++p) mx[p] = 0.f;
+    if constexpr (SHIFT) {
 #pragma unroll
-        for (int kb = 0; kb < TB; ++kb)
-            mx[p] = fmaxf(mx[p], fmaxf(fmaxf(s[p][kb][0], s[p][kb][1]), fmaxf(s[p][kb][2], s[p][kb][3])));
+        for (int p = 0; p < NP; ++p) {
+            mx[p] = -INFINITY;
+#pragma unroll
+            for (int kb = 0; kb < TB; ++kb)
+                mx[p] = fmaxf(mx[p], fmaxf(fmaxf(s[p][kb][0], s[p][kb][1]), fmaxf(s[p][kb][2], s[p][kb][3])));
+        }
+#pragma unroll
+        for (int p = 0; p < NP; ++p) mx[p] = group_max(mx[p]);
     }
-#pragma unroll
-    for (int p = 0; p < NP; ++p) mx[p] = group_max(mx[p]);
     f32x4 ls[NP];
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
         ls[p] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kb = 0; kb < TB; ++kb) {
+            f32x4 e;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) s[p][kb][i] = __builtin_amdgcn_exp2f(s[p][kb][i] - mx[p]);
-            pb[p][kb] = to_b4(s[p][kb]);
+            for (int i = 0; i < 4; ++i) e[i] = __builtin_amdgcn_exp2f(SHIFT ? s[p][kb][i] - mx[p] : s[p][kb][i]);
+            pb[p][kb] = to_b4(e);
             ls[p] = mfma16x16x16(ones, pb[p][kb], ls[p]);
         }
     }
 #pragma unroll
-    for (int p = 0; p < NP; ++p) inv[p] = __builtin_amdgcn_rcpf(row0_broadcast(ls[p][0]));
+    for (int p = 0; p < NP; ++p) {
+        sum[p] = row0_broadcast(ls[p][0]);
+        inv[p] = __builtin_amdgcn_rcpf(sum[p]);
+    }
+}
+
+// True (wavefront-uniform) when every column sum lies in [1e-30, 2^126] and every output value
+// is finite (x * 0 is 0 for finite x and NaN otherwise): the unshifted softmax is then the exact
+// one up to rounding. Otherwise the caller recomputes with the row maximum subtracted.
+template <int NP>
+PWD_DEV bool in_range(const float (&sum)[NP], const f32x4 (&o)[NP]) {
+    bool ok = true;
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+        float chk = sum[p];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) chk = fmaf(o[p][i], 0.f, chk);
+        ok = ok && chk >= 1e-30f && chk <= 0x1p126f;
+    }
+    return __builtin_amdgcn_ballot_w64(!ok) == 0;
 }
 
 // LayerNorm over the d_model features of each token (biased variance, two passes) of the state
@@ -341,21 +370,26 @@ __global__ __launch_bounds__(RWAVES * 64, 1) void resident_kernel(ResidentParams
                             q4[hh][b] = to_b4(q[hh][b] * p.qscale);
                             k4[hh][b] = to_b4(k[hh][b]);
                         }
-                    f32x4 s[NP][TB];
-                    bf16x4 pb[NP][TB];
-                    float inv[NP];
-#pragma unroll
-                    for (int pp = 0; pp < NP; ++pp)
-#pragma unroll
-                        for (int kb = 0; kb < TB; ++kb) s[pp][kb] = mfma16x16x16(k4[pp % 2][kb], q4[pp % 2][pp / 2], zero);
-                    softmax_cols<NP, TB>(s, pb, inv, p.ntok, g, ones);
                     f32x4 o[NP];
+                    float inv[NP];
+                    auto attend = [&](auto shift) {
+                        f32x4 s[NP][TB];
+                        bf16x4 pb[NP][TB];
+                        float sum[NP];
 #pragma unroll
-                    for (int pp = 0; pp < NP; ++pp) {
-                        o[pp] = zero;
+                        for (int pp = 0; pp < NP; ++pp)
 #pragma unroll
-                        for (int kb = 0; kb < TB; ++kb) o[pp] = mfma16x16x16(vt[pp % 2][kb], pb[pp][kb], o[pp]);
-                    }
+                            for (int kb = 0; kb < TB; ++kb) s[pp][kb] = mfma16x16x16(k4[pp % 2][kb], q4[pp % 2][pp / 2], zero);
+                        softmax_cols<decltype(shift)::value, NP, TB>(s, pb, sum, inv, p.ntok, g, ones);
+#pragma unroll
+                        for (int pp = 0; pp < NP; ++pp) {
+                            o[pp] = zero;
+#pragma unroll
+                            for (int kb = 0; kb < TB; ++kb) o[pp] = mfma16x16x16(vt[pp % 2][kb], pb[pp][kb], o[pp]);
+                        }
+                        return in_range<NP>(sum, o);
+                    };
+                    if (!attend(std::false_type{})) attend(std::true_type{});
 #pragma unroll
                     for (int qb = 0; qb < TB; ++qb) y[qb] = pack_b(o[2 * qb] * inv[2 * qb], o[2 * qb + 1] * inv[2 * qb + 1]);
                 } else {   // one head of 32 features
@@ -365,25 +399,40 @@ __global__ __launch_bounds__(RWAVES * 64, 1) void resident_kernel(ResidentParams
                         qf[b] = pack_b(q[0][b] * p.qscale, q[1][b] * p.qscale);
                         kf[b] = pack_b(k[0][b], k[1][b]);
                     }
-                    f32x4 s[TB][TB];
-                    bf16x4 pb[TB][TB];
+                    f32x4 o[TB][2];
                     float inv[TB];
+                    auto attend = [&](auto shift) {
+                        f32x4 s[TB][TB];
+                        bf16x4 pb[TB][TB];
+                        float sum[TB];
 #pragma unroll
-                    for (int qb = 0; qb < TB; ++qb)
+                        for (int qb = 0; qb < TB; ++qb)
 #pragma unroll
-                        for (int kb = 0; kb < TB; ++kb) s[qb][kb] = mfma16x16x32(kf[kb], qf[qb], zero);
-                    softmax_cols<TB, TB>(s, pb, inv, p.ntok, g, ones);
+                            for (int kb = 0; kb < TB; ++kb) s[qb][kb] = mfma16x16x32(kf[kb], qf[qb], zero);
+                        softmax_cols<decltype(shift)::value, TB, TB>(s, pb, sum, inv, p.ntok, g, ones);
 #pragma unroll
-                    for (int qb = 0; qb < TB; ++qb) {
-                        f32x4 o[2];
+                        for (int qb = 0; qb < TB; ++qb)
 #pragma unroll
-                        for (int hh = 0; hh < 2; ++hh) {
-                            o[hh] = zero;
+                            for (int hh = 0; hh < 2; ++hh) {
+                                o[qb][hh] = zero;
 #pragma unroll
-                            for (int kb = 0; kb < TB; ++kb) o[hh] = mfma16x16x16(vt[hh][kb], pb[qb][kb], o[hh]);
-                        }
-                        y[qb] = pack_b(o[0] * inv[qb], o[1] * inv[qb]);
-                    }
+                                for (int kb = 0; kb < TB; ++kb) o[qb][hh] = mfma16x16x16(vt[hh][kb], pb[qb][kb], o[qb][hh]);
+                            }
+                        // both halves of each query block's output against its sum
+                        float sum2[2 * TB];
+                        f32x4 o2[2 * TB];
+#pragma unroll
+                        for (int qb = 0; qb < TB; ++qb)
+#pragma unroll
+                            for (int hh = 0; hh < 2; ++hh) {
+                                sum2[2 * qb + hh] = sum[qb];
+                                o2[2 * qb + hh] = o[qb][hh];
+                            }
+                        return in_range<2 * TB>(sum2, o2);
+                    };
+                    if (!attend(std::false_type{})) attend(std::true_type{});
+#pragma unroll
+                    for (int qb = 0; qb < TB; ++qb) y[qb] = pack_b(o[qb][0] * inv[qb], o[qb][1] * inv[qb]);
                 }
 
                 // out-projection k-step og: X += Wo[:, og]^T y (the residual is the state itself)
