@@ -190,22 +190,31 @@ def mxfp8_measurement(torch, pwdec, synth, names=("d7", "d11", "d25"), reps=3):
     return out
 
 
-def source_hash():
+# The sources each profiled stage's kernel is compiled from: its counter figures stay valid
+# while these files are unchanged, whatever happens to the other kernels.
+STAGE_SOURCES = {
+    "post_qkv": ("tok.hip", "common.h", "kernels.h", "pipeline.h"),
+    "attention": ("attn.hip", "common.h", "kernels.h"),
+}
+
+
+def source_hash(stage=None):
+    """Hash of the kernel sources of `stage` (STAGE_SOURCES), or of every source file."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2601_09921_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
+    for f in (STAGE_SOURCES[stage] if stage else sorted(os.listdir(csrc))):
         h.update(open(os.path.join(csrc, f), "rb").read())
     return h.hexdigest()[:16]
 
 
 def load_traffic(stage):
     """HBM bytes per launch of `stage` from committed rocprofv3 counter runs, or None when
-    they were taken on other kernel sources."""
+    they were taken on other sources of that stage's kernel."""
     try:
         t = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
         return None
-    if t.get("source_hash") != source_hash():
+    if stage not in STAGE_SOURCES or t.get("source_hashes", {}).get(stage) != source_hash(stage):
         return None
     return t.get("bytes_per_launch", {}).get(stage)
 

@@ -32,11 +32,35 @@ def test_stage_flops_closed_forms():
 
 def test_traffic_record_is_keyed_to_the_sources(monkeypatch):
     t = json.load(open(bench.TRAFFIC_FILE))
-    assert set(t) >= {"source_hash", "fetch_scale", "write_scale", "bytes_per_launch"}
-    monkeypatch.setattr(bench, "source_hash", lambda: t["source_hash"])
+    assert set(t) >= {"source_hashes", "fetch_scale", "write_scale", "bytes_per_launch"}
+    assert set(t["source_hashes"]) == set(bench.STAGE_SOURCES)
+    monkeypatch.setattr(bench, "source_hash", lambda stage=None: t["source_hashes"][stage])
     assert bench.load_traffic("post_qkv") == t["bytes_per_launch"].get("post_qkv")
-    monkeypatch.setattr(bench, "source_hash", lambda: "0" * 16)
+    # another stage's kernel sources changing leaves this stage's record valid
+    monkeypatch.setattr(bench, "source_hash",
+                        lambda stage=None: t["source_hashes"][stage] if stage == "post_qkv" else "0" * 16)
+    assert bench.load_traffic("post_qkv") == t["bytes_per_launch"].get("post_qkv")
+    assert bench.load_traffic("attention") is None
+    monkeypatch.setattr(bench, "source_hash", lambda stage=None: "0" * 16)
     assert bench.load_traffic("post_qkv") is None
+    assert bench.load_traffic("readout") is None
+
+
+def test_stage_hash_covers_the_kernel_sources(tmp_path, monkeypatch):
+    """source_hash(stage) changes with every file of that stage's kernel and with no other."""
+    import shutil
+    csrc = os.path.join(ROOT, "paper_2601_09921_amd", "csrc")
+    root = tmp_path / "r"
+    shutil.copytree(csrc, root / "paper_2601_09921_amd" / "csrc")
+    monkeypatch.setattr(bench, "ROOT", str(root))
+    before = {k: bench.source_hash(k) for k in bench.STAGE_SOURCES}
+    with open(root / "paper_2601_09921_amd" / "csrc" / "resident.hip", "a") as f:
+        f.write("// edit\n")
+    assert {k: bench.source_hash(k) for k in bench.STAGE_SOURCES} == before
+    with open(root / "paper_2601_09921_amd" / "csrc" / "attn.hip", "a") as f:
+        f.write("// edit\n")
+    after = {k: bench.source_hash(k) for k in bench.STAGE_SOURCES}
+    assert after["post_qkv"] == before["post_qkv"] and after["attention"] != before["attention"]
 
 
 def test_more_than_one_gpu_is_refused():
