@@ -67,5 +67,26 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+def build_host_asan(verbose: bool = False) -> str:
+    """The library with the host code of pwdec.cpp (configuration checks, blob parser, handle
+    logic) instrumented by AddressSanitizer and the device code unchanged, linked from the
+    kernels' objects of build() into _build/libpwdec_asan.so for the host checks in
+    tests/asan. Builds the kernels' objects first if they are missing."""
+    objdir = os.path.join(HERE, "_build")
+    kernels = [os.path.join(objdir, src + ".o") for src in SOURCES if src != "pwdec.cpp"]
+    if not all(os.path.exists(o) for o in kernels):
+        build(verbose)
+    obj = os.path.join(objdir, "pwdec.cpp.asan.o")
+    sanitize = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fno-omit-frame-pointer"]
+    _finish(_run([hipcc(), *HIPCC_FLAGS, *sanitize, "-x", "hip", "-c", os.path.join(CSRC, "pwdec.cpp"), "-o", obj],
+                 verbose))
+    out = os.path.join(objdir, "libpwdec_asan.so")
+    rocm_lib = os.path.join(os.path.dirname(os.path.dirname(hipcc())), "lib")
+    link = ["g++", "-shared", "-fsanitize=address", *kernels, obj, f"-L{rocm_lib}", "-lamdhip64",
+            f"-Wl,-rpath,{rocm_lib}", "-o", out]
+    _finish(_run(link, verbose))
+    return out
+
+
 if __name__ == "__main__":
     print(build(verbose=True))
