@@ -455,13 +455,22 @@ hipError_t launch_shape(const AttnParams& p, int nwin, hipStream_t s) {
 
 template <int DH>
 hipError_t launch_dh(const AttnParams& p, int nwin, hipStream_t s) {
-    // wavefronts per (window, head): enough for a pass of QMAX query blocks each, at most
-    // four, so small windows run as many small workgroups rather than idle wavefronts
+    // Wavefronts per (window, head). Heads of 16 and 32 (four query blocks per pass): as few
+    // as keep two wavefronts per SIMD (8 per CU, the register limit) across the workgroups
+    // whose tiles fit a CU's 160 KB of LDS, so that as many items as possible are in flight to
+    // cover each other's K/V copies -- one where eight or more tiles fit (d11: 17 KB), two
+    // where four do (d17: 37 KB, 9 % faster than four wavefronts; 168 tokens: 12 %), four for
+    // two 79 KB tiles (d25). Heads of 64 (two query blocks per pass): enough wavefronts for a
+    // pass each, at most four (two per item measured 8 % slower at 120 tokens). Either way a
+    // tile above 80 KB leaves room for one workgroup, which gets eight wavefronts, and a
+    // window of at most QMAX query blocks takes one.
     constexpr int QM = Frag<DH>::QMAX;
+    const size_t tile = attn_smem_bytes(DH, p.Npad, p.nbw);
+    const int fit = (int)(160 * 1024 / tile);
     if (p.nbw <= QM) return launch_shape<DH, 1>(p, nwin, s);
-    if (p.nbw <= 2 * QM) return launch_shape<DH, 2>(p, nwin, s);
-    // a tile above 80 KB leaves room for one workgroup per CU: give it 8 wavefronts
-    if (ATTN_WIDE && attn_smem_bytes(DH, p.Npad, p.nbw) > 80 * 1024) return launch_shape<DH, 8>(p, nwin, s);
+    if (QM >= 4 && fit >= 8) return launch_shape<DH, 1>(p, nwin, s);
+    if (QM >= 4 ? fit >= 4 : p.nbw <= 2 * QM) return launch_shape<DH, 2>(p, nwin, s);
+    if (ATTN_WIDE && tile > 80 * 1024) return launch_shape<DH, 8>(p, nwin, s);
     return launch_shape<DH, 4>(p, nwin, s);
 }
 
