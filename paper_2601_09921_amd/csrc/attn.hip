@@ -21,8 +21,9 @@
 // denominator use the same bf16 probabilities and the VALU is left to the exponentials. The
 // output is written as the B fragments the out-projection consumes.
 //
-// One workgroup of 1, 2 or 4 wavefronts (by window size) per item, two workgroups per CU:
-// while one copies its K/V, the other keeps the SIMDs busy.
+// One workgroup of 1, 2, 4 or 8 wavefronts per item, as many workgroups per CU as their K/V
+// tiles fit in LDS (two wavefronts per SIMD in all): while some copy their K/V, the others
+// keep the SIMDs busy.
 #include "common.h"
 #include "kernels.h"
 
@@ -397,8 +398,9 @@ PWD_DEV void attn_passes(const AttnShape& sh, const AttnItem& it, int qbeg, int 
     if (qend - qb == 1) run(std::integral_constant<int, 1>{}, qb);
 }
 
-// One workgroup per (window, head); K/V stay in LDS for the whole item. Up to 4 wavefronts
-// two workgroups share a CU; 8 wavefronts (tiles above 80 KB) keep two per SIMD on their own.
+// One workgroup per (window, head); K/V stay in LDS for the whole item. Workgroups of up to 4
+// wavefronts share a CU (as many as their tiles fit in LDS); 8 wavefronts (tiles above 80 KB)
+// keep two per SIMD on their own.
 // Heads of 16 share their K/V fragments with the neighbouring head, so a workgroup stages
 // the fragments once and runs both heads of the pair in turn.
 template <int DH>
