@@ -4,6 +4,7 @@ Small batches (several token tiles and a ragged tail) compare every window; at t
 batch sizes of each workload, windows the oracle can afford are compared one by one and
 the rest are checked through batch invariance and output consistency."""
 import copy
+import dataclasses
 import ctypes
 import math
 import os
@@ -119,6 +120,34 @@ def test_zero_syndromes(name):
         assert (sel.view(np.uint32) == sel.view(np.uint32)[0]).all()
     o_logits, _, _ = oracle(name, B, zero=True)
     check_logits(name, logits, o_logits)
+
+
+DENSE_CASES = [("d3", 0.5), ("d3", 1.0), ("d7", 0.5), ("d7", 1.0), ("d11", 0.5), ("d11", 1.0), ("d25", 1.0)]
+
+
+@pytest.mark.parametrize("name,p", DENSE_CASES, ids=[f"{n}_p{p}" for n, p in DENSE_CASES])
+def test_dense_syndromes(name, p):
+    """The other end from zero syndromes: every stabilizer flips with probability 1/2, or in
+    every round (detection events in every unmasked position, 83 % of them), so the embedding
+    and the recurrent state are far from the sparse regime of the workloads. Against the oracle
+    (three windows at d25, one of each type), through the default schedule and, where the
+    decoder has another, the layer-phased one."""
+    wl = dataclasses.replace(synth.WORKLOADS[name], p=p, pair_p=0.0)
+    B = 3 if name == "d25" else 6
+    meas, types = synth.make_windows(wl, seed=77, B=B)
+    o_logits, _ = O.forward_windows(meas, types, weights(name), wl.d, wl.H)
+    dec = decoder(name, max(B, SMALL[name]))
+    for schedule in (pwdec.SCHEDULE_AUTO, pwdec.SCHEDULE_LAYERS):
+        try:
+            dec.schedule(schedule)
+        except pwdec.PwdError:
+            continue
+        say(f"dense syndromes {name} p={p} schedule={schedule}")
+        logits, bits, rc = gpu_decode(dec, meas, types)
+        assert rc == pwdec.PWD_OK
+        check_logits(name, logits, o_logits)
+        check_bits(bits, o_logits)
+    dec.schedule(pwdec.SCHEDULE_AUTO)
 
 
 @pytest.mark.parametrize("name", ["d3", "d7"])
