@@ -219,6 +219,24 @@ def load_traffic(stage):
     return t.get("bytes_per_launch", {}).get(stage)
 
 
+# v_exp_f32 issues at half the VALU rate: 8 cycles per 64-lane instruction on each of the 1024
+# SIMDs at the 2.4 GHz the dense peaks assume.
+EXP_PEAK_PER_S = 1024 * 64 / 8 * 2.4e9
+
+
+def attention_bound(st, wl, B, peak):
+    """The attention launch against both pipes it uses: its MFMA work as a fraction of the dense
+    bf16 peak and its exponentials (one per score, H N^2 per window) as a fraction of the
+    transcendental issue rate. On gfx950 a SIMD's exponentials and MFMAs barely overlap, so the
+    sum of the two fractions is the launch's share of its bound."""
+    exps = B * wl.H * wl.N * wl.N
+    exp_frac = exps / (st["avg_ms"] * 1e-3) / EXP_PEAK_PER_S
+    mfma_frac = st["tflops"] / peak
+    return {"kernel": st["kernel"], "mfma_frac": round(mfma_frac, 4), "exp_per_launch": exps,
+            "exp_per_s": exps / (st["avg_ms"] * 1e-3), "exp_peak_per_s": EXP_PEAK_PER_S,
+            "exp_frac": round(exp_frac, 4), "sum": round(mfma_frac + exp_frac, 4)}
+
+
 def stream_measurement(dec, wl, torch, pwdec, synth):
     """One decode_stream of a memory experiment as long as the batch (B windows of d rounds,
     the last one ragged): on-device windowing, decoding and XOR / soft-XOR combination."""
@@ -508,6 +526,8 @@ def main():
             "traffic": load_traffic(dom),
         },
     }
+    if bf16 and "attention" in stage_stats:
+        out["attention_bound"] = attention_bound(stage_stats["attention"], wl, B, peak)
     out["input_stage"] = input_stage_measurement(dec, wl, torch, dev_meas, dev_types)
     out["env"] = environment(torch)
     if not args.no_stream:

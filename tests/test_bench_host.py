@@ -63,6 +63,18 @@ def test_stage_hash_covers_the_kernel_sources(tmp_path, monkeypatch):
     assert after["post_qkv"] == before["post_qkv"] and after["attention"] != before["attention"]
 
 
+def test_attention_bound():
+    """Exponentials per launch are one per score (H N^2 per window); the exponential peak is
+    1024 SIMDs x 64 lanes per 8 cycles at 2.4 GHz; the two fractions add up."""
+    wl = synth.WORKLOADS["d25"]
+    st = {"kernel": "attn_kernel<32, 4>", "avg_ms": 4.0, "tflops": 800.0}
+    b = bench.attention_bound(st, wl, wl.B, 2500.0)
+    assert b["exp_per_launch"] == wl.B * 8 * 624 * 624
+    assert abs(b["exp_peak_per_s"] - 19.6608e12) < 1e6
+    assert abs(b["exp_frac"] - b["exp_per_launch"] / 4e-3 / 19.6608e12) < 1e-4
+    assert b["mfma_frac"] == 0.32 and abs(b["sum"] - (b["mfma_frac"] + b["exp_frac"])) < 1e-4
+
+
 def test_more_than_one_gpu_is_refused():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
                        capture_output=True, text=True, timeout=120, cwd=ROOT)
