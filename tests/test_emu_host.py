@@ -81,18 +81,34 @@ def _kslot(g, i):
     return 4 * g + i if i < 4 else 16 + 4 * g + (i - 4)
 
 
-@pytest.mark.parametrize("N,D,H", [(8, 256, 8), (24, 256, 8), (80, 256, 8), (120, 256, 8), (48, 128, 8), (48, 256, 4)])
-def test_attention_kernel_alone(emu, N, D, H):
+ATTN_CASES = [(8, 256, 8, "normal"), (24, 256, 8, "normal"), (80, 256, 8, "normal"), (120, 256, 8, "normal"),
+              (48, 128, 8, "normal"), (48, 256, 4, "normal"),
+              (120, 256, 8, "overflow"), (48, 128, 8, "overflow"), (48, 256, 4, "underflow"), (80, 256, 8, "underflow")]
+
+
+@pytest.mark.parametrize("N,D,H,scores", ATTN_CASES, ids=[f"N{c[0]}_D{c[1]}_H{c[2]}_{c[3]}" for c in ATTN_CASES])
+def test_attention_kernel_alone(emu, N, D, H, scores):
     """One window: Q (pre-scaled by log2(e)/sqrt(dh)), K, V written in the Q/K/V projection's
     fragment layouts; the kernel's output against softmax attention in float64 on the same
     bf16 values (heads of 16 run in pairs, 64 in two fragments; N = 80 and 120 run two and
-    two wavefronts with padding keys)."""
+    two wavefronts with padding keys). The kernel exponentiates unshifted scores; "overflow"
+    scales Q so that rows reach hundreds of log2 units (exp2 overflows to inf), "underflow"
+    gives every head's Q and K opposite shared components so that every score is below -150
+    (every exp2 underflows): both go through the running-maximum recomputation."""
     dh, npad = D // H, (N + 15) // 16 * 16
     nbw, ksd = npad // 16, D // 32
     rng = np.random.default_rng(N * 1000 + D + H)
     c = np.log2(np.e) / np.sqrt(dh)
-    Qb = _bf16(rng.standard_normal((npad, D)) * c)
-    Kb = _bf16(rng.standard_normal((npad, D)))
+    q = rng.standard_normal((npad, D)) * c
+    k = rng.standard_normal((npad, D))
+    if scores == "overflow":
+        q *= 40.0
+    elif scores == "underflow":
+        u = np.zeros(D)
+        u[::dh] = 1.0                       # the first feature of every head
+        q, k = q + 24.0 * u, k - 24.0 * u
+    Qb = _bf16(q)
+    Kb = _bf16(k)
     Vb = _bf16(rng.standard_normal((npad, D)))
     buf = np.zeros((nbw, 3, ksd, 64, 8), np.uint16)
     lane = np.arange(64)
@@ -120,13 +136,18 @@ def test_attention_kernel_alone(emu, N, D, H):
                 feat = f * 32 + np.array([_kslot(g, i) for g in lane // 16])
                 out[tb * 16 + lane % 16, feat] = _f32(Y[tb, f, :, i])
     ref = np.zeros((N, D))
+    extreme = 0
     for h in range(H):
         sl = slice(h * dh, (h + 1) * dh)
         S = _f32(Qb[:N, sl]).astype(np.float64) @ _f32(Kb[:N, sl]).astype(np.float64).T
+        extreme += int((S.max(1) > 128).sum() + (S.max(1) < -130).sum())
         P = np.exp2(S - S.max(1, keepdims=True))
         ref[:, sl] = (P / P.sum(1, keepdims=True)) @ _f32(Vb[:N, sl])
     assert emu.emu_errors() == 0
+    assert np.isfinite(out[:N]).all()
     assert np.abs(out[:N] - ref).max() < 1e-2
+    # the cases meant to leave the unshifted range do (rows whose largest score is beyond it)
+    assert (extreme > 0) == (scores != "normal"), extreme
 
 
 def _case(d, W, B, D, L, H, r, dil=(), grid=False, seed_base=1100):
