@@ -1009,6 +1009,16 @@ __global__ __launch_bounds__(256, 2) void conv_kernel(ConvParams p) {
     };
     using I0 = std::integral_constant<int, 0>;
     using I1 = std::integral_constant<int, 1>;
+    // the residual X of the workgroup's tokens, loaded during the last tap (D = 128: into the
+    // registers the first two gather slots free by then) or at the end
+    f32x4 xold[RT][TB];
+    auto load_x = [&]() {
+#pragma unroll
+        for (int b = 0; b < TB; ++b)
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt)
+                xold[rt][b] = ld_stream(reinterpret_cast<const f32x4*>(p.X + (((tb0 + b) * RT + rt) * 64 + lane) * 4));
+    };
     if constexpr (NSLOT == 3) {
         static_assert(TAP_CHUNKS == 1, "one chunk per tap");
         constexpr int LAST = WeightPipe<CHUNK, WAVES>::template last_load_read<CHUNK, LA>();
@@ -1023,6 +1033,8 @@ __global__ __launch_bounds__(256, 2) void conv_kernel(ConvParams p) {
                   std::integral_constant<int, YOUNGER>{}, T, [&](int r) {
                       if constexpr (T + 2 < 9)
                           if (r == LAST) gather(std::integral_constant<int, (T + 2) % 3>{}, T + 2);
+                      if constexpr (T == 8)
+                          if (r == 0) load_x();   // after the last sync: no chunk waits for these
                   });
         });
     } else {
@@ -1034,6 +1046,7 @@ __global__ __launch_bounds__(256, 2) void conv_kernel(ConvParams p) {
                 chunk(std::integral_constant<int, C & 1>{}, c, I0{}, I0{}, tap * TAP_CHUNKS + C, [](int) {});
             });
         }
+        load_x();
     }
 
     // X += ReLU(acc); the output's B fragments for the next unit
@@ -1045,7 +1058,7 @@ __global__ __launch_bounds__(256, 2) void conv_kernel(ConvParams p) {
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 f32x4* px = reinterpret_cast<f32x4*>(p.X + (((tb0 + b) * RT + 2 * ks + h) * 64 + lane) * 4);
-                xo[h] = ld_stream(px) + relu4(acc[2 * ks + h][b]);
+                xo[h] = xold[2 * ks + h][b] + relu4(acc[2 * ks + h][b]);
                 st_stream(px, xo[h]);
             }
             if constexpr (GOUT)
