@@ -130,3 +130,28 @@ def test_dilated_stream_and_stage_profile():
     ol, _ = O.forward_windows(meas, types, w, wl.d, wl.H, grid=True)
     assert (np.abs(wlog.cpu().numpy() - ol) <= BF16_ATOL).all()
     assert int(bit.item()) == O.combine_bits(wbits.cpu().numpy())
+
+
+def test_dilated_large_batch():
+    """conv_kernel<128> over a batch as large as the hardware holds at once, several times over:
+    the d = 25 grid (676 tokens, 43 blocks per window), 300 windows of 25 rounds, i.e. 12,900
+    token blocks in 1,613 workgroup tiles, 202 per XCD. Sampled windows against the oracle (the
+    first, the last, and the two around the boundary of the first XCD's run of tiles), and every
+    window's logits bit-identical to a decode of the batch without its first 7 windows, whose
+    tiles fall to other workgroups and XCDs."""
+    wl = workload(25, 25, 300, 128, 1, 8, 5, BF16, True, (1, 2, 4))
+    w = synth.make_weights(wl, seed=1106)
+    meas, types = synth.make_windows(wl, seed=1107, realistic_boundaries=False)
+    say("dilated conv, large batch: d25 W25 B300 D128")
+    dec = pwdec.Decoder.from_workload(wl, w, max_windows=wl.B)
+    logits, bits, rc = gpu_decode(dec, meas, types)
+    assert rc == pwdec.PWD_OK
+    sub, _, rc = gpu_decode(dec, meas[7:], types[7:])
+    assert rc == pwdec.PWD_OK
+    dec.close()
+    assert np.array_equal(sub.view(np.uint32), logits[7:].view(np.uint32))
+    idx = [0, 37, 38, 299]
+    o_logits, _ = O.forward_windows(meas[idx], types[idx], w, wl.d, wl.H, grid=True)
+    say(f"  max |gpu - oracle| on windows {idx} = {np.abs(logits[idx] - o_logits).max():.3e}")
+    assert within(logits[idx], o_logits, BF16)
+    check_bits(bits[idx], o_logits)
