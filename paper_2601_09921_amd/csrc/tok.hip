@@ -109,6 +109,13 @@ PWD_DEV void st_stream(T* p, T v) {
     if constexpr (TOK_NT) __builtin_nontemporal_store(v, p);
     else *p = v;
 }
+// The token-major copy G of the dilated convolutions' input is stored through L2 (plain
+// stores): one store instruction covers one k-step of 16 tokens, i.e. the 64-byte halves of 16
+// 128-byte lines, whose other halves the next instruction writes. Through L2 the halves of a
+// line combine before write-back; non-temporal stores sent them to memory separately (46 % more
+// bytes written than G holds, and the out-projection launch that writes G 14 % slower).
+template <typename T>
+PWD_DEV void st_l2(T* p, T v) { *p = v; }
 
 PWD_DEV bf16x8 ldfrag(const uint16_t* __restrict__ base, int64_t frag, int lane) {
     const u16x8 v = ld_stream(reinterpret_cast<const u16x8*>(base + (frag * 64 + lane) * 8));
@@ -509,7 +516,7 @@ __global__ __launch_bounds__((tok_waves<D, FLAGS>() * 64), 2) void tok_kernel(To
         for (int b = 0; b < TB; ++b)
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks)
-                st_stream(reinterpret_cast<u16x8*>(p.G + ((((tb0 + b) * 16 + col) * KS + ks) * 4 + g) * 8),
+                st_l2(reinterpret_cast<u16x8*>(p.G + ((((tb0 + b) * 16 + col) * KS + ks) * 4 + g) * 8),
                           __builtin_bit_cast(u16x8, pack_b(x[2 * ks][b], x[2 * ks + 1][b])));
     }
     if constexpr (DO_FFN) {
@@ -1062,7 +1069,7 @@ __global__ __launch_bounds__(256, 2) void conv_kernel(ConvParams p) {
                 st_stream(px, xo[h]);
             }
             if constexpr (GOUT)
-                st_stream(reinterpret_cast<u16x8*>(p.Gout + ((((tb0 + b) * 16 + col) * KS + ks) * 4 + g) * 8),
+                st_l2(reinterpret_cast<u16x8*>(p.Gout + ((((tb0 + b) * 16 + col) * KS + ks) * 4 + g) * 8),
                           __builtin_bit_cast(u16x8, pack_b(xo[0], xo[1])));
         }
     // the last chunk's reload into the idle buffer lands before the LDS is freed
